@@ -1,0 +1,182 @@
+/*
+ * attt.h -- C ABI of the aTTT in-episode update step on AMD Instinct MI355X (gfx950).
+ *
+ * "No Time Like the Present: Agentic Test-Time Training for LLM Agents" (arXiv 2607.03441).
+ * One aTTT update (Algorithm 1) takes the new update text x_k, the episode's token history
+ * H^tok_k (the concatenation of its previous updates), the n-gram size n and the weight
+ * floor w_min, weights every token of x_k by its n-gram exposure (Eq. 8-9) and takes a
+ * gradient step on the token-weighted next-token loss (Eq. 10) of an episode-specific
+ * LoRA adapter. This library computes the data-parallel part of that step on one GPU:
+ *
+ *   attt_ngram_weights        exposure f and weights w of every update token (Eq. 8-9)
+ *   attt_weighted_ce_fwd_bwd  weighted CE through the frozen LM head, loss and dL/dh (Eq. 10)
+ *   attt_lora_grad            LoRA dA / dB of the adapted projections (Sec. 3.1, Appendix C)
+ *
+ * Conventions shared by every call
+ *   - Data pointers are device pointers unless a parameter says "host". The caller owns all
+ *     memory; the library never allocates device memory, frees memory or synchronises the
+ *     stream in these calls. Scratch space comes from the caller's `workspace`, whose size is
+ *     given by the matching *_workspace_size query (any larger size is fine). The workspace
+ *     must be 256-byte aligned; its contents need not be initialised and are garbage after.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t passed as void*; NULL is the
+ *     null stream). Outputs are valid once the stream reaches that point.
+ *   - Arguments are validated on the host before any HIP call, so ATTT_EINVAL and
+ *     ATTT_ENOSPACE come back without touching the device. A failing launch returns
+ *     ATTT_EHIP. attt_last_error() gives a message for the last failing call of this thread.
+ *   - Matrices are dense row-major with the leading dimension equal to the row length, and
+ *     must be 16-byte aligned. Floating-point dtypes: ATTT_F32 (float) or ATTT_BF16
+ *     (bfloat16, accumulated in float32).
+ *   - Calls are reentrant; concurrent calls must use distinct workspaces. Results are
+ *     bitwise reproducible for identical inputs on the same device (ordered reductions,
+ *     integer atomics only).
+ */
+#ifndef ATTT_H_
+#define ATTT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t attt_status;
+#define ATTT_OK 0
+#define ATTT_EINVAL 1       /* an argument is out of range, misaligned or inconsistent        */
+#define ATTT_ENOSPACE 2     /* workspace smaller than the size query returned                 */
+#define ATTT_EUNSUPPORTED 3 /* valid by the paper but beyond this build's limits (see below)  */
+#define ATTT_EHIP 4         /* the HIP runtime reported an error while launching              */
+
+#define ATTT_F32 0
+#define ATTT_BF16 1
+
+#define ATTT_NGRAM_MAX_N 16  /* largest n-gram size accepted                                   */
+#define ATTT_LORA_MAX_RANK 64
+
+const char* attt_status_string(attt_status status);
+/* Message of the last failing call on the calling thread ("" if none). */
+const char* attt_last_error(void);
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t attt_version(void);
+
+/* --------------------------------------------------------------------------------------
+ * n-gram exposure and token weights (Sec. 3.3, Eq. 8-9; the weighting loop of Algorithm 1)
+ *
+ * For each of E episodes, history e is H^tok_k: the flat concatenation of the token ids
+ * of that episode's previous updates. n-grams that straddle two previous updates count,
+ * and occurrences overlap (every start position counts). For every position j of the
+ * episode's update x_k:
+ *     f(j) = max over the n-grams g of x_k that contain j of count(g, H^tok_k)
+ *            (0 when no n-gram of x_k contains j, i.e. when L < n)
+ *     w(j) = max(w_min, 1 / (1 + f(j)))   in float32, round to nearest even
+ * Repeats of an n-gram inside x_k itself are not counted (only H^tok_k is).
+ *
+ * history          device int32 [history_offsets[E]]: all histories, back to back
+ * history_offsets  HOST int64 [E+1]: history e is history[history_offsets[e] .. [e+1])
+ * tokens           device int32 [token_offsets[E]]: all update texts x_k, back to back
+ * token_offsets    HOST int64 [E+1]
+ * num_episodes     E >= 1
+ * n                1 <= n <= ATTT_NGRAM_MAX_N
+ * w_min            weight floor, 2^-20 <= w_min <= 1 (the paper uses 0.05)
+ * exposure         device uint32 [T] or NULL: f per update token (T = token_offsets[E])
+ * weights          device float [T]: w per update token
+ * Token ids are compared for equality only; any int32 value is allowed. Offsets must start
+ * at 0 and be non-decreasing; each episode may hold up to 2^31 - 1 history tokens.
+ * ------------------------------------------------------------------------------------ */
+attt_status attt_ngram_workspace_size(const int64_t* history_offsets, const int64_t* token_offsets,
+                                      int32_t num_episodes, int32_t n, size_t* bytes);
+attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_offsets,
+                               const int32_t* tokens, const int64_t* token_offsets,
+                               int32_t num_episodes, int32_t n, float w_min,
+                               uint32_t* exposure, float* weights,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * Token-weighted next-token cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10;
+ * the gradient of the weighted loss in Algorithm 1), forward and backward.
+ *
+ * Row t of `hidden` is the hidden state that predicts token labels[t]; weights[t] is that
+ * token's weight w. Rows are grouped into E episodes by row_offsets; episode e has
+ * L_e = row_offsets[e+1] - row_offsets[e] rows and
+ *     z_t    = W h_t                                   (logits, never written to memory)
+ *     lse_t  = log sum_v exp(z_tv)
+ *     loss_e = (1 / L_e) sum_{t in e} w_t (lse_t - z_{t, labels[t]})
+ *     dL/dh_t = (w_t / L_e) (softmax(z_t) - onehot(labels[t])) W
+ * Natural log, full softmax over V, no bias, no label smoothing; the head gets no gradient.
+ *
+ * hidden       device [N, d] of dtype
+ * lm_head      device [V, d] of dtype (the nn.Linear weight layout)
+ * labels       device int32 [N], each in [0, V) (not checked on the device)
+ * weights      device float [N]
+ * row_offsets  HOST int64 [E+1], from 0 to N, non-decreasing; NULL means one episode of N rows
+ * num_episodes E >= 1
+ * N, d, V      N >= 0, 1 <= d with d % 8 == 0, 1 <= V < 2^31
+ * dtype        ATTT_F32 or ATTT_BF16
+ * loss         device float [E]
+ * lse          device float [N] or NULL
+ * grad_hidden  device [N, d] of dtype, or NULL for the forward only
+ * The workspace query takes want_grad = (grad_hidden != NULL).
+ * ------------------------------------------------------------------------------------ */
+attt_status attt_ce_workspace_size(int64_t N, int64_t d, int64_t V, int32_t dtype, int32_t want_grad,
+                                   size_t* bytes);
+attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* lm_head, const int32_t* labels,
+                                     const float* weights, const int64_t* row_offsets,
+                                     int32_t num_episodes, int64_t N, int64_t d, int64_t V,
+                                     int32_t dtype, float* loss, float* lse, void* grad_hidden,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * LoRA adapter gradients (episode-specific adapter, Sec. 3.1; rank and alpha, Appendix C).
+ *
+ * An adapted projection computes y = x W0^T + scale * (x A^T) B^T, scale = alpha / rank.
+ * Given its input x and the upstream gradient dy = dL/dy, with U = x A^T:
+ *     dB += scale * dy^T U          dA += (scale * dy B)^T x
+ * Both outputs are float32 and accumulated into (+=), so several micro-batches can share
+ * one gradient buffer; zero them first for a plain gradient.
+ *
+ * problems   HOST array of `count` descriptors, processed as one grouped launch:
+ *   x      device [rows, d_in]  of dtype
+ *   dy     device [rows, d_out] of dtype
+ *   A      device [rank, d_in]  of dtype
+ *   B      device [d_out, rank] of dtype
+ *   dA     device float [rank, d_in]   (+=)
+ *   dB     device float [d_out, rank]  (+=)
+ *   rows >= 0, d_in and d_out >= 1 and multiples of 8, 1 <= rank <= ATTT_LORA_MAX_RANK
+ *   Outputs of different problems must not overlap.
+ * ------------------------------------------------------------------------------------ */
+typedef struct attt_lora_problem {
+  const void* x;
+  const void* dy;
+  const void* A;
+  const void* B;
+  float* dA;
+  float* dB;
+  int64_t rows;
+  int64_t d_in;
+  int64_t d_out;
+  int32_t rank;
+  float scale;
+} attt_lora_problem;
+
+attt_status attt_lora_workspace_size(const attt_lora_problem* problems, int32_t count, int32_t dtype,
+                                     size_t* bytes);
+attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t count, int32_t dtype,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * Kernel timing (diagnostics). When enabled, every launch of a named kernel is bracketed
+ * by HIP events recorded on the launch stream. attt_timing_read waits for those events and
+ * returns the summed duration and launch count of one kernel since the last reset; names
+ * are those attt_timing_kernel_name enumerates. Not thread-safe against concurrent calls.
+ * ------------------------------------------------------------------------------------ */
+attt_status attt_timing_enable(int32_t on);
+attt_status attt_timing_reset(void);
+attt_status attt_timing_read(const char* kernel, double* total_ms, int64_t* launches);
+/* Name of kernel number i (0-based), or NULL past the last one. */
+const char* attt_timing_kernel_name(int32_t i);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTT_H_ */

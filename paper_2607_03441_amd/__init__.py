@@ -1,0 +1,280 @@
+"""Python binding of libattt.so, the gfx950 library of the aTTT in-episode update step
+(arXiv 2607.03441: n-gram token weights, Eq. 8-9; weighted LM-head cross-entropy, Eq. 10;
+LoRA adapter gradients).
+
+This module only marshals arguments: torch tensors provide device memory and the current
+HIP stream, and every step runs in the library's HIP kernels. There is no fallback: if the
+library is not built, every call raises.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_workspace_size",
+           "weighted_ce_fwd_bwd", "ce_workspace_size", "lora_grad", "lora_workspace_size",
+           "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
+           "F32", "BF16", "LoraProblem"]
+
+F32 = 0
+BF16 = 1
+OK, EINVAL, ENOSPACE, EUNSUPPORTED, EHIP = range(5)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+
+class AtttError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"attt status {status}: {message}")
+        self.status = status
+
+
+class LoraProblem(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("dy", ctypes.c_void_p), ("A", ctypes.c_void_p),
+                ("B", ctypes.c_void_p), ("dA", ctypes.c_void_p), ("dB", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64),
+                ("rank", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+def lib_path():
+    return os.path.join(_HERE, "libattt.so")
+
+
+def load():
+    """Load libattt.so (built in-tree by __graft_entry__.build()). Raises if it is missing."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(path)
+    i32, i64, f32, vp, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+    p64 = ctypes.POINTER(ctypes.c_int64)
+    psz = ctypes.POINTER(ctypes.c_size_t)
+    L.attt_status_string.restype = ctypes.c_char_p
+    L.attt_status_string.argtypes = [i32]
+    L.attt_last_error.restype = ctypes.c_char_p
+    L.attt_last_error.argtypes = []
+    L.attt_version.restype = i32
+    L.attt_version.argtypes = []
+    L.attt_ngram_workspace_size.restype = i32
+    L.attt_ngram_workspace_size.argtypes = [p64, p64, i32, i32, psz]
+    L.attt_ngram_weights.restype = i32
+    L.attt_ngram_weights.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp, sz, vp]
+    L.attt_ce_workspace_size.restype = i32
+    L.attt_ce_workspace_size.argtypes = [i64, i64, i64, i32, i32, psz]
+    L.attt_weighted_ce_fwd_bwd.restype = i32
+    L.attt_weighted_ce_fwd_bwd.argtypes = [vp, vp, vp, vp, p64, i32, i64, i64, i64, i32, vp, vp, vp,
+                                           vp, sz, vp]
+    L.attt_lora_workspace_size.restype = i32
+    L.attt_lora_workspace_size.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, psz]
+    L.attt_lora_grad.restype = i32
+    L.attt_lora_grad.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, vp, sz, vp]
+    L.attt_timing_enable.restype = i32
+    L.attt_timing_enable.argtypes = [i32]
+    L.attt_timing_reset.restype = i32
+    L.attt_timing_reset.argtypes = []
+    L.attt_timing_read.restype = i32
+    L.attt_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), p64]
+    L.attt_timing_kernel_name.restype = ctypes.c_char_p
+    L.attt_timing_kernel_name.argtypes = [i32]
+    _LIB = L
+    return L
+
+
+def _check(status):
+    if status != OK:
+        L = load()
+        raise AtttError(status, L.attt_last_error().decode())
+
+
+def _offsets(off):
+    arr = np.ascontiguousarray(np.asarray(off, dtype=np.int64))
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr():
+    return _torch().cuda.current_stream().cuda_stream
+
+
+def _dptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if workspace is not None and workspace.numel() >= nbytes:
+        return workspace
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def _dev(t, name):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    return t
+
+
+# ------------------------------------------------------------------------------------------
+def ngram_workspace_size(history_offsets, token_offsets, n):
+    L = load()
+    ho, hp = _offsets(history_offsets)
+    to, tp = _offsets(token_offsets)
+    out = ctypes.c_size_t(0)
+    _check(L.attt_ngram_workspace_size(hp, tp, len(ho) - 1, n, ctypes.byref(out)))
+    return out.value
+
+
+def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.05,
+                  want_exposure=True, workspace=None):
+    """Eq. 8-9 for E episodes. history / tokens: int32 device tensors (flat); offsets: host
+    int64 sequences of length E+1. Returns (f, w): f as an int32 tensor holding the uint32
+    exposure (or None), w float32."""
+    torch = _torch()
+    L = load()
+    ho, hp = _offsets(history_offsets)
+    to, tp = _offsets(token_offsets)
+    E = len(ho) - 1
+    dev = tokens.device
+    _dev(tokens, "tokens")
+    _dev(history, "history")
+    if tokens.dtype != torch.int32 or history.dtype != torch.int32:
+        raise TypeError("history and tokens must be int32")
+    T = int(to[-1])
+    f = torch.empty(T, dtype=torch.int32, device=dev) if want_exposure else None
+    w = torch.empty(T, dtype=torch.float32, device=dev)
+    need = ctypes.c_size_t(0)
+    _check(L.attt_ngram_workspace_size(hp, tp, E, n, ctypes.byref(need)))
+    ws = _workspace(need.value, dev, workspace)
+    _check(L.attt_ngram_weights(_dptr(history), hp, _dptr(tokens), tp, E, n, float(w_min), _dptr(f),
+                                _dptr(w), _dptr(ws), ws.numel(), _stream_ptr()))
+    return f, w
+
+
+# ------------------------------------------------------------------------------------------
+def ce_workspace_size(N, d, V, dtype, want_grad=True):
+    L = load()
+    out = ctypes.c_size_t(0)
+    _check(L.attt_ce_workspace_size(N, d, V, dtype, 1 if want_grad else 0, ctypes.byref(out)))
+    return out.value
+
+
+def weighted_ce_fwd_bwd(hidden, lm_head, labels, weights, row_offsets=None, want_grad=True,
+                        want_lse=True, workspace=None, out=None):
+    """Eq. 10 forward and backward. hidden [N, d], lm_head [V, d] (float32 or bfloat16),
+    labels int32 [N], weights float32 [N]; row_offsets: host int64 [E+1] or None (one episode).
+    Returns (loss [E], lse [N] or None, grad_hidden [N, d] or None)."""
+    torch = _torch()
+    L = load()
+    for t, nm in ((hidden, "hidden"), (lm_head, "lm_head"), (labels, "labels"), (weights, "weights")):
+        _dev(t, nm)
+    dt = _dtype_code(hidden)
+    if lm_head.dtype != hidden.dtype:
+        raise TypeError("hidden and lm_head must share a dtype")
+    if labels.dtype != torch.int32 or weights.dtype != torch.float32:
+        raise TypeError("labels must be int32 and weights float32")
+    N, d = hidden.shape
+    V = lm_head.shape[0]
+    if lm_head.shape[1] != d:
+        raise ValueError("lm_head must be [V, d]")
+    if row_offsets is None:
+        ro, rp, E = None, None, 1
+    else:
+        ro, rp = _offsets(row_offsets)
+        E = len(ro) - 1
+    dev = hidden.device
+    if out is not None:
+        loss, lse, grad = out
+    else:
+        loss = torch.empty(E, dtype=torch.float32, device=dev)
+        lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
+        grad = torch.empty_like(hidden) if want_grad else None
+    need = ctypes.c_size_t(0)
+    _check(L.attt_ce_workspace_size(N, d, V, dt, 1 if grad is not None else 0, ctypes.byref(need)))
+    ws = _workspace(need.value, dev, workspace)
+    _check(L.attt_weighted_ce_fwd_bwd(_dptr(hidden), _dptr(lm_head), _dptr(labels), _dptr(weights),
+                                      rp, E, N, d, V, dt, _dptr(loss), _dptr(lse), _dptr(grad),
+                                      _dptr(ws), ws.numel(), _stream_ptr()))
+    return loss, lse, grad
+
+
+# ------------------------------------------------------------------------------------------
+def _lora_array(problems):
+    arr = (LoraProblem * max(len(problems), 1))()
+    for i, p in enumerate(problems):
+        x, dy, A, B = p["x"], p["dy"], p["A"], p["B"]
+        arr[i] = LoraProblem(_dptr(x), _dptr(dy), _dptr(A), _dptr(B), _dptr(p["dA"]), _dptr(p["dB"]),
+                             x.shape[0], x.shape[1], dy.shape[1], A.shape[0], float(p["scale"]))
+    return arr
+
+
+def lora_workspace_size(problems, dtype):
+    L = load()
+    arr = _lora_array(problems)
+    out = ctypes.c_size_t(0)
+    _check(L.attt_lora_workspace_size(arr, len(problems), dtype, ctypes.byref(out)))
+    return out.value
+
+
+def lora_grad(problems, workspace=None):
+    """LoRA dA / dB for a group of projections, accumulated (+=) into each problem's float32
+    dA [r, d_in] and dB [d_out, r]. Each problem: dict(x, dy, A, B, dA, dB, scale)."""
+    L = load()
+    if not problems:
+        return
+    dt = _dtype_code(problems[0]["x"])
+    for p in problems:
+        for k in ("x", "dy", "A", "B", "dA", "dB"):
+            _dev(p[k], k)
+    arr = _lora_array(problems)
+    need = ctypes.c_size_t(0)
+    _check(L.attt_lora_workspace_size(arr, len(problems), dt, ctypes.byref(need)))
+    ws = _workspace(need.value, problems[0]["x"].device, workspace)
+    _check(L.attt_lora_grad(arr, len(problems), dt, _dptr(ws), ws.numel(), _stream_ptr()))
+
+
+# ------------------------------------------------------------------------------------------
+def timing_enable(on=True):
+    _check(load().attt_timing_enable(1 if on else 0))
+
+
+def timing_reset():
+    _check(load().attt_timing_reset())
+
+
+def timing_read(name):
+    """(total milliseconds, launches) of one kernel since the last reset."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(load().attt_timing_read(name.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def kernel_names():
+    L = load()
+    out, i = [], 0
+    while True:
+        nm = L.attt_timing_kernel_name(i)
+        if nm is None:
+            return out
+        out.append(nm.decode())
+        i += 1
+
+
+def version():
+    return load().attt_version()

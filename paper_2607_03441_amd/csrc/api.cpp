@@ -1,0 +1,573 @@
+// C ABI of the aTTT update-step library: argument validation (host only, before any HIP
+// call), workspace planning, episode / problem batching into kernel-argument descriptors,
+// kernel launches on the caller's stream, and optional per-kernel event timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "attt.h"
+#include "internal.hpp"
+
+using namespace attt;
+
+// ------------------------------------------------------------------------------------------
+// Status, messages, timing registry
+// ------------------------------------------------------------------------------------------
+static thread_local std::string g_last_error;
+
+static attt_status fail(attt_status code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+static attt_status fail(attt_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+static attt_status hip_fail(hipError_t e, const char* where) {
+  return fail(ATTT_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, where)                  \
+  do {                                        \
+    hipError_t e_ = (expr);                   \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+namespace attt {
+
+static const char* kKernelNames[K_NUM_KERNELS] = {
+    "ngram_build", "ngram_count", "ngram_weight", "ce_fwd_lse",  "ce_row_reduce", "ce_loss",
+    "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "lora_u_du",  "lora_dadb",     "lora_reduce"};
+
+const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
+
+struct TimingRec {
+  int id;
+  hipEvent_t a, b;
+};
+static std::mutex g_tmu;
+static bool g_timing = false;
+static std::vector<TimingRec> g_recs;
+static double g_ms[K_NUM_KERNELS];
+static int64_t g_launches[K_NUM_KERNELS];
+
+bool timing_on() { return g_timing; }
+
+void timing_record(int id, hipEvent_t a, hipEvent_t b) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_recs.push_back({id, a, b});
+}
+
+static hipError_t timing_drain() {
+  hipError_t first = hipSuccess;
+  for (auto& r : g_recs) {
+    hipError_t e = hipEventSynchronize(r.b);
+    float ms = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e == hipSuccess) {
+      g_ms[r.id] += ms;
+      g_launches[r.id] += 1;
+    } else if (first == hipSuccess) {
+      first = e;
+    }
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  g_recs.clear();
+  return first;
+}
+
+}  // namespace attt
+
+extern "C" {
+
+const char* attt_status_string(attt_status s) {
+  switch (s) {
+    case ATTT_OK: return "ok";
+    case ATTT_EINVAL: return "invalid argument";
+    case ATTT_ENOSPACE: return "workspace too small";
+    case ATTT_EUNSUPPORTED: return "unsupported by this build";
+    case ATTT_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* attt_last_error(void) { return g_last_error.c_str(); }
+
+int32_t attt_version(void) { return 100; }
+
+attt_status attt_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+  return ATTT_OK;
+}
+
+attt_status attt_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  hipError_t e = timing_drain();
+  std::fill(g_ms, g_ms + K_NUM_KERNELS, 0.0);
+  std::fill(g_launches, g_launches + K_NUM_KERNELS, 0);
+  if (e != hipSuccess) return hip_fail(e, "attt_timing_reset");
+  return ATTT_OK;
+}
+
+attt_status attt_timing_read(const char* kernel, double* total_ms, int64_t* launches) {
+  if (!kernel || !total_ms || !launches) return fail(ATTT_EINVAL, "attt_timing_read: null argument");
+  int id = -1;
+  for (int i = 0; i < K_NUM_KERNELS; ++i)
+    if (std::strcmp(kernel, kKernelNames[i]) == 0) id = i;
+  if (id < 0) return fail(ATTT_EINVAL, "attt_timing_read: unknown kernel '%s'", kernel);
+  std::lock_guard<std::mutex> lk(g_tmu);
+  hipError_t e = timing_drain();
+  if (e != hipSuccess) return hip_fail(e, "attt_timing_read");
+  *total_ms = g_ms[id];
+  *launches = g_launches[id];
+  return ATTT_OK;
+}
+
+const char* attt_timing_kernel_name(int32_t i) { return kernel_name(i); }
+
+}  // extern "C"
+
+// ------------------------------------------------------------------------------------------
+// Helpers
+// ------------------------------------------------------------------------------------------
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+static inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+static inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+static inline bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+static attt_status check_offsets(const char* what, const int64_t* off, int32_t E, int64_t limit) {
+  if (!off) return fail(ATTT_EINVAL, "%s: offsets pointer is null", what);
+  if (off[0] != 0) return fail(ATTT_EINVAL, "%s: offsets[0] must be 0", what);
+  for (int32_t e = 0; e < E; ++e) {
+    if (off[e + 1] < off[e]) return fail(ATTT_EINVAL, "%s: offsets decrease at episode %d", what, e);
+    if (off[e + 1] - off[e] > limit)
+      return fail(ATTT_EUNSUPPORTED, "%s: episode %d holds %lld entries (limit %lld)", what, e,
+                  (long long)(off[e + 1] - off[e]), (long long)limit);
+  }
+  return ATTT_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// n-gram exposure and weights
+// ------------------------------------------------------------------------------------------
+namespace {
+
+struct NgramPlan {
+  std::vector<NgramPart> parts;
+  size_t off_tables = 0, off_counts = 0, off_qcell = 0, total = 0;
+  int64_t total_slots = 0;
+};
+
+int next_pow2(int v) {
+  int p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+attt_status ngram_validate(const int64_t* hoff, const int64_t* toff, int32_t E, int32_t n) {
+  if (E < 1) return fail(ATTT_EINVAL, "ngram: num_episodes must be >= 1 (got %d)", E);
+  if (n < 1 || n > ATTT_NGRAM_MAX_N)
+    return fail(ATTT_EINVAL, "ngram: n must be in [1, %d] (got %d)", ATTT_NGRAM_MAX_N, n);
+  attt_status st = check_offsets("ngram history", hoff, E, INT32_MAX);
+  if (st) return st;
+  st = check_offsets("ngram tokens", toff, E, INT32_MAX);
+  if (st) return st;
+  if (toff[E] >= ((int64_t)1 << 31)) return fail(ATTT_EUNSUPPORTED, "ngram: more than 2^31-1 update tokens");
+  return ATTT_OK;
+}
+
+NgramPlan ngram_plan(const int64_t* hoff, const int64_t* toff, int32_t E, int32_t n) {
+  NgramPlan P;
+  int64_t table_slots = 0;
+  for (int32_t e = 0; e < E; ++e) {
+    const int64_t L = toff[e + 1] - toff[e];
+    const int64_t H = hoff[e + 1] - hoff[e];
+    const int64_t Q = std::max<int64_t>(0, L - n + 1);
+    for (int64_t q0 = 0; q0 < Q; q0 += kQMax) {
+      NgramPart p{};
+      p.tok_base = toff[e];
+      p.hist_base = hoff[e];
+      p.hist_ngrams = (int32_t)std::max<int64_t>(0, H - n + 1);
+      p.q0 = (int32_t)q0;
+      p.qn = (int32_t)std::min<int64_t>(kQMax, Q - q0);
+      p.slots = std::max(64, next_pow2(2 * p.qn));
+      p.table_off = table_slots;
+      p.count_off = (uint32_t)table_slots;
+      table_slots += p.slots;
+      P.parts.push_back(p);
+    }
+  }
+  P.total_slots = table_slots;
+  P.off_tables = 0;
+  P.off_counts = align256((size_t)table_slots * 8);
+  P.off_qcell = P.off_counts + align256((size_t)table_slots * 4);
+  P.total = P.off_qcell + align256((size_t)toff[E] * 4);
+  if (P.total == 0) P.total = 256;
+  return P;
+}
+
+}  // namespace
+
+extern "C" attt_status attt_ngram_workspace_size(const int64_t* history_offsets,
+                                                 const int64_t* token_offsets, int32_t num_episodes,
+                                                 int32_t n, size_t* bytes) {
+  if (!bytes) return fail(ATTT_EINVAL, "ngram: bytes is null");
+  attt_status st = ngram_validate(history_offsets, token_offsets, num_episodes, n);
+  if (st) return st;
+  *bytes = ngram_plan(history_offsets, token_offsets, num_episodes, n).total;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_offsets,
+                                          const int32_t* tokens, const int64_t* token_offsets,
+                                          int32_t num_episodes, int32_t n, float w_min,
+                                          uint32_t* exposure, float* weights, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  attt_status st = ngram_validate(history_offsets, token_offsets, num_episodes, n);
+  if (st) return st;
+  if (!(w_min >= 0x1p-20f && w_min <= 1.0f))
+    return fail(ATTT_EINVAL, "ngram: w_min must be in [2^-20, 1] (got %g)", (double)w_min);
+  const int32_t E = num_episodes;
+  const int64_t T = token_offsets[E];
+  if (T > 0 && !tokens) return fail(ATTT_EINVAL, "ngram: tokens is null");
+  if (T > 0 && !weights) return fail(ATTT_EINVAL, "ngram: weights is null");
+  if (history_offsets[E] > 0 && !history) return fail(ATTT_EINVAL, "ngram: history is null");
+  NgramPlan P = ngram_plan(history_offsets, token_offsets, E, n);
+  if (P.total_slots >= ((int64_t)1 << 32))
+    return fail(ATTT_EUNSUPPORTED, "ngram: too many table slots (%lld)", (long long)P.total_slots);
+  if (workspace_bytes < P.total)
+    return fail(ATTT_ENOSPACE, "ngram: workspace %zu bytes, need %zu", workspace_bytes, P.total);
+  if (!workspace) return fail(ATTT_EINVAL, "ngram: workspace is null");
+  if (!aligned256(workspace)) return fail(ATTT_EINVAL, "ngram: workspace must be 256-byte aligned");
+  if (T == 0) return ATTT_OK;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint2* tables = reinterpret_cast<uint2*>(ws + P.off_tables);
+  uint32_t* counts = reinterpret_cast<uint32_t*>(ws + P.off_counts);
+  uint32_t* qcell = reinterpret_cast<uint32_t*>(ws + P.off_qcell);
+
+  // Count blocks: spread the history work over about two workgroups per CU.
+  int64_t work = 0;
+  for (auto& p : P.parts) work += p.hist_ngrams;
+  const int64_t chunk_len = std::max<int64_t>(16384, ceil_div(work, 512));
+
+  for (size_t b0 = 0; b0 < P.parts.size(); b0 += kPartBatch) {
+    NgramPartBatch batch{};
+    batch.count = (int32_t)std::min<size_t>(kPartBatch, P.parts.size() - b0);
+    int max_slots = 64, blocks = 0;
+    for (int i = 0; i < batch.count; ++i) {
+      NgramPart p = P.parts[b0 + i];
+      p.chunks = p.hist_ngrams > 0 ? (int32_t)ceil_div(p.hist_ngrams, chunk_len) : 0;
+      p.chunk_begin = blocks;
+      blocks += p.chunks;
+      max_slots = std::max(max_slots, p.slots);
+      batch.p[i] = p;
+    }
+    HIP_TRY(launch_ngram_build(batch, max_slots, tokens, n, tables, counts, qcell, s), "ngram_build");
+    HIP_TRY(launch_ngram_count(batch, blocks, max_slots, history, tokens, n, tables, counts, s),
+            "ngram_count");
+  }
+  for (int32_t e0 = 0; e0 < E; e0 += kEpBatch) {
+    NgramEpBatch batch{};
+    batch.count = std::min<int32_t>(kEpBatch, E - e0);
+    int blocks = 0;
+    for (int i = 0; i < batch.count; ++i) {
+      const int32_t e = e0 + i;
+      batch.e[i].tok_base = token_offsets[e];
+      batch.e[i].L = (int32_t)(token_offsets[e + 1] - token_offsets[e]);
+      batch.e[i].block_begin = blocks;
+      blocks += (int)ceil_div(batch.e[i].L, 256);
+    }
+    HIP_TRY(launch_ngram_weight(batch, blocks, n, w_min, counts, qcell, exposure, weights, s),
+            "ngram_weight");
+  }
+  return ATTT_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Weighted cross-entropy
+// ------------------------------------------------------------------------------------------
+namespace {
+
+constexpr int64_t kCeRowBlock = 8192;     // rows per backward block
+constexpr int64_t kCeVocabChunk = 8192;   // vocab columns per backward chunk
+
+struct CePlan {
+  CeGemmShape fwd{64, 64}, dz{64, 64}, dh{64, 64};
+  int64_t n_vb = 0, R = 0, Vc = 0, Vp = 0;
+  size_t off_part = 0, off_label = 0, off_lse = 0, off_coef = 0, off_rowloss = 0;
+  size_t off_wt = 0, off_dz = 0, off_acc = 0, total = 0;
+};
+
+CeGemmShape mfma_shape(int64_t rows, int64_t cols) {
+  const int64_t big = ceil_div(rows, 256) * ceil_div(cols, 256);
+  return big >= 512 ? CeGemmShape{256, 256} : CeGemmShape{128, 128};
+}
+
+attt_status ce_validate(int64_t N, int64_t d, int64_t V, int32_t dtype) {
+  if (dtype != ATTT_F32 && dtype != ATTT_BF16) return fail(ATTT_EINVAL, "ce: unknown dtype %d", dtype);
+  if (N < 0) return fail(ATTT_EINVAL, "ce: N must be >= 0 (got %lld)", (long long)N);
+  if (d < 1 || d % 8 != 0) return fail(ATTT_EINVAL, "ce: d must be a positive multiple of 8 (got %lld)", (long long)d);
+  if (V < 1) return fail(ATTT_EINVAL, "ce: V must be >= 1 (got %lld)", (long long)V);
+  if (N >= ((int64_t)1 << 31) || V >= ((int64_t)1 << 31) || d >= ((int64_t)1 << 20))
+    return fail(ATTT_EUNSUPPORTED, "ce: dimensions beyond this build's limits");
+  return ATTT_OK;
+}
+
+CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
+  CePlan P;
+  const size_t esz = dtype == ATTT_BF16 ? 2 : 4;
+  if (dtype == ATTT_BF16) {
+    P.fwd = mfma_shape(N, V);
+    P.Vc = std::min<int64_t>(round_up(V, 256), kCeVocabChunk);
+    P.R = std::min<int64_t>(std::max<int64_t>(N, 1), kCeRowBlock);
+    P.dz = mfma_shape(P.R, P.Vc);
+    P.dh = mfma_shape(P.R, d);
+    P.Vp = round_up(V, 256);
+  } else {
+    P.Vc = std::min<int64_t>(round_up(V, 64), kCeVocabChunk);
+    P.R = std::min<int64_t>(std::max<int64_t>(N, 1), kCeRowBlock);
+    P.Vp = V;
+  }
+  P.n_vb = ceil_div(V, P.fwd.bn);
+  size_t o = 0;
+  P.off_part = o;    o += align256((size_t)N * P.n_vb * 8);
+  P.off_label = o;   o += align256((size_t)N * 4);
+  P.off_lse = o;     o += align256((size_t)N * 4);
+  P.off_coef = o;    o += align256((size_t)N * 4);
+  P.off_rowloss = o; o += align256((size_t)N * 4);
+  if (grad && N > 0) {
+    if (dtype == ATTT_BF16) {
+      P.off_wt = o;
+      o += align256((size_t)d * P.Vp * 2);
+    }
+    P.off_dz = o;
+    o += align256((size_t)P.R * P.Vc * esz);
+    const bool chunks = V > P.Vc;
+    if (dtype == ATTT_BF16 && chunks) {
+      P.off_acc = o;
+      o += align256((size_t)P.R * d * 4);
+    }
+  }
+  P.total = std::max<size_t>(o, 256);
+  return P;
+}
+
+}  // namespace
+
+extern "C" attt_status attt_ce_workspace_size(int64_t N, int64_t d, int64_t V, int32_t dtype,
+                                              int32_t want_grad, size_t* bytes) {
+  if (!bytes) return fail(ATTT_EINVAL, "ce: bytes is null");
+  attt_status st = ce_validate(N, d, V, dtype);
+  if (st) return st;
+  *bytes = ce_plan(N, d, V, dtype, want_grad != 0).total;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* lm_head,
+                                                const int32_t* labels, const float* weights,
+                                                const int64_t* row_offsets, int32_t num_episodes,
+                                                int64_t N, int64_t d, int64_t V, int32_t dtype,
+                                                float* loss, float* lse, void* grad_hidden,
+                                                void* workspace, size_t workspace_bytes,
+                                                void* stream) {
+  attt_status st = ce_validate(N, d, V, dtype);
+  if (st) return st;
+  if (num_episodes < 1) return fail(ATTT_EINVAL, "ce: num_episodes must be >= 1 (got %d)", num_episodes);
+  int64_t single[2] = {0, N};
+  const int64_t* off = row_offsets;
+  if (!off) {
+    if (num_episodes != 1) return fail(ATTT_EINVAL, "ce: row_offsets may be NULL only for one episode");
+    off = single;
+  }
+  st = check_offsets("ce rows", off, num_episodes, INT32_MAX);
+  if (st) return st;
+  if (off[num_episodes] != N) return fail(ATTT_EINVAL, "ce: row_offsets[E] (%lld) != N (%lld)",
+                                          (long long)off[num_episodes], (long long)N);
+  if (!loss) return fail(ATTT_EINVAL, "ce: loss is null");
+  if (N > 0) {
+    if (!hidden || !lm_head || !labels || !weights) return fail(ATTT_EINVAL, "ce: null input pointer");
+    if (!aligned16(hidden) || !aligned16(lm_head) || (grad_hidden && !aligned16(grad_hidden)))
+      return fail(ATTT_EINVAL, "ce: hidden, lm_head and grad_hidden must be 16-byte aligned");
+  }
+  const bool grad = grad_hidden != nullptr;
+  CePlan P = ce_plan(N, d, V, dtype, grad);
+  if (workspace_bytes < P.total)
+    return fail(ATTT_ENOSPACE, "ce: workspace %zu bytes, need %zu", workspace_bytes, P.total);
+  if (!workspace) return fail(ATTT_EINVAL, "ce: workspace is null");
+  if (!aligned256(workspace)) return fail(ATTT_EINVAL, "ce: workspace must be 256-byte aligned");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float2* part = reinterpret_cast<float2*>(ws + P.off_part);
+  float* label_logit = reinterpret_cast<float*>(ws + P.off_label);
+  float* lse_buf = lse ? lse : reinterpret_cast<float*>(ws + P.off_lse);
+  float* coef = reinterpret_cast<float*>(ws + P.off_coef);
+  float* rowloss = reinterpret_cast<float*>(ws + P.off_rowloss);
+  const int E = num_episodes;
+
+  HIP_TRY(launch_ce_fwd(dtype, P.fwd, hidden, lm_head, labels, (int)N, (int)d, (int)V, part,
+                        (int)P.n_vb, label_logit, s),
+          "ce_fwd_lse");
+  for (int e0 = 0; e0 < E; e0 += kEpBatch) {
+    CeEpBatch b{};
+    b.count = std::min(kEpBatch, E - e0);
+    b.first = e0;
+    int blocks = 0;
+    for (int i = 0; i < b.count; ++i) {
+      b.e[i].row0 = off[e0 + i];
+      b.e[i].L = (int32_t)(off[e0 + i + 1] - off[e0 + i]);
+      b.e[i].block_begin = blocks;
+      blocks += (int)ceil_div(b.e[i].L, 4);
+    }
+    HIP_TRY(launch_ce_row_reduce(b, blocks, part, (int)P.n_vb, label_logit, weights, lse_buf, coef,
+                                 rowloss, s),
+            "ce_row_reduce");
+    HIP_TRY(launch_ce_loss(b, rowloss, loss, s), "ce_loss");
+  }
+  if (!grad || N == 0) return ATTT_OK;
+
+  void* dz = ws + P.off_dz;
+  void* wt = nullptr;
+  float* acc = P.off_acc ? reinterpret_cast<float*>(ws + P.off_acc) : nullptr;
+  if (dtype == ATTT_BF16) {
+    wt = ws + P.off_wt;
+    HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)P.Vp, wt, s), "ce_head_transpose");
+  }
+  for (int64_t r0 = 0; r0 < N; r0 += P.R) {
+    const int64_t R = std::min(P.R, N - r0);
+    for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
+      const int64_t width = std::min(P.Vc, V - c0);
+      const bool first = c0 == 0, last = c0 + P.Vc >= V;
+      HIP_TRY(launch_ce_bwd_dz(dtype, P.dz, hidden, lm_head, labels, lse_buf, coef, (int)r0, (int)R,
+                               (int)d, (int)c0, (int)width, (int)V, dz, (int)P.Vc, s),
+              "ce_bwd_dz");
+      const int64_t K = dtype == ATTT_BF16 ? round_up(width, 64) : round_up(width, 16);
+      HIP_TRY(launch_ce_bwd_dh(dtype, P.dh, dz, (int)P.Vc, lm_head, wt, (int)P.Vp, (int)r0, (int)R,
+                               (int)d, (int)c0, (int)K, (int)V, acc, grad_hidden, first, last, s),
+              "ce_bwd_dh");
+    }
+  }
+  return ATTT_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// LoRA gradients
+// ------------------------------------------------------------------------------------------
+namespace {
+
+struct LoraPlan {
+  std::vector<LoraJob> jobs;
+  size_t total = 0;
+};
+
+attt_status lora_validate(const attt_lora_problem* p, int32_t count, int32_t dtype) {
+  if (dtype != ATTT_F32 && dtype != ATTT_BF16) return fail(ATTT_EINVAL, "lora: unknown dtype %d", dtype);
+  if (count < 0) return fail(ATTT_EINVAL, "lora: count must be >= 0");
+  if (count > 0 && !p) return fail(ATTT_EINVAL, "lora: problems is null");
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_problem& q = p[i];
+    if (q.rank < 1 || q.rank > ATTT_LORA_MAX_RANK)
+      return fail(ATTT_EINVAL, "lora[%d]: rank must be in [1, %d] (got %d)", i, ATTT_LORA_MAX_RANK, q.rank);
+    if (q.rows < 0 || q.d_in < 1 || q.d_out < 1 || q.d_in % 8 || q.d_out % 8)
+      return fail(ATTT_EINVAL, "lora[%d]: need rows >= 0 and d_in, d_out positive multiples of 8", i);
+    if (q.rows >= ((int64_t)1 << 30) || q.d_in >= ((int64_t)1 << 24) || q.d_out >= ((int64_t)1 << 24))
+      return fail(ATTT_EUNSUPPORTED, "lora[%d]: dimensions beyond this build's limits", i);
+    if (!std::isfinite(q.scale)) return fail(ATTT_EINVAL, "lora[%d]: scale is not finite", i);
+    if (!q.dA || !q.dB) return fail(ATTT_EINVAL, "lora[%d]: dA / dB is null", i);
+    if (q.rows > 0 && (!q.x || !q.dy || !q.A || !q.B)) return fail(ATTT_EINVAL, "lora[%d]: null input", i);
+    if (q.rows > 0 && (!aligned16(q.x) || !aligned16(q.dy) || !aligned16(q.A)))
+      return fail(ATTT_EINVAL, "lora[%d]: x, dy and A must be 16-byte aligned", i);
+  }
+  return ATTT_OK;
+}
+
+LoraPlan lora_plan(const attt_lora_problem* p, int32_t count, int32_t dtype) {
+  LoraPlan P;
+  const size_t esz = dtype == ATTT_BF16 ? 2 : 4;
+  int64_t colblocks = 0;
+  for (int32_t i = 0; i < count; ++i)
+    if (p[i].rows > 0)
+      colblocks += ceil_div(p[i].d_in, kLoraColTile) + ceil_div(p[i].d_out, kLoraColTile);
+  size_t o = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_problem& q = p[i];
+    if (q.rows == 0) continue;
+    LoraJob J{};
+    J.x = q.x; J.dy = q.dy; J.A = q.A; J.B = q.B; J.dA = q.dA; J.dB = q.dB;
+    J.rows = (int32_t)q.rows;
+    J.rows_pad = (int32_t)round_up(q.rows, kLoraRowTile);
+    J.d_in = (int32_t)q.d_in;
+    J.d_out = (int32_t)q.d_out;
+    J.rank = q.rank;
+    J.rp = (int32_t)round_up(q.rank, 16);
+    J.scale = q.scale;
+    // Row splits of pass 2: about 1024 blocks over the whole group, at least 256 rows each.
+    const int64_t want = std::max<int64_t>(1, ceil_div(1024, std::max<int64_t>(colblocks, 1)));
+    J.splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>(want, J.rows_pad / 256));
+    J.ut_off = (int64_t)o;  o += align256((size_t)J.rp * J.rows_pad * esz);
+    J.dut_off = (int64_t)o; o += align256((size_t)J.rp * J.rows_pad * esz);
+    J.pa_off = (int64_t)o;  o += align256((size_t)J.splits * J.rp * J.d_in * 4);
+    J.pb_off = (int64_t)o;  o += align256((size_t)J.splits * J.rp * J.d_out * 4);
+    P.jobs.push_back(J);
+  }
+  P.total = std::max<size_t>(o, 256);
+  return P;
+}
+
+}  // namespace
+
+extern "C" attt_status attt_lora_workspace_size(const attt_lora_problem* problems, int32_t count,
+                                                int32_t dtype, size_t* bytes) {
+  if (!bytes) return fail(ATTT_EINVAL, "lora: bytes is null");
+  attt_status st = lora_validate(problems, count, dtype);
+  if (st) return st;
+  *bytes = lora_plan(problems, count, dtype).total;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t count, int32_t dtype,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  attt_status st = lora_validate(problems, count, dtype);
+  if (st) return st;
+  LoraPlan P = lora_plan(problems, count, dtype);
+  if (workspace_bytes < P.total)
+    return fail(ATTT_ENOSPACE, "lora: workspace %zu bytes, need %zu", workspace_bytes, P.total);
+  if (!workspace) return fail(ATTT_EINVAL, "lora: workspace is null");
+  if (!aligned256(workspace)) return fail(ATTT_EINVAL, "lora: workspace must be 256-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  for (size_t j0 = 0; j0 < P.jobs.size(); j0 += kLoraBatch) {
+    LoraBatch b{};
+    b.count = (int32_t)std::min<size_t>(kLoraBatch, P.jobs.size() - j0);
+    int b1 = 0, b2 = 0, b3 = 0;
+    for (int i = 0; i < b.count; ++i) {
+      LoraJob J = P.jobs[j0 + i];
+      J.b1_begin = b1;
+      b1 += 2 * (J.rows_pad / kLoraRowTile);
+      J.b2_begin = b2;
+      b2 += J.splits * (int)(ceil_div(J.d_in, kLoraColTile) + ceil_div(J.d_out, kLoraColTile));
+      J.b3_begin = b3;
+      b3 += (int)ceil_div((int64_t)J.rank * J.d_in + (int64_t)J.d_out * J.rank, 256);
+      b.j[i] = J;
+    }
+    HIP_TRY(launch_lora_pass1(dtype, b, b1, ws, s), "lora_u_du");
+    HIP_TRY(launch_lora_pass2(dtype, b, b2, ws, s), "lora_dadb");
+    HIP_TRY(launch_lora_reduce(b, b3, ws, s), "lora_reduce");
+  }
+  return ATTT_OK;
+}

@@ -1,0 +1,628 @@
+// Token-weighted cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10), forward and
+// backward with respect to the hidden states, on gfx950.
+//
+// Forward (logits never leave the chip): one GEMM z = h W^T over (row tile, vocab tile)
+// whose epilogue reduces every row of the tile to (max, sum exp(z - max)) and picks the
+// label logit. A row kernel merges the partials into lse and w * CE; an episode kernel sums
+// those in a fixed order into loss_e = (1/L_e) sum w_t CE_t.
+//
+// Backward, per vocab chunk: a GEMM recomputes the chunk's logits and its epilogue forms
+// dZ = (w_t / L_e)(exp(z - lse_t) - [v == y_t]) directly from the accumulators, stored in
+// the GEMM operand dtype into a bounded staging buffer; a second GEMM accumulates
+// dH += dZ_chunk W_chunk in float32 and the last chunk writes dH in the output dtype.
+//
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 4 waves per workgroup in a 2x2 grid, each wave
+// a (BM/2)x(BN/2) sub-tile, K step 64 double-buffered in LDS with an XOR swizzle of the
+// 16-byte chunks (chunk ^ row%8) so that the 32 rows one MFMA operand read touches fall in
+// distinct banks. Tiles are ordered XCD-aware: workgroup i runs on XCD i%8, and each XCD
+// gets a contiguous range of tiles in vocab-major order, so the workgroups of one XCD
+// share the same LM-head panel in their L2.
+// f32 path: plain VALU tiles (64x64, 4x4 per thread); it serves the float32 configuration.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace attt {
+
+// ------------------------------------------------------------------------------------------
+// Shared helpers
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
+  const int xcd = bid & 7, j = bid >> 3;
+  const int q = total >> 3, r = total & 7;
+  return xcd * q + min(xcd, r) + j;
+}
+
+template <int BM, int BN>
+struct MfmaTile {
+  static constexpr int BK = 64;
+  static constexpr int TM = BM / 64;  // 32x32 MFMA tiles per wave along rows
+  static constexpr int TN = BN / 64;  // ... along columns
+  static constexpr int AL = BM / 32;  // 16-byte global loads per thread per stage (A)
+  static constexpr int BL = BN / 32;
+  static constexpr int SA = BM * BK;  // bf16 elements per stage
+  static constexpr int SB = BN * BK;
+  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);
+};
+
+// acc += A[0:BM, 0:K] * B[0:BN, 0:K]^T, A and B K-contiguous bf16. Rows at or past mval
+// (nval) and K-chunks at or past K read as zero. K % 8 == 0.
+template <int BM, int BN>
+__device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                              const bf16_t* __restrict__ B, int64_t ldb, int nval,
+                                              int K, bf16_t* lds,
+                                              f32x16 (&acc)[BM / 64][BN / 64]) {
+  using T = MfmaTile<BM, BN>;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lrow = tid >> 3, lch = tid & 7;
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  u32x4 ra[T::AL], rb[T::BL];
+  auto gload = [&](int k0) {
+    const int k = k0 + lch * 8;
+    const bool kin = k < K;
+#pragma unroll
+    for (int i = 0; i < T::AL; ++i) {
+      const int row = lrow + 32 * i;
+      ra[i] = (kin && row < mval) ? *reinterpret_cast<const u32x4*>(A + (int64_t)row * lda + k)
+                                  : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < T::BL; ++i) {
+      const int row = lrow + 32 * i;
+      rb[i] = (kin && row < nval) ? *reinterpret_cast<const u32x4*>(B + (int64_t)row * ldb + k)
+                                  : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto lstore = [&](int st) {
+    bf16_t* As = lds + st * (T::SA + T::SB);
+    bf16_t* Bs = As + T::SA;
+#pragma unroll
+    for (int i = 0; i < T::AL; ++i) {
+      const int row = lrow + 32 * i;
+      *reinterpret_cast<u32x4*>(As + row * 64 + ((lch ^ (row & 7)) << 3)) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < T::BL; ++i) {
+      const int row = lrow + 32 * i;
+      *reinterpret_cast<u32x4*>(Bs + row * 64 + ((lch ^ (row & 7)) << 3)) = rb[i];
+    }
+  };
+
+  const int nk = (K + 63) / 64;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int l32 = lane & 31, hi = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload((kt + 1) * 64);
+    const bf16_t* As = lds + (kt & 1) * (T::SA + T::SB);
+    const bf16_t* Bs = As + T::SA;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int ch = kk * 2 + hi;
+      const int sw = (ch ^ (l32 & 7)) << 3;
+      bf16x8 a[T::TM], b[T::TN];
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i) {
+        const int r = wm * (BM / 2) + i * 32 + l32;
+        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + r * 64 + sw));
+      }
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int r = wn * (BN / 2) + j * 32 + l32;
+        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + r * 64 + sw));
+      }
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore((kt + 1) & 1);
+    __syncthreads();
+  }
+}
+
+// Output layout of a 32x32 MFMA accumulator: register r of lane l holds
+// row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+__device__ __forceinline__ int mfma_row(int r, int lane) { return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3); }
+
+// ------------------------------------------------------------------------------------------
+// bf16 forward: partial (max, sumexp) per (row, BN-wide vocab tile) and the label logit.
+// ------------------------------------------------------------------------------------------
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void ce_fwd_bf16_kernel(const bf16_t* __restrict__ h,
+                                                          const bf16_t* __restrict__ W,
+                                                          const int32_t* __restrict__ labels,
+                                                          int N, int d, int V, int tiles_m,
+                                                          int tiles_n, float2* __restrict__ partials,
+                                                          int n_vb, float* __restrict__ label_logit) {
+  using T = MfmaTile<BM, BN>;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int tm = tile % tiles_m, tn = tile / tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  f32x16 acc[T::TM][T::TN];
+  mfma_mainloop<BM, BN>(h + (int64_t)m0 * d, d, N - m0, W + (int64_t)n0 * d, d, V - n0, d,
+                        reinterpret_cast<bf16_t*>(smem), acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  float* red_m = reinterpret_cast<float*>(smem);  // [2][BM]
+  float* red_s = red_m + 2 * BM;
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      const int row = m0 + rl;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+        if (col < V) mx = fmaxf(mx, acc[i][j][r]);
+      }
+      mx = group_max<32>(mx);
+      float s = 0.0f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j) {
+          const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+          if (col < V) s += expf(acc[i][j][r] - mx);
+        }
+      }
+      s = group_sum<32>(s);
+      if ((lane & 31) == 0) {
+        red_m[wn * BM + rl] = mx;
+        red_s[wn * BM + rl] = s;
+      }
+      if (row < N) {
+        const int y = labels[row];
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j) {
+          const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+          if (col == y) label_logit[row] = acc[i][j][r];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int rl = threadIdx.x; rl < BM; rl += blockDim.x) {
+    const int row = m0 + rl;
+    if (row >= N) continue;
+    float m = red_m[rl], s = red_s[rl];
+    lse_merge(m, s, red_m[BM + rl], red_s[BM + rl]);
+    partials[(int64_t)row * n_vb + tn] = make_float2(m, s);
+  }
+}
+
+// bf16 backward part 1: dZ for rows [r0, r0+R) x vocab [c0, c0 + tiles_n*BN) into staging.
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void ce_dz_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
+    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
+    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
+  using T = MfmaTile<BM, BN>;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int tm = tile % tiles_m, tn = tile / tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  f32x16 acc[T::TM][T::TN];
+  mfma_mainloop<BM, BN>(h + (int64_t)(r0 + m0) * d, d, R - m0, W + (int64_t)(c0 + n0) * d, d,
+                        cend - (c0 + n0), d, reinterpret_cast<bf16_t*>(smem), acc);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = m0 + wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      if (rl >= R) continue;
+      const int row = r0 + rl;
+      const float l = lse[row], c = coef[row];
+      const int y = labels[row];
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int cl = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+        const int col = c0 + cl;
+        float g = 0.0f;
+        if (col < V) g = c * (expf(acc[i][j][r] - l) - (col == y ? 1.0f : 0.0f));
+        dz[(int64_t)rl * ldz + cl] = (bf16_t)f32_to_bf16_bits(g);
+      }
+    }
+  }
+}
+
+// bf16 backward part 2: dH[r0 + m, n] (+)= sum_k dZ[m, k] WT[n, c0 + k].
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void ce_dh_bf16_kernel(const bf16_t* __restrict__ dz, int ldz,
+                                                         const bf16_t* __restrict__ WT, int Vp,
+                                                         int r0, int R, int d, int c0, int K,
+                                                         int tiles_m, int tiles_n,
+                                                         float* __restrict__ accbuf,
+                                                         bf16_t* __restrict__ grad, int first,
+                                                         int last) {
+  using T = MfmaTile<BM, BN>;
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
+  const int tm = tile % tiles_m, tn = tile / tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  f32x16 acc[T::TM][T::TN];
+  mfma_mainloop<BM, BN>(dz + (int64_t)m0 * ldz, ldz, R - m0, WT + (int64_t)n0 * Vp + c0, Vp,
+                        d - n0, K, reinterpret_cast<bf16_t*>(smem), acc);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = m0 + wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      if (rl >= R) continue;
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) {
+        const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+        if (col >= d) continue;
+        float v = acc[i][j][r];
+        const int64_t o = (int64_t)rl * d + col;
+        if (!first) v += accbuf[o];
+        if (last)
+          grad[(int64_t)(r0 + rl) * d + col] = (bf16_t)f32_to_bf16_bits(v);
+        else
+          accbuf[o] = v;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// f32 path: VALU tiles of 64x64, 256 threads with 4x4 outputs each.
+// ------------------------------------------------------------------------------------------
+constexpr int kVT = 64, kVK = 16;
+
+// acc += A[0:64, 0:K] * op(B): NT reads B as [64 cols, K] (K-contiguous), NN as [K, 64 cols].
+template <bool NN>
+__device__ __forceinline__ void valu_mainloop(const float* __restrict__ A, int64_t lda, int mval,
+                                              const float* __restrict__ B, int64_t ldb, int nval,
+                                              int K, int kval_b, float (&acc)[4][4]) {
+  __shared__ float As[kVK][kVT + 4];
+  __shared__ float Bs[kVK][kVT + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  for (int k0 = 0; k0 < K; k0 += kVK) {
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (lr < mval && k0 + lk < K) a = *reinterpret_cast<const float4*>(A + (int64_t)lr * lda + k0 + lk);
+    As[lk + 0][lr] = a.x; As[lk + 1][lr] = a.y; As[lk + 2][lr] = a.z; As[lk + 3][lr] = a.w;
+    if (!NN) {
+      float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (lr < nval && k0 + lk < K) b = *reinterpret_cast<const float4*>(B + (int64_t)lr * ldb + k0 + lk);
+      Bs[lk + 0][lr] = b.x; Bs[lk + 1][lr] = b.y; Bs[lk + 2][lr] = b.z; Bs[lk + 3][lr] = b.w;
+    } else {
+      const int kr = tid >> 4, nc = (tid & 15) * 4;
+      float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (k0 + kr < kval_b && nc < nval) b = *reinterpret_cast<const float4*>(B + (int64_t)(k0 + kr) * ldb + nc);
+      Bs[kr][nc + 0] = b.x; Bs[kr][nc + 1] = b.y; Bs[kr][nc + 2] = b.z; Bs[kr][nc + 3] = b.w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kVK; ++k) {
+      float a4[4], b4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a4[i] = As[k][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b4[j] = Bs[k][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a4[i], b4[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void ce_fwd_f32_kernel(const float* __restrict__ h,
+                                                         const float* __restrict__ W,
+                                                         const int32_t* __restrict__ labels, int N,
+                                                         int d, int V, int tiles_m,
+                                                         float2* __restrict__ partials, int n_vb,
+                                                         float* __restrict__ label_logit) {
+  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int m0 = tm * kVT, n0 = tn * kVT;
+  float acc[4][4];
+  valu_mainloop<false>(h + (int64_t)m0 * d, d, N - m0, W + (int64_t)n0 * d, d, V - n0, d, 0, acc);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + ty * 4 + i;
+    float mx = -INFINITY;
+    for (int j = 0; j < 4; ++j)
+      if (n0 + tx * 4 + j < V) mx = fmaxf(mx, acc[i][j]);
+    mx = group_max<16>(mx);
+    float s = 0.0f;
+    if (mx != -INFINITY)
+      for (int j = 0; j < 4; ++j)
+        if (n0 + tx * 4 + j < V) s += expf(acc[i][j] - mx);
+    s = group_sum<16>(s);
+    if (row < N) {
+      if (tx == 0) partials[(int64_t)row * n_vb + tn] = make_float2(mx, s);
+      const int y = labels[row];
+      for (int j = 0; j < 4; ++j)
+        if (n0 + tx * 4 + j == y) label_logit[row] = acc[i][j];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void ce_dz_f32_kernel(const float* __restrict__ h,
+                                                        const float* __restrict__ W,
+                                                        const int32_t* __restrict__ labels,
+                                                        const float* __restrict__ lse,
+                                                        const float* __restrict__ coef, int r0,
+                                                        int R, int d, int c0, int cend, int V,
+                                                        int tiles_m, float* __restrict__ dz,
+                                                        int ldz) {
+  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int m0 = tm * kVT, n0 = tn * kVT;
+  float acc[4][4];
+  valu_mainloop<false>(h + (int64_t)(r0 + m0) * d, d, R - m0, W + (int64_t)(c0 + n0) * d, d,
+                       cend - (c0 + n0), d, 0, acc);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  for (int i = 0; i < 4; ++i) {
+    const int rl = m0 + ty * 4 + i;
+    if (rl >= R) continue;
+    const int row = r0 + rl;
+    const float l = lse[row], c = coef[row];
+    const int y = labels[row];
+    for (int j = 0; j < 4; ++j) {
+      const int cl = n0 + tx * 4 + j, col = c0 + cl;
+      float g = 0.0f;
+      if (col < V) g = c * (expf(acc[i][j] - l) - (col == y ? 1.0f : 0.0f));
+      dz[(int64_t)rl * ldz + cl] = g;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void ce_dh_f32_kernel(const float* __restrict__ dz, int ldz,
+                                                        const float* __restrict__ W, int r0, int R,
+                                                        int d, int c0, int K, int kval,
+                                                        int tiles_m, float* __restrict__ grad,
+                                                        int first) {
+  const int tm = blockIdx.x % tiles_m, tn = blockIdx.x / tiles_m;
+  const int m0 = tm * kVT, n0 = tn * kVT;
+  float acc[4][4];
+  valu_mainloop<true>(dz + (int64_t)m0 * ldz, ldz, R - m0, W + (int64_t)c0 * d + n0, d, d - n0, K,
+                      kval, acc);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  for (int i = 0; i < 4; ++i) {
+    const int rl = m0 + ty * 4 + i;
+    if (rl >= R) continue;
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + tx * 4 + j;
+      if (col >= d) continue;
+      const int64_t o = (int64_t)(r0 + rl) * d + col;
+      grad[o] = first ? acc[i][j] : grad[o] + acc[i][j];
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Row and episode reductions, LM-head transpose.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void ce_row_reduce_kernel(CeEpBatch b,
+                                                            const float2* __restrict__ partials,
+                                                            int n_vb,
+                                                            const float* __restrict__ label_logit,
+                                                            const float* __restrict__ weights,
+                                                            float* __restrict__ lse,
+                                                            float* __restrict__ coef,
+                                                            float* __restrict__ rowloss) {
+  int ei = 0;
+  while (ei + 1 < b.count && b.e[ei + 1].block_begin <= (int)blockIdx.x) ++ei;
+  const CeEp E = b.e[ei];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int local = ((int)blockIdx.x - E.block_begin) * 4 + wave;
+  if (local >= E.L) return;
+  const int64_t row = E.row0 + local;
+  float m = -INFINITY, s = 0.0f;
+  for (int i = lane; i < n_vb; i += 64) {
+    const float2 p = partials[row * n_vb + i];
+    lse_merge(m, s, p.x, p.y);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(s, o, 64);
+    lse_merge(m, s, m2, s2);
+  }
+  if (lane == 0) {
+    const float l = m + logf(s);
+    const float w = weights[row];
+    lse[row] = l;
+    coef[row] = __fdiv_rn(w, (float)E.L);
+    rowloss[row] = w * (l - label_logit[row]);
+  }
+}
+
+__global__ __launch_bounds__(256) void ce_loss_kernel(CeEpBatch b, const float* __restrict__ rowloss,
+                                                      float* __restrict__ loss) {
+  const CeEp E = b.e[blockIdx.x];
+  double acc = 0.0;
+  for (int i = threadIdx.x; i < E.L; i += blockDim.x) acc += (double)rowloss[E.row0 + i];
+  acc = wave_sum_f64(acc);
+  __shared__ double part[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) part[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double t = (part[0] + part[1]) + (part[2] + part[3]);
+    loss[b.first + blockIdx.x] = E.L > 0 ? (float)(t / (double)E.L) : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(256) void ce_head_transpose_kernel(const bf16_t* __restrict__ W, int V,
+                                                                int d, int Vp,
+                                                                bf16_t* __restrict__ WT) {
+  __shared__ bf16_t t[64][66];
+  const int v0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
+  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
+    const int r = idx >> 6, c = idx & 63;
+    const int v = v0 + r, j = j0 + c;
+    t[r][c] = (v < V && j < d) ? W[(int64_t)v * d + j] : (bf16_t)0;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
+    const int r = idx >> 6, c = idx & 63;
+    const int j = j0 + r, v = v0 + c;
+    if (j < d && v < Vp) WT[(int64_t)j * Vp + v] = t[c][r];
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Launchers
+// ------------------------------------------------------------------------------------------
+template <class Kern>
+static hipError_t allow_big_lds(Kern k) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+}
+
+template <int BM, int BN>
+static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, int N, int d,
+                           int V, float2* partials, int n_vb, float* label_logit, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = allow_big_lds(ce_fwd_bf16_kernel<BM, BN>);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int tm = (N + BM - 1) / BM, tn = (V + BN - 1) / BN;
+  KernelTimer t(K_CE_FWD, s);
+  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
+  hipLaunchKernelGGL((ce_fwd_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, h, W, labels, N,
+                     d, V, tm, tn, partials, n_vb, label_logit);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
+                         const int32_t* labels, int N, int d, int V, float2* partials, int n_vb,
+                         float* label_logit, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  if (dtype == 1) {
+    const bf16_t* hb = static_cast<const bf16_t*>(h);
+    const bf16_t* Wb = static_cast<const bf16_t*>(W);
+    if (t.bm == 256) return fwd_bf16<256, 256>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
+    return fwd_bf16<128, 128>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
+  }
+  const int tm = (N + kVT - 1) / kVT, tn = (V + kVT - 1) / kVT;
+  KernelTimer tt(K_CE_FWD, s);
+  hipLaunchKernelGGL(ce_fwd_f32_kernel, dim3(tm * tn), dim3(256), 0, s,
+                     static_cast<const float*>(h), static_cast<const float*>(W), labels, N, d, V, tm,
+                     partials, n_vb, label_logit);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const float2* partials,
+                                int n_vb, const float* label_logit, const float* weights,
+                                float* lse, float* coef, float* rowloss, hipStream_t s) {
+  if (total_blocks <= 0) return hipSuccess;
+  KernelTimer t(K_CE_ROW_REDUCE, s);
+  hipLaunchKernelGGL(ce_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
+                     label_logit, weights, lse, coef, rowloss);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, hipStream_t s) {
+  if (b.count <= 0) return hipSuccess;
+  KernelTimer t(K_CE_LOSS, s);
+  hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* WT, hipStream_t s) {
+  KernelTimer t(K_CE_HEAD_T, s);
+  hipLaunchKernelGGL(ce_head_transpose_kernel, dim3((Vp + 63) / 64, (d + 63) / 64), dim3(256), 0, s,
+                     static_cast<const bf16_t*>(W), V, d, Vp, static_cast<bf16_t*>(WT));
+  return hipGetLastError();
+}
+
+template <int BM, int BN>
+static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, const float* lse,
+                          const float* coef, int r0, int R, int d, int c0, int Vc, int V, bf16_t* dz,
+                          int ldz, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = allow_big_lds(ce_dz_bf16_kernel<BM, BN>);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int tm = (R + BM - 1) / BM, tn = (Vc + BN - 1) / BN;
+  const int cend = min(c0 + Vc, V);
+  KernelTimer t(K_CE_BWD_DZ, s);
+  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
+  hipLaunchKernelGGL((ce_dz_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, h, W, labels, lse,
+                     coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
+                            const int32_t* labels, const float* lse, const float* coef, int r0,
+                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  if (dtype == 1) {
+    const bf16_t* hb = static_cast<const bf16_t*>(h);
+    const bf16_t* Wb = static_cast<const bf16_t*>(W);
+    bf16_t* z = static_cast<bf16_t*>(dz);
+    if (t.bm == 256) return dz_bf16<256, 256>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
+    return dz_bf16<128, 128>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
+  }
+  const int tm = (R + kVT - 1) / kVT, tn = (Vc + kVT - 1) / kVT;
+  const int cend = min(c0 + Vc, V);
+  KernelTimer tt(K_CE_BWD_DZ, s);
+  hipLaunchKernelGGL(ce_dz_f32_kernel, dim3(tm * tn), dim3(256), 0, s, static_cast<const float*>(h),
+                     static_cast<const float*>(W), labels, lse, coef, r0, R, d, c0, cend, V, tm,
+                     static_cast<float*>(dz), ldz);
+  return hipGetLastError();
+}
+
+template <int BM, int BN>
+static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, int r0, int R, int d,
+                          int c0, int K, float* acc, bf16_t* grad, bool first, bool last,
+                          hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = allow_big_lds(ce_dh_bf16_kernel<BM, BN>);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int tm = (R + BM - 1) / BM, tn = (d + BN - 1) / BN;
+  KernelTimer t(K_CE_BWD_DH, s);
+  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
+  hipLaunchKernelGGL((ce_dh_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, dz, ldz, WT, Vp, r0,
+                     R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
+                            const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
+                            float* acc, void* grad, bool first, bool last, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  if (dtype == 1) {
+    const bf16_t* z = static_cast<const bf16_t*>(dz);
+    const bf16_t* wt = static_cast<const bf16_t*>(WT);
+    bf16_t* g = static_cast<bf16_t*>(grad);
+    if (t.bm == 256) return dh_bf16<256, 256>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
+    return dh_bf16<128, 128>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
+  }
+  const int tm = (R + kVT - 1) / kVT, tn = (d + kVT - 1) / kVT;
+  KernelTimer tt(K_CE_BWD_DH, s);
+  hipLaunchKernelGGL(ce_dh_f32_kernel, dim3(tm * tn), dim3(256), 0, s, static_cast<const float*>(dz),
+                     ldz, static_cast<const float*>(W), r0, R, d, c0, K, V - c0, tm,
+                     static_cast<float*>(grad), first ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace attt

@@ -1,0 +1,174 @@
+// Host-side interfaces between the C ABI layer (api.cpp) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace attt {
+
+// ---- kernel timing ---------------------------------------------------------------------
+enum KernelId {
+  K_NGRAM_BUILD = 0,
+  K_NGRAM_COUNT,
+  K_NGRAM_WEIGHT,
+  K_CE_FWD,
+  K_CE_ROW_REDUCE,
+  K_CE_LOSS,
+  K_CE_HEAD_T,
+  K_CE_BWD_DZ,
+  K_CE_BWD_DH,
+  K_LORA_U,
+  K_LORA_DADB,
+  K_LORA_REDUCE,
+  K_NUM_KERNELS
+};
+
+const char* kernel_name(int id);
+bool timing_on();
+void timing_record(int id, hipEvent_t start, hipEvent_t stop);
+
+// Brackets one launch with events on its stream when timing is enabled.
+struct KernelTimer {
+  int id;
+  hipStream_t stream;
+  hipEvent_t a = nullptr, b = nullptr;
+  KernelTimer(int id_, hipStream_t s) : id(id_), stream(s) {
+    if (timing_on() && hipEventCreate(&a) == hipSuccess && hipEventCreate(&b) == hipSuccess)
+      (void)hipEventRecord(a, stream);
+    else
+      a = b = nullptr;
+  }
+  ~KernelTimer() {
+    if (a && b) {
+      (void)hipEventRecord(b, stream);
+      timing_record(id, a, b);
+    }
+  }
+};
+
+// ---- n-gram ----------------------------------------------------------------------------
+constexpr int kQMax = 4096;        // query n-gram starts per partition
+constexpr int kMaxSlots = 8192;    // table slots per partition (load factor <= 1/2)
+constexpr int kPartBatch = 32;     // partitions per launch (kernel-argument descriptors)
+constexpr int kEpBatch = 64;       // episodes per launch
+
+struct NgramPart {
+  int64_t tok_base;     // first update token of the episode in `tokens`
+  int64_t hist_base;    // first history token of the episode in `history`
+  int64_t table_off;    // first slot of this partition's table (uint2 units)
+  uint32_t count_off;   // first counter of this partition (uint32 units)
+  int32_t hist_ngrams;  // history n-gram starts of the episode: max(0, H_e - n + 1)
+  int32_t q0;           // first query start of this partition, relative to the episode
+  int32_t qn;           // query starts in this partition, 1 .. kQMax
+  int32_t slots;        // power of two, >= 2 * qn
+  int32_t chunk_begin;  // first count-kernel block of this partition within the launch
+  int32_t chunks;       // count-kernel blocks of this partition (0 when hist_ngrams == 0)
+  int32_t pad;
+};
+
+struct NgramPartBatch {
+  int32_t count;
+  int32_t pad;
+  NgramPart p[kPartBatch];
+};
+
+struct NgramEp {
+  int64_t tok_base;
+  int32_t L;
+  int32_t block_begin;
+};
+
+struct NgramEpBatch {
+  int32_t count;
+  int32_t pad;
+  NgramEp e[kEpBatch];
+};
+
+size_t ngram_build_lds(int slots, int n);
+size_t ngram_count_lds(int slots, int n);
+hipError_t launch_ngram_build(const NgramPartBatch& b, int max_slots, const int32_t* tokens, int n,
+                              uint2* tables, uint32_t* counts, uint32_t* qcell, hipStream_t s);
+hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max_slots,
+                              const int32_t* history, const int32_t* tokens, int n,
+                              const uint2* tables, uint32_t* counts, hipStream_t s);
+hipError_t launch_ngram_weight(const NgramEpBatch& b, int total_blocks, int n, float w_min,
+                               const uint32_t* counts, const uint32_t* qcell, uint32_t* exposure,
+                               float* weights, hipStream_t s);
+
+// ---- weighted cross-entropy ------------------------------------------------------------
+struct CeEp {
+  int64_t row0;       // first row of the episode
+  int32_t L;          // rows of the episode
+  int32_t block_begin;
+};
+
+struct CeEpBatch {
+  int32_t count;
+  int32_t first;  // index of e[0] among all episodes of the call
+  CeEp e[kEpBatch];
+};
+
+// Tile shapes of the LM-head GEMMs (bf16 MFMA path: 256x256 or 128x128; f32 path: 64x64).
+struct CeGemmShape {
+  int bm, bn;
+};
+
+// Forward: per (row, vocab tile) partial (max, sum exp) and the label logit.
+hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
+                         const int32_t* labels, int N, int d, int V, float2* partials, int n_vb,
+                         float* label_logit, hipStream_t s);
+hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const float2* partials,
+                                int n_vb, const float* label_logit, const float* weights,
+                                float* lse, float* coef, float* rowloss, hipStream_t s);
+hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, hipStream_t s);
+// W [V, d] -> WT [d, Vp] (bf16 only), zero columns V .. Vp-1.
+hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* WT, hipStream_t s);
+// dZ chunk: rows [r0, r0+R) x vocab [c0, c0+Vc) of coef * (softmax - onehot), into
+// staging [R, ldz] (dtype), zero past V.
+hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
+                            const int32_t* labels, const float* lse, const float* coef, int r0,
+                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, hipStream_t s);
+// dH rows [r0, r0+R) (+)= dZ chunk . W[c0 : c0+K]: f32 path reads W [V, d]; bf16 path reads
+// WT [d, Vp]. first: no accumulator read; last: write grad (dtype) instead of acc (f32).
+hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
+                            const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
+                            float* acc, void* grad, bool first, bool last, hipStream_t s);
+
+// ---- LoRA ------------------------------------------------------------------------------
+constexpr int kLoraBatch = 16;
+
+struct LoraJob {
+  const void* x;
+  const void* dy;
+  const void* A;
+  const void* B;
+  float* dA;
+  float* dB;
+  int64_t ut_off;    // workspace byte offset of s*U^T  [rp, rows_pad] (dtype)
+  int64_t dut_off;   // workspace byte offset of s*(dy B)^T [rp, rows_pad] (dtype)
+  int64_t pa_off;    // workspace byte offset of dA partials [splits, rp, d_in] f32
+  int64_t pb_off;    // workspace byte offset of dB partials [splits, rp, d_out] f32
+  int32_t rows, rows_pad, d_in, d_out, rank, rp, splits;
+  float scale;
+  int32_t b1_begin;  // first pass-1 block (U and dU row tiles)
+  int32_t b2_begin;  // first pass-2 block (dA / dB column blocks x splits)
+  int32_t b3_begin;  // first reduce block
+  int32_t pad;
+};
+
+struct LoraBatch {
+  int32_t count;
+  int32_t pad;
+  LoraJob j[kLoraBatch];
+};
+
+constexpr int kLoraRowTile = 128;   // pass-1 rows per block
+constexpr int kLoraColTile = 64;    // pass-2 output columns per block
+constexpr int kLoraTStep = 32;      // pass-2 contraction step over rows
+
+hipError_t launch_lora_pass1(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+hipError_t launch_lora_pass2(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+hipError_t launch_lora_reduce(const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+
+}  // namespace attt

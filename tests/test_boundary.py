@@ -1,0 +1,140 @@
+"""The C-ABI boundary without a GPU: the library loads, exports every function the header
+declares, and rejects invalid arguments on the host (before any HIP call) with the
+documented status codes. No call here reaches a kernel launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_03441_amd as attt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "attt.h")
+FAKE = ctypes.c_void_p(0x7F0000000000)        # never dereferenced: validation fails first
+FAKE_WS = ctypes.c_void_p(0x7F0000001000)      # 256-byte aligned
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(attt.lib_path()):
+        pytest.fail("libattt.so is not built; run __graft_entry__.build()")
+    return attt.load()
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(attt_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_declares_the_three_calls():
+    names = _declared()
+    for n in ("attt_ngram_weights", "attt_weighted_ce_fwd_bwd", "attt_lora_grad",
+              "attt_ngram_workspace_size", "attt_ce_workspace_size", "attt_lora_workspace_size"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    missing = [n for n in _declared() if not hasattr(L, n)]
+    assert not missing, missing
+
+
+def test_status_strings_and_version(L):
+    assert L.attt_status_string(0) == b"ok"
+    assert L.attt_status_string(2) == b"workspace too small"
+    assert L.attt_version() >= 100
+    names = attt.kernel_names()
+    assert "ce_fwd_lse" in names and "ngram_count" in names and "lora_dadb" in names
+
+
+def _off(a):
+    arr = np.asarray(a, np.int64)
+    return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def _ngram(L, hoff, toff, n=3, w_min=0.05, ws=FAKE_WS, ws_bytes=1 << 30):
+    _, hp = _off(hoff)
+    _, tp = _off(toff)
+    return L.attt_ngram_weights(FAKE, hp, FAKE, tp, len(hoff) - 1, n, w_min, None, FAKE, ws, ws_bytes, None)
+
+
+def test_ngram_validation(L):
+    assert _ngram(L, [0, 10], [0, 5], n=0) == attt.EINVAL
+    assert _ngram(L, [0, 10], [0, 5], n=17) == attt.EINVAL
+    assert b"n must be" in L.attt_last_error()
+    assert _ngram(L, [0, 10], [0, 5], w_min=0.0) == attt.EINVAL
+    assert _ngram(L, [0, 10], [0, 5], w_min=1.5) == attt.EINVAL
+    assert _ngram(L, [0, 10], [0, 5], w_min=float("nan")) == attt.EINVAL
+    assert _ngram(L, [0, 10, 4], [0, 5, 6]) == attt.EINVAL          # decreasing
+    assert _ngram(L, [1, 10], [0, 5]) == attt.EINVAL                # must start at 0
+    assert _ngram(L, [0, 10], [0, 5], ws_bytes=8) == attt.ENOSPACE
+    assert _ngram(L, [0, 10], [0, 5], ws=ctypes.c_void_p(0x7F0000001010)) == attt.EINVAL
+    _, hp = _off([0, 10])
+    _, tp = _off([0, 5])
+    assert L.attt_ngram_weights(FAKE, hp, FAKE, tp, 0, 3, 0.05, None, FAKE, FAKE_WS, 1 << 30, None) == attt.EINVAL
+
+
+def test_ngram_workspace_size_grows_with_update_length():
+    small = attt.ngram_workspace_size([0, 100], [0, 64], 3)
+    big = attt.ngram_workspace_size([0, 100], [0, 20000], 3)
+    multi = attt.ngram_workspace_size([0, 100, 200], [0, 20000, 40000], 3)
+    assert 0 < small < big < multi
+    assert small % 256 == 0 and big % 256 == 0
+    with pytest.raises(attt.AtttError):
+        attt.ngram_workspace_size([0, 100], [0, 64], 0)
+
+
+def _ce(L, N=16, d=64, V=100, dtype=1, E=1, off=(0, 16), loss=FAKE, hidden=FAKE, ws_bytes=1 << 40,
+        grad=FAKE):
+    _, op = _off(off) if off is not None else (None, None)
+    return L.attt_weighted_ce_fwd_bwd(hidden, FAKE, FAKE, FAKE, op, E, N, d, V, dtype, loss, None, grad,
+                                      FAKE_WS, ws_bytes, None)
+
+
+def test_ce_validation(L):
+    assert _ce(L, d=60) == attt.EINVAL                    # d % 8
+    assert _ce(L, dtype=7) == attt.EINVAL
+    assert _ce(L, V=0) == attt.EINVAL
+    assert _ce(L, off=(0, 15)) == attt.EINVAL             # offsets must end at N
+    assert _ce(L, E=2, off=None) == attt.EINVAL           # NULL offsets only for one episode
+    assert _ce(L, E=2, off=(0, 9, 8)) == attt.EINVAL      # decreasing
+    assert _ce(L, loss=None) == attt.EINVAL
+    assert _ce(L, hidden=ctypes.c_void_p(0x7F0000000008)) == attt.EINVAL   # misaligned
+    assert _ce(L, ws_bytes=100) == attt.ENOSPACE
+
+
+def test_ce_workspace_sizes():
+    fwd = attt.ce_workspace_size(8192, 4096, 128256, attt.BF16, want_grad=False)
+    bwd = attt.ce_workspace_size(8192, 4096, 128256, attt.BF16, want_grad=True)
+    assert 0 < fwd < bwd
+    # the backward stages one bounded vocab chunk, never the full N x V gradient
+    assert bwd - fwd < 8192 * 128256 * 2
+    assert attt.ce_workspace_size(4, 8, 3, attt.F32) >= 256
+
+
+def _lora(L, **kw):
+    p = dict(x=FAKE, dy=FAKE, A=FAKE, B=FAKE, dA=FAKE, dB=FAKE, rows=32, d_in=64, d_out=64, rank=8,
+             scale=2.0)
+    p.update(kw)
+    arr = (attt.LoraProblem * 1)(attt.LoraProblem(**p))
+    return L.attt_lora_grad(arr, 1, attt.BF16, FAKE_WS, 1 << 30, None)
+
+
+def test_lora_validation(L):
+    assert _lora(L, rank=0) == attt.EINVAL
+    assert _lora(L, rank=65) == attt.EINVAL
+    assert _lora(L, d_in=60) == attt.EINVAL
+    assert _lora(L, d_out=0) == attt.EINVAL
+    assert _lora(L, dA=None) == attt.EINVAL
+    assert _lora(L, x=ctypes.c_void_p(0x7F0000000004)) == attt.EINVAL
+    assert _lora(L, scale=float("inf")) == attt.EINVAL
+    arr = (attt.LoraProblem * 1)()
+    assert L.attt_lora_grad(arr, 1, 5, FAKE_WS, 1 << 30, None) == attt.EINVAL
+
+
+def test_timing_api_without_launches(L):
+    attt.timing_reset()
+    assert attt.timing_read("ce_fwd_lse") == (0.0, 0)
+    with pytest.raises(attt.AtttError):
+        attt.timing_read("no_such_kernel")

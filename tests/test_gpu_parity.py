@@ -1,0 +1,278 @@
+"""GPU parity of the three C-ABI calls against the float64 oracle, element by element, at
+sizes the oracle finishes in seconds: the tiny float32 step, the small bf16 model shape,
+ragged tiles and tails, several episodes, and the degenerate cases of the method.
+
+Bars: f and w bit-exact; float32 loss / lse / gradients within 1e-5 relative (normwise
+for gradients); bf16 loss within 2e-2 relative and gradient cosine >= 0.999."""
+import numpy as np
+import pytest
+
+from gpu_util import cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
+from oracle import ce as oce
+from oracle import lora as olora
+from oracle import ngram as ongram
+from workloads import Workload, pack_episodes, random_dense
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-5
+BF16_LOSS_TOL = 2e-2
+BF16_COS = 0.999
+
+
+# ------------------------------------------------------------------------------------------
+# n-gram exposure and weights
+# ------------------------------------------------------------------------------------------
+def _run_ngram(attt, tok, n, w_min):
+    f, w = attt.ngram_weights(dev_i32(tok["hist_flat"]), tok["hist_off"], dev_i32(tok["tok_flat"]),
+                              tok["tok_off"], n=n, w_min=w_min)
+    return host(f).view(np.uint32), host(w)
+
+
+def _check_ngram(attt, tok, n, w_min=0.05):
+    f, w = _run_ngram(attt, tok, n, w_min)
+    fo, wo = ongram.ngram_weights(tok["history"], tok["updates"], n, w_min)
+    assert f.tolist() == fo.tolist()
+    assert w.view(np.uint32).tolist() == wo.view(np.uint32).tolist()
+    return fo
+
+
+@pytest.mark.parametrize("key", ["c1", "c2"])
+def test_ngram_configs(attt, key):
+    wl = Workload(key)
+    note(f"ngram {key}")
+    fo = _check_ngram(attt, wl.tokens(), wl.cfg.n, wl.cfg.w_min)
+    assert fo.max() > 0
+
+
+def _rand_tokens(rng, sizes, vocab):
+    return [rng.integers(0, vocab, s, dtype=np.int32) for s in sizes]
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 16])
+def test_ngram_edge_cases(attt, n):
+    rng = np.random.default_rng(40 + n)
+    note(f"ngram edges n={n}")
+    # episodes: empty history, update shorter than n, empty update, normal, heavy repetition
+    hist = _rand_tokens(rng, [0, 50, 300, 1000, 0], 6)
+    upd = _rand_tokens(rng, [100, max(n - 1, 0), 0, 777, 5], 6)
+    hist[3] = np.concatenate([hist[3], np.tile(upd[3][:40], 20)])
+    _check_ngram(attt, pack_episodes(hist, upd), n)
+
+
+def test_ngram_w_min_values(attt):
+    rng = np.random.default_rng(7)
+    x = rng.integers(0, 3, 600, dtype=np.int32)
+    H = np.tile(x[:50], 400)
+    tok = pack_episodes([H], [x])
+    for w_min in (2.0 ** -20, 0.05, 0.3, 1.0):
+        note(f"ngram w_min={w_min}")
+        _check_ngram(attt, tok, 2, w_min)
+
+
+def test_ngram_multiple_partitions_and_ragged(attt):
+    # an update longer than one partition (4096 query starts) with a ragged tail
+    rng = np.random.default_rng(9)
+    hist = [rng.integers(0, 50, 20000, dtype=np.int32)]
+    x = rng.integers(0, 50, 9001, dtype=np.int32)
+    x[100:700] = hist[0][5000:5600]
+    x[8000:9001] = hist[0][1000:2001]
+    note("ngram partitions")
+    _check_ngram(attt, pack_episodes(hist, [x]), 3)
+
+
+def test_ngram_boundary_reading_and_overlap(attt):
+    # previous updates [10 11][12 13]: (11,12) straddles them and counts; (7,7) in 7 7 7 7 counts 3
+    tok = pack_episodes([np.array([10, 11, 12, 13], np.int32), np.array([7, 7, 7, 7], np.int32)],
+                        [np.array([11, 12], np.int32), np.array([7, 7], np.int32)])
+    f, w = _run_ngram(attt, tok, 2, 0.05)
+    assert f.tolist() == [1, 1, 3, 3]
+    assert w.tolist() == [0.5, 0.5, 0.25, 0.25]
+
+
+def test_ngram_deterministic(attt):
+    tok = Workload("c2").tokens()
+    a = _run_ngram(attt, tok, 3, 0.05)
+    b = _run_ngram(attt, tok, 3, 0.05)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1].view(np.uint32), b[1].view(np.uint32))
+
+
+# ------------------------------------------------------------------------------------------
+# weighted cross-entropy
+# ------------------------------------------------------------------------------------------
+def _ce_case(attt, h, W, labels, weights, off, bf16):
+    th, tW = dev_dense(h), dev_dense(W)
+    loss, lse, dH = attt.weighted_ce_fwd_bwd(th, tW, dev_i32(labels), dev_f32(weights), row_offsets=off)
+    lo, lseo, dHo = oce.weighted_ce(h.f32, W.f32, labels, weights, off)
+    loss, lse, dH = host(loss), host(lse), host(dH)
+    if bf16:
+        assert np.all(np.abs(loss - lo) <= BF16_LOSS_TOL * np.abs(lo)), (loss, lo)
+        assert cosine(dH, dHo) >= BF16_COS
+        for r in range(0, len(dHo), max(1, len(dHo) // 64)):
+            assert cosine(dH[r], dHo[r]) >= 0.99
+    else:
+        assert np.all(np.abs(loss - lo) <= F32_TOL * np.abs(lo)), (loss, lo)
+        assert rel_norm(dH, dHo) <= F32_TOL
+    assert np.max(np.abs(lse - lseo) / np.abs(lseo)) <= (1e-4 if bf16 else F32_TOL)
+    return loss, lse, dH
+
+
+def test_ce_tiny_f32(attt):
+    wl = Workload("c1")
+    ce = wl.ce()
+    f, w = ongram.ngram_weights(wl.tokens()["history"], wl.tokens()["updates"], 4, 0.05)
+    note("ce c1 f32")
+    _ce_case(attt, ce["h"], ce["W"], ce["labels"], w, ce["row_offsets"], False)
+
+
+def test_ce_small_bf16(attt):
+    wl = Workload("c2")
+    ce = wl.ce()
+    f, w = ongram.ngram_weights(wl.tokens()["history"], wl.tokens()["updates"], 3, 0.05)
+    note("ce c2 bf16")
+    _ce_case(attt, ce["h"], ce["W"], ce["labels"], w, ce["row_offsets"], True)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+@pytest.mark.parametrize("shape", [(300, 200, 1000), (77, 64, 9000), (513, 96, 8200)])
+def test_ce_ragged(attt, bf16, shape):
+    N, d, V = shape
+    note(f"ce ragged {shape} bf16={bf16}")
+    h = random_dense((N, d), 1.0, bf16, 11)
+    W = random_dense((V, d), 0.05, bf16, 12)
+    rng = np.random.default_rng(13)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    labels[:3] = [0, V - 1, V // 2]
+    weights = rng.choice(np.array([1.0, 0.5, 0.25, 0.05], np.float32), N)
+    off = np.array([0, N // 3, N // 3, N], np.int64)          # includes an empty episode
+    _ce_case(attt, h, W, labels, weights, off, bf16)
+
+
+def test_ce_unit_weights_is_mean_ce(attt):
+    N, d, V = 128, 64, 500
+    h = random_dense((N, d), 1.0, False, 21)
+    W = random_dense((V, d), 0.1, False, 22)
+    labels = np.random.default_rng(23).integers(0, V, N).astype(np.int32)
+    loss, lse, _ = attt.weighted_ce_fwd_bwd(dev_dense(h), dev_dense(W), dev_i32(labels),
+                                            dev_f32(np.ones(N, np.float32)), want_grad=False)
+    z = h.f32.astype(np.float64) @ W.f32.astype(np.float64).T
+    m = z.max(1)
+    ce = m + np.log(np.exp(z - m[:, None]).sum(1)) - z[np.arange(N), labels]
+    assert abs(host(loss)[0] - ce.mean()) <= F32_TOL * ce.mean()
+
+
+def test_ce_forward_only_matches(attt):
+    wl = Workload("c1")
+    ce = wl.ce()
+    w = np.full(512, 0.5, np.float32)
+    a = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
+                                 dev_f32(w), want_grad=False)
+    b = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
+                                 dev_f32(w), want_grad=True)
+    assert host(a[0]).tobytes() == host(b[0]).tobytes()
+
+
+def test_ce_deterministic(attt):
+    wl = Workload("c2")
+    ce = wl.ce()
+    w = np.random.default_rng(5).uniform(0.05, 1, 2048).astype(np.float32)
+    args = (dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]), dev_f32(w))
+    r1 = [host(t) for t in attt.weighted_ce_fwd_bwd(*args)]
+    r2 = [host(t) for t in attt.weighted_ce_fwd_bwd(*args)]
+    for a, b in zip(r1, r2):
+        assert a.tobytes() == b.tobytes()
+
+
+# ------------------------------------------------------------------------------------------
+# LoRA gradients
+# ------------------------------------------------------------------------------------------
+def _lora_case(attt, problems, bf16, zero_dA=False):
+    import torch
+    dev = []
+    for p in problems:
+        r, d_in, d_out = p["A"].shape[0], p["A"].shape[1], p["B"].shape[0]
+        dev.append(dict(x=dev_dense(p["x"]), dy=dev_dense(p["dy"]), A=dev_dense(p["A"]),
+                        B=dev_dense(p["B"]), scale=p["scale"],
+                        dA=torch.zeros(r, d_in, dtype=torch.float32, device="cuda"),
+                        dB=torch.zeros(d_out, r, dtype=torch.float32, device="cuda")))
+    attt.lora_grad(dev)
+    for p, q in zip(problems, dev):
+        dAo, dBo = olora.lora_grad(p["x"].f32, p["dy"].f32, p["A"].f32, p["B"].f32, p["scale"])
+        dA, dB = host(q["dA"]), host(q["dB"])
+        if zero_dA:
+            assert np.all(dA == 0.0)
+        if bf16:
+            if np.any(dAo != 0):
+                assert cosine(dA, dAo) >= BF16_COS
+            assert cosine(dB, dBo) >= BF16_COS
+        else:
+            if np.any(dAo != 0):
+                assert rel_norm(dA, dAo) <= F32_TOL
+            assert rel_norm(dB, dBo) <= F32_TOL
+    return dev
+
+
+def test_lora_tiny_f32(attt):
+    note("lora c1")
+    _lora_case(attt, Workload("c1").lora(), False, zero_dA=True)
+
+
+def test_lora_small_bf16(attt):
+    note("lora c2")
+    _lora_case(attt, Workload("c2").lora(), True)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+@pytest.mark.parametrize("rank", [1, 3, 8, 16, 32, 64])
+def test_lora_ranks_and_ragged_rows(attt, bf16, rank):
+    note(f"lora rank={rank} bf16={bf16}")
+    probs = []
+    for i, (rows, d_in, d_out) in enumerate([(300, 200, 72), (1, 64, 64), (1000, 136, 520)]):
+        s = 100 * rank + 10 * i
+        probs.append(dict(x=random_dense((rows, d_in), 1.0, bf16, s), dy=random_dense((rows, d_out), 0.1, bf16, s + 1),
+                          A=random_dense((rank, d_in), 0.05, bf16, s + 2),
+                          B=random_dense((d_out, rank), 0.05, bf16, s + 3), scale=16.0 / rank))
+    _lora_case(attt, probs, bf16)
+
+
+def test_lora_accumulates(attt):
+    import torch
+    probs = Workload("c1").lora()
+    p = probs[0]
+    B = random_dense(p["B"].shape, 0.05, False, 3)
+    q = dict(x=dev_dense(p["x"]), dy=dev_dense(p["dy"]), A=dev_dense(p["A"]), B=dev_dense(B),
+             scale=p["scale"], dA=torch.ones(p["A"].shape, dtype=torch.float32, device="cuda"),
+             dB=torch.ones(p["B"].shape, dtype=torch.float32, device="cuda"))
+    attt.lora_grad([q])
+    attt.lora_grad([q])
+    dAo, dBo = olora.lora_grad(p["x"].f32, p["dy"].f32, p["A"].f32, B.f32, p["scale"])
+    assert rel_norm(host(q["dA"]) - 1.0, 2 * dAo) <= F32_TOL
+    assert rel_norm(host(q["dB"]) - 1.0, 2 * dBo) <= F32_TOL
+
+
+# ------------------------------------------------------------------------------------------
+# the chained update step
+# ------------------------------------------------------------------------------------------
+def test_chained_step_tiny_f32(attt):
+    """weights -> CE -> LoRA of the output projection with dy = dH, all on the GPU."""
+    import torch
+    from oracle import step as ostep
+    wl = Workload("c1")
+    tok, ce, probs = wl.tokens(), wl.ce(), wl.lora()
+    B = random_dense(probs[0]["B"].shape, 0.05, False, 99)      # non-zero B so dA != 0
+    probs = [dict(probs[0], name="e0.o", B=B)]
+    note("chained c1")
+    _, w = attt.ngram_weights(dev_i32(tok["hist_flat"]), tok["hist_off"], dev_i32(tok["tok_flat"]),
+                              tok["tok_off"], n=4, w_min=0.05)
+    loss, _, dH = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
+                                           w, row_offsets=ce["row_offsets"])
+    p = probs[0]
+    q = dict(x=dev_dense(p["x"]), dy=dH, A=dev_dense(p["A"]), B=dev_dense(B), scale=p["scale"],
+             dA=torch.zeros(p["A"].shape, dtype=torch.float32, device="cuda"),
+             dB=torch.zeros(p["B"].shape, dtype=torch.float32, device="cuda"))
+    attt.lora_grad([q])
+    out = ostep.update_step(tok, ce, probs, 4, 0.05)
+    assert abs(host(loss)[0] - out["loss"][0]) <= F32_TOL * abs(out["loss"][0])
+    dAo, dBo = out["lora"][0]
+    assert rel_norm(host(q["dA"]), dAo) <= F32_TOL
+    assert rel_norm(host(q["dB"]), dBo) <= F32_TOL
