@@ -1,0 +1,248 @@
+"""Throughput of the aTTT in-episode update step on one MI355X.
+
+One step = the whole hot path over one batch of synthetic inputs resident in HBM:
+  1. n-gram exposure and weights of the update tokens against the episode history (Eq. 8-9)
+  2. token-weighted CE through the LM head, loss and dL/dh (Eq. 10)
+  3. LoRA dA / dB of q, k, v, o; the o projection takes dL/dh as its upstream gradient
+all through the C ABI on one stream. Default workload: the Llama-8B-shaped bf16 step
+(8192 update tokens, 32 previous updates of 4096 tokens, n = 4, d = 4096, V = 128256,
+rank-16 LoRA on q/k/v/o 4096x4096 / 4096x1024).
+
+Prints one JSON line: update tokens/s, the roofline of the dominant kernel (per-launch
+durations from HIP events recorded on the launch stream inside the timed region), and
+the CPU oracle timed on a bounded sample on this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+METRIC = "aTTT update tokens/s (weights+weighted CE+LoRA grad); %MFMA and %HBM peak"
+PEAK_BF16 = 2.5e15       # dense bf16 MFMA, FLOP/s
+PEAK_F32_MFMA = 157.3e12
+PEAK_HBM = 8.0e12        # bytes/s
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c3", help="workload key c1..c5 (default: Llama-8B shape)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=128, help="CE rows the oracle sample covers")
+    return ap.parse_args()
+
+
+class Step:
+    """Device-resident inputs, outputs and workspaces of one update step."""
+
+    def __init__(self, wl, attt, torch):
+        from gpu_util import dev_dense, dev_i32
+        cfg = wl.cfg
+        self.cfg, self.attt, self.torch = cfg, attt, torch
+        t0 = time.time()
+        tok, ce, probs = wl.tokens(), wl.ce(), wl.lora()
+        log(f"inputs generated on host in {time.time() - t0:.1f}s")
+        self.tok = tok
+        self.hist = dev_i32(tok["hist_flat"])
+        self.toks = dev_i32(tok["tok_flat"])
+        self.h = dev_dense(ce["h"])
+        self.W = dev_dense(ce["W"])
+        self.labels = dev_i32(ce["labels"])
+        self.row_off = ce["row_offsets"]
+        T = int(tok["tok_off"][-1])
+        dev = self.h.device
+        self.f = torch.empty(T, dtype=torch.int32, device=dev)
+        self.w = torch.empty(T, dtype=torch.float32, device=dev)
+        E = cfg.episodes
+        self.loss = torch.empty(E, dtype=torch.float32, device=dev)
+        self.lse = torch.empty(T, dtype=torch.float32, device=dev)
+        self.dH = torch.empty_like(self.h)
+        xs = {}
+        self.problems = []
+        off = self.row_off
+        for p in probs:
+            key = id(p["x"])
+            if key not in xs:
+                xs[key] = dev_dense(p["x"])
+            e = p["episode"]
+            chained = p["name"].endswith(".o")
+            dy = self.dH[int(off[e]):int(off[e + 1])] if chained else dev_dense(p["dy"])
+            r = p["rank"]
+            self.problems.append(dict(x=xs[key], dy=dy, A=dev_dense(p["A"]), B=dev_dense(p["B"]),
+                                      scale=p["scale"],
+                                      dA=torch.zeros(r, p["d_in"], dtype=torch.float32, device=dev),
+                                      dB=torch.zeros(p["d_out"], r, dtype=torch.float32, device=dev)))
+        self.probs_host = probs
+        dt = attt.BF16 if cfg.dtype == "bf16" else attt.F32
+        u8 = torch.uint8
+        self.ws_ngram = torch.empty(attt.ngram_workspace_size(tok["hist_off"], tok["tok_off"], cfg.n), dtype=u8, device=dev)
+        self.ws_ce = torch.empty(attt.ce_workspace_size(T, cfg.d, cfg.vocab, dt), dtype=u8, device=dev)
+        self.ws_lora = torch.empty(attt.lora_workspace_size(self.problems, dt), dtype=u8, device=dev)
+        log(f"workspaces: ngram {self.ws_ngram.numel() / 2**20:.1f} MiB, ce {self.ws_ce.numel() / 2**20:.1f} MiB, "
+            f"lora {self.ws_lora.numel() / 2**20:.1f} MiB")
+
+    def run(self):
+        a, cfg = self.attt, self.cfg
+        a.ngram_weights(self.hist, self.tok["hist_off"], self.toks, self.tok["tok_off"], n=cfg.n,
+                        w_min=cfg.w_min, workspace=self.ws_ngram, out=(self.f, self.w))
+        a.weighted_ce_fwd_bwd(self.h, self.W, self.labels, self.w, row_offsets=self.row_off,
+                              workspace=self.ws_ce, out=(self.loss, self.lse, self.dH))
+        a.lora_grad(self.problems, workspace=self.ws_lora)
+
+
+def algorithmic(cfg, tok, probs):
+    """Algorithmic work per step of each part (what the method needs, not what a design
+    executes): flops of the contractions and compulsory HBM bytes."""
+    N, d, V = cfg.rows, cfg.d, cfg.vocab
+    esz = 2 if cfg.dtype == "bf16" else 4
+    H = int(tok["hist_off"][-1])
+    ngram_bytes = 4 * H + 4 * N + 8 * N          # read history and tokens, write f and w
+    lora_bytes, lora_flops, seen = 0, 0, set()
+    for p in probs:
+        if id(p["x"]) not in seen:
+            seen.add(id(p["x"]))
+            lora_bytes += p["x"].f32.size * esz
+        r, di, do, rows = p["rank"], p["d_in"], p["d_out"], p["rows"]
+        lora_bytes += rows * do * esz + (r * di + do * r) * esz + 2 * 4 * (r * di + do * r)
+        lora_flops += 4 * rows * r * (di + do)
+    return dict(ce_flops_fwd=2.0 * N * V * d, ce_flops_bwd=2.0 * N * V * d,
+                ngram_bytes=float(ngram_bytes), lora_bytes=float(lora_bytes), lora_flops=float(lora_flops))
+
+
+def cpu_baseline(wl, rows):
+    """The oracle as it stands on this host: full n-gram and LoRA parts, the CE part on the
+    first `rows` update rows (rows are independent) scaled to all rows."""
+    from oracle import ce as oce
+    from oracle import lora as olora
+    from oracle import ngram as ongram
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    cfg = wl.cfg
+    tok, ce, probs = wl.tokens(), wl.ce(), wl.lora()
+    N = cfg.rows
+    t = time.perf_counter()
+    f, w = ongram.ngram_weights(tok["history"], tok["updates"], cfg.n, cfg.w_min)
+    t_ng = time.perf_counter() - t
+    t = time.perf_counter()
+    W64 = np.asarray(ce["W"].f32, np.float64)
+    t_conv = time.perf_counter() - t
+    rows = min(rows, N)
+    t = time.perf_counter()
+    oce.ce_rows(ce["h"].f32, W64, ce["labels"], w, ce["row_offsets"], np.arange(rows))
+    t_rows = time.perf_counter() - t
+    del W64
+    t = time.perf_counter()
+    for p in probs:
+        olora.lora_grad(p["x"].f32, p["dy"].f32, p["A"].f32, p["B"].f32, p["scale"])
+    t_lora = time.perf_counter() - t
+    t_ce = t_conv + t_rows * N / rows
+    total = t_ng + t_ce + t_lora
+    return {"value": N / total, "unit": "update tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"float64 numpy oracle: n-gram weights and LoRA grads in full, CE fwd+bwd on "
+                       f"{rows} of {N} rows scaled by {N / rows:.0f} (rows are independent); "
+                       f"ngram {t_ng:.2f}s, ce {t_ce:.1f}s est, lora {t_lora:.2f}s")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the update step of one episode group runs on a single "
+              "MI355X and this build has no multi-GPU path (--gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2607_03441_amd as attt
+    from workloads import Workload
+
+    attt.load()
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    wl = Workload(args.config)
+    cfg = wl.cfg
+    step = Step(wl, attt, torch)
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    attt.timing_enable(True)
+    attt.timing_reset()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step.run()
+    stop.record()
+    torch.cuda.synchronize()
+    attt.timing_enable(False)
+    ms_step = start.elapsed_time(stop) / args.steps
+    kern = {}
+    for name in attt.kernel_names():
+        ms, n = attt.timing_read(name)
+        if n:
+            kern[name] = {"ms_per_step": ms / args.steps, "launches_per_step": n / args.steps,
+                          "avg_launch_ms": ms / n}
+    log("kernels: " + ", ".join(f"{k} {v['ms_per_step']:.3f}ms" for k, v in kern.items()))
+
+    alg = algorithmic(cfg, wl.tokens(), wl.lora())
+    bf16 = cfg.dtype == "bf16"
+    peak = PEAK_BF16 if bf16 else PEAK_F32_MFMA
+    ce_kernels = ("ce_fwd_lse", "ce_bwd_dz", "ce_bwd_dh")
+    dom = max(ce_kernels, key=lambda k: kern.get(k, {}).get("ms_per_step", 0.0))
+    # each of the three LM-head GEMM kernels contracts N x V x d once per step
+    per_step_flops = alg["ce_flops_fwd"]
+    k = kern[dom]
+    per_launch = per_step_flops / k["launches_per_step"]
+    achieved = per_launch / (k["avg_launch_ms"] * 1e-3)
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                "flops_per_launch": per_launch}
+    ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
+                ("ce_fwd_lse", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh"))
+    ng_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("ngram_build", "ngram_count", "ngram_weight"))
+    lo_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("lora_u_du", "lora_dadb", "lora_reduce"))
+    parts = {
+        "ce_pass": {"ms": ce_ms, "algorithmic_tflops": 4 * cfg.rows * cfg.vocab * cfg.d / (ce_ms * 1e-3) / 1e12,
+                    "frac_of_mfma_peak": 4 * cfg.rows * cfg.vocab * cfg.d / (ce_ms * 1e-3) / peak},
+        "ngram_pass": {"ms": ng_ms, "algorithmic_gbs": alg["ngram_bytes"] / (ng_ms * 1e-3) / 1e9,
+                       "frac_of_hbm_peak": alg["ngram_bytes"] / (ng_ms * 1e-3) / PEAK_HBM},
+        "lora_pass": {"ms": lo_ms, "algorithmic_gbs": alg["lora_bytes"] / (lo_ms * 1e-3) / 1e9,
+                      "frac_of_hbm_peak": alg["lora_bytes"] / (lo_ms * 1e-3) / PEAK_HBM},
+    }
+    out = {
+        "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic (seeded; see workloads/gen.py)",
+        "config": {"workload": cfg.name, "episodes": cfg.episodes, "update_tokens": cfg.rows,
+                   "history_tokens": int(wl.tokens()["hist_off"][-1]), "n": cfg.n, "w_min": cfg.w_min,
+                   "d": cfg.d, "V": cfg.vocab, "lora_rank": cfg.rank,
+                   "lora_projections": [f"{p.name}:{p.d_in}x{p.d_out}" for p in cfg.projections]},
+        "roofline": roofline, "parts": parts, "kernels": kern,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle sample")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

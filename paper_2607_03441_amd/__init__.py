@@ -141,7 +141,7 @@ def ngram_workspace_size(history_offsets, token_offsets, n):
 
 
 def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.05,
-                  want_exposure=True, workspace=None):
+                  want_exposure=True, workspace=None, out=None):
     """Eq. 8-9 for E episodes. history / tokens: int32 device tensors (flat); offsets: host
     int64 sequences of length E+1. Returns (f, w): f as an int32 tensor holding the uint32
     exposure (or None), w float32."""
@@ -156,8 +156,11 @@ def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.
     if tokens.dtype != torch.int32 or history.dtype != torch.int32:
         raise TypeError("history and tokens must be int32")
     T = int(to[-1])
-    f = torch.empty(T, dtype=torch.int32, device=dev) if want_exposure else None
-    w = torch.empty(T, dtype=torch.float32, device=dev)
+    if out is not None:
+        f, w = out
+    else:
+        f = torch.empty(T, dtype=torch.int32, device=dev) if want_exposure else None
+        w = torch.empty(T, dtype=torch.float32, device=dev)
     need = ctypes.c_size_t(0)
     _check(L.attt_ngram_workspace_size(hp, tp, E, n, ctypes.byref(need)))
     ws = _workspace(need.value, dev, workspace)
