@@ -42,7 +42,22 @@ def parse():
     ap.add_argument("--config", default="c3", help="workload key c1..c5 (default: Llama-8B shape)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=128, help="CE rows the oracle sample covers")
+    ap.add_argument("--hbm-calibrate", action="store_true",
+                    help="only run a plain 1 GiB device copy, 4 times: the reference for scaling "
+                         "FETCH_SIZE / WRITE_SIZE counter readings to bytes")
     return ap.parse_args()
+
+
+def hbm_calibrate():
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes": n, "copies": 4}), flush=True)
 
 
 class Step:
@@ -122,6 +137,33 @@ def algorithmic(cfg, tok, probs):
                 ngram_bytes=float(ngram_bytes), lora_bytes=float(lora_bytes), lora_flops=float(lora_flops))
 
 
+KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_"}
+
+
+def counter_traffic(config, kernel):
+    """HBM bytes per dispatch of `kernel` from the committed rocprofv3 counter summary of this
+    workload, or None when there is none or the kernel sources changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{config}_kernels_hbm.md")
+    if not os.path.exists(path):
+        return None
+    rec = None
+    for line in open(path):
+        if line.startswith("traffic-json: "):
+            rec = json.loads(line[len("traffic-json: "):])
+    if rec is None:
+        return None
+    for src, digest in rec["sources"].items():
+        with open(os.path.join(ROOT, src), "rb") as fh:
+            if hashlib.sha256(fh.read()).hexdigest()[:16] != digest:
+                return None
+    prefix = KERNEL_SYMBOL.get(kernel)
+    for name, b in rec["bytes_per_dispatch"].items():
+        if prefix and name.startswith(prefix):
+            return b
+    return None
+
+
 def cpu_baseline(wl, rows):
     """The oracle as it stands on this host: full n-gram and LoRA parts, the CE part on the
     first `rows` update rows (rows are independent) scaled to all rows."""
@@ -161,6 +203,9 @@ def cpu_baseline(wl, rows):
 
 def main():
     args = parse()
+    if args.hbm_calibrate:
+        hbm_calibrate()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the update step of one episode group runs on a single "
               "MI355X and this build has no multi-GPU path (--gpus 1)", file=sys.stderr)
@@ -211,7 +256,8 @@ def main():
     per_launch = per_step_flops / k["launches_per_step"]
     achieved = per_launch / (k["avg_launch_ms"] * 1e-3)
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": peak / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": counter_traffic(args.config, dom),
                 "flops_per_launch": per_launch}
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
                 ("ce_fwd_lse", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh"))
