@@ -32,64 +32,97 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return xcd * q + min(xcd, r) + j;
 }
 
-template <int BM, int BN>
-struct MfmaTile {
+// Tile of workgroup `bid`: each XCD takes a contiguous range of the tile order, and that
+// order walks groups of 8 row tiles column by column, so the ~32 workgroups resident on one
+// XCD cover about 8 row panels x 4 column panels and share them in that XCD's L2.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int t = xcd_remap(bid, tiles_m * tiles_n);
+  constexpr int GM = 8;
+  const int per_group = GM * tiles_n;
+  const int g = t / per_group;
+  const int first = g * GM;
+  const int gm = min(GM, tiles_m - first);
+  const int local = t - g * per_group;
+  tm = first + local % gm;
+  tn = local / gm;
+}
+
+// Workgroup tile BM x BN computed by WGM x WGN waves; each wave owns a (BM/WGM) x (BN/WGN)
+// block of 32x32 MFMA tiles. K advances 64 per stage, two stages in LDS.
+template <int BM_, int BN_, int WGM_, int WGN_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NT = 64 * WGM * WGN;
   static constexpr int BK = 64;
-  static constexpr int TM = BM / 64;  // 32x32 MFMA tiles per wave along rows
-  static constexpr int TN = BN / 64;  // ... along columns
-  static constexpr int AL = BM / 32;  // 16-byte global loads per thread per stage (A)
-  static constexpr int BL = BN / 32;
-  static constexpr int SA = BM * BK;  // bf16 elements per stage
-  static constexpr int SB = BN * BK;
+  static constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int RPL = NT / 8;  // rows one load round covers (8 x 16-byte chunks per row)
+  static constexpr int AL = BM / RPL, BL = BN / RPL;
+  static constexpr int SA = BM * BK, SB = BN * BK;
   static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);
 };
+using CfgBig = Cfg<256, 256, 2, 4>;    // 8 waves, 128x64 per wave
+using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
+
+// Buffer loads return zero for offsets past the descriptor's range: masked lanes use kOOB
+// instead of branching. Valid offsets stay far below kRsrcBytes (a tile spans < 256 rows).
+constexpr uint32_t kOOB = 0x7FFFFFF0u;
+constexpr int kRsrcBytes = 0x40000000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, kRsrcBytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 // acc += A[0:BM, 0:K] * B[0:BN, 0:K]^T, A and B K-contiguous bf16. Rows at or past mval
 // (nval) and K-chunks at or past K read as zero. K % 8 == 0.
-template <int BM, int BN>
+template <class C>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                               const bf16_t* __restrict__ B, int64_t ldb, int nval,
-                                              int K, bf16_t* lds,
-                                              f32x16 (&acc)[BM / 64][BN / 64]) {
-  using T = MfmaTile<BM, BN>;
+                                              int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int lrow = tid >> 3, lch = tid & 7;
 #pragma unroll
-  for (int i = 0; i < T::TM; ++i)
+  for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-    for (int j = 0; j < T::TN; ++j)
+    for (int j = 0; j < C::TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  u32x4 ra[T::AL], rb[T::BL];
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
+  uint32_t aoff[C::AL], boff[C::BL];
+#pragma unroll
+  for (int i = 0; i < C::AL; ++i) {
+    const int row = lrow + C::RPL * i;
+    aoff[i] = row < mval ? (uint32_t)((int64_t)row * lda * 2) + lch * 16 : kOOB;
+  }
+#pragma unroll
+  for (int i = 0; i < C::BL; ++i) {
+    const int row = lrow + C::RPL * i;
+    boff[i] = row < nval ? (uint32_t)((int64_t)row * ldb * 2) + lch * 16 : kOOB;
+  }
+  u32x4 ra[C::AL], rb[C::BL];
   auto gload = [&](int k0) {
-    const int k = k0 + lch * 8;
-    const bool kin = k < K;
+    const bool kin = k0 + lch * 8 < K;
+    const uint32_t kb = (uint32_t)k0 * 2;
 #pragma unroll
-    for (int i = 0; i < T::AL; ++i) {
-      const int row = lrow + 32 * i;
-      ra[i] = (kin && row < mval) ? *reinterpret_cast<const u32x4*>(A + (int64_t)row * lda + k)
-                                  : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < C::AL; ++i) ra[i] = bload16(rA, (kin && aoff[i] != kOOB) ? aoff[i] + kb : kOOB);
 #pragma unroll
-    for (int i = 0; i < T::BL; ++i) {
-      const int row = lrow + 32 * i;
-      rb[i] = (kin && row < nval) ? *reinterpret_cast<const u32x4*>(B + (int64_t)row * ldb + k)
-                                  : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < C::BL; ++i) rb[i] = bload16(rB, (kin && boff[i] != kOOB) ? boff[i] + kb : kOOB);
   };
   auto lstore = [&](int st) {
-    bf16_t* As = lds + st * (T::SA + T::SB);
-    bf16_t* Bs = As + T::SA;
+    bf16_t* As = lds + st * (C::SA + C::SB);
+    bf16_t* Bs = As + C::SA;
 #pragma unroll
-    for (int i = 0; i < T::AL; ++i) {
-      const int row = lrow + 32 * i;
+    for (int i = 0; i < C::AL; ++i) {
+      const int row = lrow + C::RPL * i;
       *reinterpret_cast<u32x4*>(As + row * 64 + ((lch ^ (row & 7)) << 3)) = ra[i];
     }
 #pragma unroll
-    for (int i = 0; i < T::BL; ++i) {
-      const int row = lrow + 32 * i;
+    for (int i = 0; i < C::BL; ++i) {
+      const int row = lrow + C::RPL * i;
       *reinterpret_cast<u32x4*>(Bs + row * 64 + ((lch ^ (row & 7)) << 3)) = rb[i];
     }
   };
@@ -101,27 +134,27 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
   const int l32 = lane & 31, hi = lane >> 5;
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) gload((kt + 1) * 64);
-    const bf16_t* As = lds + (kt & 1) * (T::SA + T::SB);
-    const bf16_t* Bs = As + T::SA;
+    const bf16_t* As = lds + (kt & 1) * (C::SA + C::SB);
+    const bf16_t* Bs = As + C::SA;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int ch = kk * 2 + hi;
       const int sw = (ch ^ (l32 & 7)) << 3;
-      bf16x8 a[T::TM], b[T::TN];
+      bf16x8 a[C::TM], b[C::TN];
 #pragma unroll
-      for (int i = 0; i < T::TM; ++i) {
-        const int r = wm * (BM / 2) + i * 32 + l32;
+      for (int i = 0; i < C::TM; ++i) {
+        const int r = wm * C::WTM + i * 32 + l32;
         a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + r * 64 + sw));
       }
 #pragma unroll
-      for (int j = 0; j < T::TN; ++j) {
-        const int r = wn * (BN / 2) + j * 32 + l32;
+      for (int j = 0; j < C::TN; ++j) {
+        const int r = wn * C::WTN + j * 32 + l32;
         b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + r * 64 + sw));
       }
 #pragma unroll
-      for (int i = 0; i < T::TM; ++i)
+      for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < T::TN; ++j)
+        for (int j = 0; j < C::TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) lstore((kt + 1) & 1);
@@ -136,100 +169,99 @@ __device__ __forceinline__ int mfma_row(int r, int lane) { return ((r >> 2) << 3
 // ------------------------------------------------------------------------------------------
 // bf16 forward: partial (max, sumexp) per (row, BN-wide vocab tile) and the label logit.
 // ------------------------------------------------------------------------------------------
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void ce_fwd_bf16_kernel(const bf16_t* __restrict__ h,
-                                                          const bf16_t* __restrict__ W,
-                                                          const int32_t* __restrict__ labels,
-                                                          int N, int d, int V, int tiles_m,
-                                                          int tiles_n, float2* __restrict__ partials,
-                                                          int n_vb, float* __restrict__ label_logit) {
-  using T = MfmaTile<BM, BN>;
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(const bf16_t* __restrict__ h,
+                                                            const bf16_t* __restrict__ W,
+                                                            const int32_t* __restrict__ labels,
+                                                            int N, int d, int V, int tiles_m,
+                                                            int tiles_n, float2* __restrict__ partials,
+                                                            int n_vb, float* __restrict__ label_logit) {
   extern __shared__ __align__(16) uint8_t smem[];
-  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
-  const int tm = tile % tiles_m, tn = tile / tiles_m;
-  const int m0 = tm * BM, n0 = tn * BN;
-  f32x16 acc[T::TM][T::TN];
-  mfma_mainloop<BM, BN>(h + (int64_t)m0 * d, d, N - m0, W + (int64_t)n0 * d, d, V - n0, d,
-                        reinterpret_cast<bf16_t*>(smem), acc);
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * C::BM, n0 = tn * C::BN;
+  f32x16 acc[C::TM][C::TN];
+  mfma_mainloop<C>(h + (int64_t)m0 * d, d, N - m0, W + (int64_t)n0 * d, d, V - n0, d,
+                   reinterpret_cast<bf16_t*>(smem), acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  float* red_m = reinterpret_cast<float*>(smem);  // [2][BM]
-  float* red_s = red_m + 2 * BM;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  float* red_m = reinterpret_cast<float*>(smem);  // [WGN][BM]
+  float* red_s = red_m + C::WGN * C::BM;
 #pragma unroll
-  for (int i = 0; i < T::TM; ++i) {
+  for (int i = 0; i < C::TM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      const int rl = wm * C::WTM + i * 32 + mfma_row(r, lane);
       const int row = m0 + rl;
       float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < T::TN; ++j) {
-        const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+      for (int j = 0; j < C::TN; ++j) {
+        const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
         if (col < V) mx = fmaxf(mx, acc[i][j][r]);
       }
       mx = group_max<32>(mx);
       float s = 0.0f;
       if (mx != -INFINITY) {
 #pragma unroll
-        for (int j = 0; j < T::TN; ++j) {
-          const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+        for (int j = 0; j < C::TN; ++j) {
+          const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
           if (col < V) s += expf(acc[i][j][r] - mx);
         }
       }
       s = group_sum<32>(s);
       if ((lane & 31) == 0) {
-        red_m[wn * BM + rl] = mx;
-        red_s[wn * BM + rl] = s;
+        red_m[wn * C::BM + rl] = mx;
+        red_s[wn * C::BM + rl] = s;
       }
       if (row < N) {
         const int y = labels[row];
 #pragma unroll
-        for (int j = 0; j < T::TN; ++j) {
-          const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+        for (int j = 0; j < C::TN; ++j) {
+          const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
           if (col == y) label_logit[row] = acc[i][j][r];
         }
       }
     }
   }
   __syncthreads();
-  for (int rl = threadIdx.x; rl < BM; rl += blockDim.x) {
+  for (int rl = threadIdx.x; rl < C::BM; rl += C::NT) {
     const int row = m0 + rl;
     if (row >= N) continue;
     float m = red_m[rl], s = red_s[rl];
-    lse_merge(m, s, red_m[BM + rl], red_s[BM + rl]);
+#pragma unroll
+    for (int w = 1; w < C::WGN; ++w) lse_merge(m, s, red_m[w * C::BM + rl], red_s[w * C::BM + rl]);
     partials[(int64_t)row * n_vb + tn] = make_float2(m, s);
   }
 }
 
 // bf16 backward part 1: dZ for rows [r0, r0+R) x vocab [c0, c0 + tiles_n*BN) into staging.
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void ce_dz_bf16_kernel(
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
     const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
     const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
     int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
-  using T = MfmaTile<BM, BN>;
   extern __shared__ __align__(16) uint8_t smem[];
-  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
-  const int tm = tile % tiles_m, tn = tile / tiles_m;
-  const int m0 = tm * BM, n0 = tn * BN;
-  f32x16 acc[T::TM][T::TN];
-  mfma_mainloop<BM, BN>(h + (int64_t)(r0 + m0) * d, d, R - m0, W + (int64_t)(c0 + n0) * d, d,
-                        cend - (c0 + n0), d, reinterpret_cast<bf16_t*>(smem), acc);
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * C::BM, n0 = tn * C::BN;
+  f32x16 acc[C::TM][C::TN];
+  mfma_mainloop<C>(h + (int64_t)(r0 + m0) * d, d, R - m0, W + (int64_t)(c0 + n0) * d, d,
+                   cend - (c0 + n0), d, reinterpret_cast<bf16_t*>(smem), acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
 #pragma unroll
-  for (int i = 0; i < T::TM; ++i) {
+  for (int i = 0; i < C::TM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = m0 + wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      const int rl = m0 + wm * C::WTM + i * 32 + mfma_row(r, lane);
       if (rl >= R) continue;
       const int row = r0 + rl;
       const float l = lse[row], c = coef[row];
       const int y = labels[row];
 #pragma unroll
-      for (int j = 0; j < T::TN; ++j) {
-        const int cl = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+      for (int j = 0; j < C::TN; ++j) {
+        const int cl = n0 + wn * C::WTN + j * 32 + (lane & 31);
         const int col = c0 + cl;
         float g = 0.0f;
         if (col < V) g = c * (expf(acc[i][j][r] - l) - (col == y ? 1.0f : 0.0f));
@@ -240,33 +272,32 @@ __global__ __launch_bounds__(256) void ce_dz_bf16_kernel(
 }
 
 // bf16 backward part 2: dH[r0 + m, n] (+)= sum_k dZ[m, k] WT[n, c0 + k].
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void ce_dh_bf16_kernel(const bf16_t* __restrict__ dz, int ldz,
-                                                         const bf16_t* __restrict__ WT, int Vp,
-                                                         int r0, int R, int d, int c0, int K,
-                                                         int tiles_m, int tiles_n,
-                                                         float* __restrict__ accbuf,
-                                                         bf16_t* __restrict__ grad, int first,
-                                                         int last) {
-  using T = MfmaTile<BM, BN>;
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restrict__ dz, int ldz,
+                                                           const bf16_t* __restrict__ WT, int Vp,
+                                                           int r0, int R, int d, int c0, int K,
+                                                           int tiles_m, int tiles_n,
+                                                           float* __restrict__ accbuf,
+                                                           bf16_t* __restrict__ grad, int first,
+                                                           int last) {
   extern __shared__ __align__(16) uint8_t smem[];
-  const int tile = xcd_remap(blockIdx.x, tiles_m * tiles_n);
-  const int tm = tile % tiles_m, tn = tile / tiles_m;
-  const int m0 = tm * BM, n0 = tn * BN;
-  f32x16 acc[T::TM][T::TN];
-  mfma_mainloop<BM, BN>(dz + (int64_t)m0 * ldz, ldz, R - m0, WT + (int64_t)n0 * Vp + c0, Vp,
-                        d - n0, K, reinterpret_cast<bf16_t*>(smem), acc);
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * C::BM, n0 = tn * C::BN;
+  f32x16 acc[C::TM][C::TN];
+  mfma_mainloop<C>(dz + (int64_t)m0 * ldz, ldz, R - m0, WT + (int64_t)n0 * Vp + c0, Vp, d - n0, K,
+                   reinterpret_cast<bf16_t*>(smem), acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
 #pragma unroll
-  for (int i = 0; i < T::TM; ++i) {
+  for (int i = 0; i < C::TM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rl = m0 + wm * (BM / 2) + i * 32 + mfma_row(r, lane);
+      const int rl = m0 + wm * C::WTM + i * 32 + mfma_row(r, lane);
       if (rl >= R) continue;
 #pragma unroll
-      for (int j = 0; j < T::TN; ++j) {
-        const int col = n0 + wn * (BN / 2) + j * 32 + (lane & 31);
+      for (int j = 0; j < C::TN; ++j) {
+        const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
         if (col >= d) continue;
         float v = acc[i][j][r];
         const int64_t o = (int64_t)rl * d + col;
@@ -490,19 +521,18 @@ static hipError_t allow_big_lds(Kern k) {
                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
 }
 
-template <int BM, int BN>
+template <class C>
 static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, int N, int d,
                            int V, float2* partials, int n_vb, float* label_logit, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_big_lds(ce_fwd_bf16_kernel<BM, BN>);
+    hipError_t e = allow_big_lds(ce_fwd_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tm = (N + BM - 1) / BM, tn = (V + BN - 1) / BN;
+  const int tm = (N + C::BM - 1) / C::BM, tn = (V + C::BN - 1) / C::BN;
   KernelTimer t(K_CE_FWD, s);
-  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
-  hipLaunchKernelGGL((ce_fwd_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, h, W, labels, N,
+  hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, N,
                      d, V, tm, tn, partials, n_vb, label_logit);
   return hipGetLastError();
 }
@@ -514,8 +544,8 @@ hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
   if (dtype == 1) {
     const bf16_t* hb = static_cast<const bf16_t*>(h);
     const bf16_t* Wb = static_cast<const bf16_t*>(W);
-    if (t.bm == 256) return fwd_bf16<256, 256>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
-    return fwd_bf16<128, 128>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
+    if (t.bm == 256) return fwd_bf16<CfgBig>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
+    return fwd_bf16<CfgSmall>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
   }
   const int tm = (N + kVT - 1) / kVT, tn = (V + kVT - 1) / kVT;
   KernelTimer tt(K_CE_FWD, s);
@@ -549,21 +579,20 @@ hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* W
   return hipGetLastError();
 }
 
-template <int BM, int BN>
+template <class C>
 static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, const float* lse,
                           const float* coef, int r0, int R, int d, int c0, int Vc, int V, bf16_t* dz,
                           int ldz, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_big_lds(ce_dz_bf16_kernel<BM, BN>);
+    hipError_t e = allow_big_lds(ce_dz_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tm = (R + BM - 1) / BM, tn = (Vc + BN - 1) / BN;
+  const int tm = (R + C::BM - 1) / C::BM, tn = (Vc + C::BN - 1) / C::BN;
   const int cend = min(c0 + Vc, V);
   KernelTimer t(K_CE_BWD_DZ, s);
-  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
-  hipLaunchKernelGGL((ce_dz_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, h, W, labels, lse,
+  hipLaunchKernelGGL(ce_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
                      coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz);
   return hipGetLastError();
 }
@@ -576,8 +605,8 @@ hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void*
     const bf16_t* hb = static_cast<const bf16_t*>(h);
     const bf16_t* Wb = static_cast<const bf16_t*>(W);
     bf16_t* z = static_cast<bf16_t*>(dz);
-    if (t.bm == 256) return dz_bf16<256, 256>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
-    return dz_bf16<128, 128>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
+    if (t.bm == 256) return dz_bf16<CfgBig>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
+    return dz_bf16<CfgSmall>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
   }
   const int tm = (R + kVT - 1) / kVT, tn = (Vc + kVT - 1) / kVT;
   const int cend = min(c0 + Vc, V);
@@ -588,20 +617,19 @@ hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void*
   return hipGetLastError();
 }
 
-template <int BM, int BN>
+template <class C>
 static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, int r0, int R, int d,
                           int c0, int K, float* acc, bf16_t* grad, bool first, bool last,
                           hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    hipError_t e = allow_big_lds(ce_dh_bf16_kernel<BM, BN>);
+    hipError_t e = allow_big_lds(ce_dh_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tm = (R + BM - 1) / BM, tn = (d + BN - 1) / BN;
+  const int tm = (R + C::BM - 1) / C::BM, tn = (d + C::BN - 1) / C::BN;
   KernelTimer t(K_CE_BWD_DH, s);
-  constexpr size_t lds = MfmaTile<BM, BN>::LDS;
-  hipLaunchKernelGGL((ce_dh_bf16_kernel<BM, BN>), dim3(tm * tn), dim3(256), lds, s, dz, ldz, WT, Vp, r0,
+  hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
                      R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0);
   return hipGetLastError();
 }
@@ -614,8 +642,8 @@ hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, c
     const bf16_t* z = static_cast<const bf16_t*>(dz);
     const bf16_t* wt = static_cast<const bf16_t*>(WT);
     bf16_t* g = static_cast<bf16_t*>(grad);
-    if (t.bm == 256) return dh_bf16<256, 256>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
-    return dh_bf16<128, 128>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
+    if (t.bm == 256) return dh_bf16<CfgBig>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
+    return dh_bf16<CfgSmall>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
   }
   const int tm = (R + kVT - 1) / kVT, tn = (d + kVT - 1) / kVT;
   KernelTimer tt(K_CE_BWD_DH, s);
