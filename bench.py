@@ -260,7 +260,8 @@ def main():
                 "traffic": counter_traffic(args.config, dom),
                 "flops_per_launch": per_launch}
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
-                ("ce_fwd_lse", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh"))
+                ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_bwd_dz",
+                 "ce_bwd_dh"))
     ng_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("ngram_build", "ngram_count", "ngram_weight"))
     lo_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("lora_u_du", "lora_dadb", "lora_reduce"))
     parts = {

@@ -46,8 +46,8 @@ static attt_status hip_fail(hipError_t e, const char* where) {
 namespace attt {
 
 static const char* kKernelNames[K_NUM_KERNELS] = {
-    "ngram_build", "ngram_count", "ngram_weight", "ce_fwd_lse",  "ce_row_reduce", "ce_loss",
-    "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "lora_u_du",  "lora_dadb",     "lora_reduce"};
+    "ngram_build", "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
+    "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "lora_u_du", "lora_dadb", "lora_reduce"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 

@@ -11,12 +11,15 @@
 // the GEMM operand dtype into a bounded staging buffer; a second GEMM accumulates
 // dH += dZ_chunk W_chunk in float32 and the last chunk writes dH in the output dtype.
 //
-// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 4 waves per workgroup in a 2x2 grid, each wave
-// a (BM/2)x(BN/2) sub-tile, K step 64 double-buffered in LDS with an XOR swizzle of the
-// 16-byte chunks (chunk ^ row%8) so that the 32 rows one MFMA operand read touches fall in
-// distinct banks. Tiles are ordered XCD-aware: workgroup i runs on XCD i%8, and each XCD
-// gets a contiguous range of tiles in vocab-major order, so the workgroups of one XCD
-// share the same LM-head panel in their L2.
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16. A 256x256 tile runs on 8 waves (2x4, 128x64
+// each, two waves per SIMD); small problems use 128x128 on 4 waves. K advances 64 per stage,
+// double-buffered in LDS, with an XOR swizzle of the 16-byte chunks (chunk ^ (row/2)%8): the
+// LDS serves 16 lanes of a 16-byte read per clock over 64 banks, and the 16 consecutive rows
+// those lanes read fall in distinct banks. Global reads are buffer loads whose masked lanes
+// point past the descriptor's range (the hardware returns zero, no branches). Tile order is
+// XCD-aware: workgroup i runs on XCD i%8, each XCD takes a contiguous range of the order, and
+// the order walks groups of 8 row tiles column by column, so the workgroups resident on one
+// XCD share a few hidden and LM-head panels in its L2.
 // f32 path: plain VALU tiles (64x64, 4x4 per thread); it serves the float32 configuration.
 #include "common.hpp"
 #include "internal.hpp"
@@ -118,12 +121,12 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
 #pragma unroll
     for (int i = 0; i < C::AL; ++i) {
       const int row = lrow + C::RPL * i;
-      *reinterpret_cast<u32x4*>(As + row * 64 + ((lch ^ (row & 7)) << 3)) = ra[i];
+      *reinterpret_cast<u32x4*>(As + row * 64 + ((lch ^ ((row >> 1) & 7)) << 3)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < C::BL; ++i) {
       const int row = lrow + C::RPL * i;
-      *reinterpret_cast<u32x4*>(Bs + row * 64 + ((lch ^ (row & 7)) << 3)) = rb[i];
+      *reinterpret_cast<u32x4*>(Bs + row * 64 + ((lch ^ ((row >> 1) & 7)) << 3)) = rb[i];
     }
   };
 
@@ -132,30 +135,35 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
   lstore(0);
   __syncthreads();
   const int l32 = lane & 31, hi = lane >> 5;
+  const int swz = (l32 >> 1) & 7;
+  const int arow = (wm * C::WTM + l32) * 64, brow = (wn * C::WTN + l32) * 64;
+  // operand fragments of sub-step kk live in fa/fb[kk & 1]; the reads for kk+1 are issued
+  // before the MFMAs of kk so their LDS latency hides behind those MFMAs
+  bf16x8 fa[2][C::TM], fb[2][C::TN];
+  auto fragload = [&](const bf16_t* As, const bf16_t* Bs, int kk, int slot) {
+    const int sw = ((kk * 2 + hi) ^ swz) << 3;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+      fa[slot][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 32 * 64 + sw));
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+      fb[slot][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
+  };
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) gload((kt + 1) * 64);
     const bf16_t* As = lds + (kt & 1) * (C::SA + C::SB);
     const bf16_t* Bs = As + C::SA;
+    fragload(As, Bs, 0, 0);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const int ch = kk * 2 + hi;
-      const int sw = (ch ^ (l32 & 7)) << 3;
-      bf16x8 a[C::TM], b[C::TN];
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i) {
-        const int r = wm * C::WTM + i * 32 + l32;
-        a[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + r * 64 + sw));
-      }
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int r = wn * C::WTN + j * 32 + l32;
-        b[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + r * 64 + sw));
-      }
+      if (kk + 1 < 4) fragload(As, Bs, kk + 1, (kk + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < C::TM; ++i)
 #pragma unroll
         for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (kt + 1 < nk) lstore((kt + 1) & 1);
     __syncthreads();
@@ -167,72 +175,93 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
 __device__ __forceinline__ int mfma_row(int r, int lane) { return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3); }
 
 // ------------------------------------------------------------------------------------------
-// bf16 forward: partial (max, sumexp) per (row, BN-wide vocab tile) and the label logit.
+// bf16 forward. The GEMM runs transposed, z^T = W h^T, so a workgroup tile is 256 vocab rows x
+// 256 token columns and every lane holds, for one token, 64 of the tile's vocab logits in its
+// registers: the per-token (max, sum exp) needs one cross-lane step (lanes l and l+32) and a
+// two-wave merge in LDS, instead of a 32-lane shuffle tree per row.
 // ------------------------------------------------------------------------------------------
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(const bf16_t* __restrict__ h,
                                                             const bf16_t* __restrict__ W,
-                                                            const int32_t* __restrict__ labels,
-                                                            int N, int d, int V, int tiles_m,
-                                                            int tiles_n, float2* __restrict__ partials,
-                                                            int n_vb, float* __restrict__ label_logit) {
+                                                            int N, int d, int V, int tiles_v,
+                                                            int tiles_t, float2* __restrict__ partials,
+                                                            int n_vb) {
   extern __shared__ __align__(16) uint8_t smem[];
-  int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * C::BM, n0 = tn * C::BN;
+  int tv, tt;
+  tile_of(blockIdx.x, tiles_v, tiles_t, tv, tt);
+  const int v0 = tv * C::BM, t0 = tt * C::BN;
   f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(h + (int64_t)m0 * d, d, N - m0, W + (int64_t)n0 * d, d, V - n0, d,
+  mfma_mainloop<C>(W + (int64_t)v0 * d, d, V - v0, h + (int64_t)t0 * d, d, N - t0, d,
                    reinterpret_cast<bf16_t*>(smem), acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  float* red_m = reinterpret_cast<float*>(smem);  // [WGN][BM]
-  float* red_s = red_m + C::WGN * C::BM;
+  float* red_m = reinterpret_cast<float*>(smem);  // [WGM][BN]
+  float* red_s = red_m + C::WGM * C::BN;
+  const int vbase = v0 + wm * C::WTM;
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
+  for (int j = 0; j < C::TN; ++j) {
+    float mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = wm * C::WTM + i * 32 + mfma_row(r, lane);
-      const int row = m0 + rl;
-      float mx = -INFINITY;
+    for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
-        if (col < V) mx = fmaxf(mx, acc[i][j][r]);
-      }
-      mx = group_max<32>(mx);
-      float s = 0.0f;
-      if (mx != -INFINITY) {
+      for (int r = 0; r < 16; ++r)
+        if (vbase + i * 32 + mfma_row(r, lane) < V) mx = fmaxf(mx, acc[i][j][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float s = 0.0f;
+    if (mx != -INFINITY) {
 #pragma unroll
-        for (int j = 0; j < C::TN; ++j) {
-          const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
-          if (col < V) s += expf(acc[i][j][r] - mx);
-        }
-      }
-      s = group_sum<32>(s);
-      if ((lane & 31) == 0) {
-        red_m[wn * C::BM + rl] = mx;
-        red_s[wn * C::BM + rl] = s;
-      }
-      if (row < N) {
-        const int y = labels[row];
+      for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-        for (int j = 0; j < C::TN; ++j) {
-          const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
-          if (col == y) label_logit[row] = acc[i][j][r];
-        }
-      }
+        for (int r = 0; r < 16; ++r)
+          if (vbase + i * 32 + mfma_row(r, lane) < V) s += __expf(acc[i][j][r] - mx);
+    }
+    s += __shfl_xor(s, 32, 64);
+    if (lane < 32) {
+      const int tl = wn * C::WTN + j * 32 + lane;
+      red_m[wm * C::BN + tl] = mx;
+      red_s[wm * C::BN + tl] = s;
     }
   }
   __syncthreads();
-  for (int rl = threadIdx.x; rl < C::BM; rl += C::NT) {
-    const int row = m0 + rl;
-    if (row >= N) continue;
-    float m = red_m[rl], s = red_s[rl];
+  for (int tl = threadIdx.x; tl < C::BN; tl += C::NT) {
+    const int t = t0 + tl;
+    if (t >= N) continue;
+    float m = red_m[tl], s = red_s[tl];
 #pragma unroll
-    for (int w = 1; w < C::WGN; ++w) lse_merge(m, s, red_m[w * C::BM + rl], red_s[w * C::BM + rl]);
-    partials[(int64_t)row * n_vb + tn] = make_float2(m, s);
+    for (int w = 1; w < C::WGM; ++w) lse_merge(m, s, red_m[w * C::BN + tl], red_s[w * C::BN + tl]);
+    partials[(int64_t)t * n_vb + tv] = make_float2(m, s);
   }
+}
+
+// Label logit z_{t, y_t} = h_t . W_{y_t} (float32 accumulation), one wave per row.
+__global__ __launch_bounds__(256) void ce_label_logit_bf16_kernel(const bf16_t* __restrict__ h,
+                                                                  const bf16_t* __restrict__ W,
+                                                                  const int32_t* __restrict__ labels,
+                                                                  int N, int d, int V,
+                                                                  float* __restrict__ label_logit) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= N) return;
+  const int y = labels[row];
+  if (y < 0 || y >= V) {  // outside the contract: make the loss NaN instead of reading out of bounds
+    if (lane == 0) label_logit[row] = __int_as_float(0x7FC00000);
+    return;
+  }
+  const bf16_t* hr = h + (int64_t)row * d;
+  const bf16_t* wr = W + (int64_t)y * d;
+  float s = 0.0f;
+  for (int k = lane * 8; k < d; k += 64 * 8) {
+    const u32x4 a = *reinterpret_cast<const u32x4*>(hr + k);
+    const u32x4 b = *reinterpret_cast<const u32x4*>(wr + k);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      s = fmaf(bf16_bits_to_f32(a[e] & 0xFFFFu), bf16_bits_to_f32(b[e] & 0xFFFFu), s);
+      s = fmaf(bf16_bits_to_f32(a[e] >> 16), bf16_bits_to_f32(b[e] >> 16), s);
+    }
+  }
+  s = group_sum<64>(s);
+  if (lane == 0) label_logit[row] = s;
 }
 
 // bf16 backward part 1: dZ for rows [r0, r0+R) x vocab [c0, c0 + tiles_n*BN) into staging.
@@ -264,7 +293,7 @@ __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
         const int cl = n0 + wn * C::WTN + j * 32 + (lane & 31);
         const int col = c0 + cl;
         float g = 0.0f;
-        if (col < V) g = c * (expf(acc[i][j][r] - l) - (col == y ? 1.0f : 0.0f));
+        if (col < V) g = c * (__expf(acc[i][j][r] - l) - (col == y ? 1.0f : 0.0f));
         dz[(int64_t)rl * ldz + cl] = (bf16_t)f32_to_bf16_bits(g);
       }
     }
@@ -530,10 +559,17 @@ static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labe
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tm = (N + C::BM - 1) / C::BM, tn = (V + C::BN - 1) / C::BN;
-  KernelTimer t(K_CE_FWD, s);
-  hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, N,
-                     d, V, tm, tn, partials, n_vb, label_logit);
+  const int tv = (V + C::BM - 1) / C::BM, tt = (N + C::BN - 1) / C::BN;
+  {
+    KernelTimer t(K_CE_FWD, s);
+    hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V, tv,
+                       tt, partials, n_vb);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  KernelTimer t(K_CE_LABEL, s);
+  hipLaunchKernelGGL(ce_label_logit_bf16_kernel, dim3((N + 3) / 4), dim3(256), 0, s, h, W, labels, N, d,
+                     V, label_logit);
   return hipGetLastError();
 }
 

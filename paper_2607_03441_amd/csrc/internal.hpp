@@ -13,6 +13,7 @@ enum KernelId {
   K_NGRAM_COUNT,
   K_NGRAM_WEIGHT,
   K_CE_FWD,
+  K_CE_LABEL,
   K_CE_ROW_REDUCE,
   K_CE_LOSS,
   K_CE_HEAD_T,
