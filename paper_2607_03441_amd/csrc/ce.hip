@@ -84,9 +84,9 @@ template <class C>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                               const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                               int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const int lrow = tid >> 3, lch = tid & 7;
 #pragma unroll
   for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -94,45 +94,47 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // Global -> LDS without registers: buffer_load_dwordx4 ... lds writes lane i's 16 bytes at
+  // LDS base + 16 i, so one instruction fills a 1 KiB block of 8 rows x 128 bytes. Lane i of a
+  // block takes row 8*block + i/8 and physical chunk i%8, and fetches the logical chunk that
+  // the swizzle stores there (physical ^ (row/2)%8). The stage's blocks are dealt round-robin
+  // to the waves.
   const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
-  uint32_t aoff[C::AL], boff[C::BL];
+  constexpr int NW = C::NT / 64;
+  constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
+  constexpr int BPW = (ABLK + BBLK) / NW;  // blocks per wave per stage
+  static_assert((ABLK + BBLK) % NW == 0 && ABLK % NW == 0, "stage blocks must split evenly");
+  uint32_t goff[BPW];
+  int gch[BPW];
 #pragma unroll
-  for (int i = 0; i < C::AL; ++i) {
-    const int row = lrow + C::RPL * i;
-    aoff[i] = row < mval ? (uint32_t)((int64_t)row * lda * 2) + lch * 16 : kOOB;
+  for (int j = 0; j < BPW; ++j) {
+    const int blk = wave + j * NW;
+    const bool isA = blk < ABLK;
+    const int row = (isA ? blk : blk - ABLK) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    gch[j] = c;
+    const int val = isA ? mval : nval;
+    const int64_t ld = isA ? lda : ldb;
+    goff[j] = row < val ? (uint32_t)((int64_t)row * ld * 2) + c * 16 : kOOB;
   }
-#pragma unroll
-  for (int i = 0; i < C::BL; ++i) {
-    const int row = lrow + C::RPL * i;
-    boff[i] = row < nval ? (uint32_t)((int64_t)row * ldb * 2) + lch * 16 : kOOB;
-  }
-  u32x4 ra[C::AL], rb[C::BL];
-  auto gload = [&](int k0) {
-    const bool kin = k0 + lch * 8 < K;
+  auto dma = [&](int st, int k0) {
+    bf16_t* base = lds + st * (C::SA + C::SB);
     const uint32_t kb = (uint32_t)k0 * 2;
 #pragma unroll
-    for (int i = 0; i < C::AL; ++i) ra[i] = bload16(rA, (kin && aoff[i] != kOOB) ? aoff[i] + kb : kOOB);
-#pragma unroll
-    for (int i = 0; i < C::BL; ++i) rb[i] = bload16(rB, (kin && boff[i] != kOOB) ? boff[i] + kb : kOOB);
-  };
-  auto lstore = [&](int st) {
-    bf16_t* As = lds + st * (C::SA + C::SB);
-    bf16_t* Bs = As + C::SA;
-#pragma unroll
-    for (int i = 0; i < C::AL; ++i) {
-      const int row = lrow + C::RPL * i;
-      *reinterpret_cast<u32x4*>(As + row * 64 + ((lch ^ ((row >> 1) & 7)) << 3)) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::BL; ++i) {
-      const int row = lrow + C::RPL * i;
-      *reinterpret_cast<u32x4*>(Bs + row * 64 + ((lch ^ ((row >> 1) & 7)) << 3)) = rb[i];
+    for (int j = 0; j < BPW; ++j) {
+      const int blk = wave + j * NW;
+      const bool isA = blk < ABLK;
+      const bool kin = k0 + gch[j] * 8 < K;
+      const uint32_t off = (kin && goff[j] != kOOB) ? goff[j] + kb : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rA : rB,
+                                               (__attribute__((address_space(3))) void*)(base + blk * 512),
+                                               16, off, 0, 0, 0);
     }
   };
 
   const int nk = (K + 63) / 64;
-  gload(0);
-  lstore(0);
+  dma(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   const int l32 = lane & 31, hi = lane >> 5;
   const int swz = (l32 >> 1) & 7;
@@ -150,7 +152,7 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
       fb[slot][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
   };
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * 64);
+    if (kt + 1 < nk) dma((kt + 1) & 1, (kt + 1) * 64);
     const bf16_t* As = lds + (kt & 1) * (C::SA + C::SB);
     const bf16_t* Bs = As + C::SA;
     fragload(As, Bs, 0, 0);
@@ -165,7 +167,7 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) lstore((kt + 1) & 1);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next stage have landed in LDS
     __syncthreads();
   }
 }

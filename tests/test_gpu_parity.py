@@ -134,7 +134,7 @@ def test_ce_small_bf16(attt):
 
 
 @pytest.mark.parametrize("bf16", [False, True])
-@pytest.mark.parametrize("shape", [(300, 200, 1000), (77, 64, 9000), (513, 96, 8200)])
+@pytest.mark.parametrize("shape", [(300, 200, 1000), (77, 64, 9000), (513, 96, 8200), (2100, 512, 33000)])
 def test_ce_ragged(attt, bf16, shape):
     N, d, V = shape
     note(f"ce ragged {shape} bf16={bf16}")
