@@ -81,7 +81,7 @@ __device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off)
 // acc += A[0:BM, 0:K] * B[0:BN, 0:K]^T, A and B K-contiguous bf16. Rows at or past mval
 // (nval) and K-chunks at or past K read as zero. K % 8 == 0.
 template <class C>
-__device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
+__device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                               const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                               int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
   const int lane = threadIdx.x & 63;
@@ -170,6 +170,137 @@ __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int6
     __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next stage have landed in LDS
     __syncthreads();
   }
+}
+
+// 8-wave ping-pong schedule. Waves 0-3 and 4-7 form two groups with one wave of each on every
+// SIMD. Phases are separated by workgroup barriers and group 1 runs one phase behind group 0, so
+// in every phase one wave per SIMD reads a whole K-step of operand fragments from LDS (memory
+// phase) while the other runs its 32 MFMAs (compute phase).
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <class C>
+__device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                                 const bf16_t* __restrict__ B, int64_t ldb, int nval,
+                                                 int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
+  static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4, "ping-pong needs 8 waves in 2 groups of 4");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int grp = wave >> 2;
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // Only group 0 (waves 0-3) loads tiles: each of its waves fills 16 of the stage's 64 blocks,
+  // in its memory phase, so no load instruction ever sits in front of an MFMA of the wave that
+  // is computing on the same SIMD.
+  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
+  constexpr int LW = 4;                               // loading waves
+  constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
+  constexpr int BPW = (ABLK + BBLK) / LW;             // blocks per loading wave per stage
+  static_assert(ABLK % LW == 0 && BBLK % LW == 0, "stage blocks must split evenly");
+  // Offsets are formed per load: the block's first row is wave-uniform, and the swizzled chunk
+  // of a lane depends only on the lane and on the parity of the block (rows 8b .. 8b+7).
+  const int lr = lane >> 3;
+  const int c_even = (lane & 7) ^ ((lr >> 1) & 7);
+  const int c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
+  const uint32_t la = (uint32_t)(lr * lda * 2), lb = (uint32_t)(lr * ldb * 2);
+  auto dma = [&](int st, int k0) {
+    bf16_t* base = lds + st * (C::SA + C::SB);
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int blk = (wave & 3) + j * LW;
+      const bool isA = blk < ABLK;
+      const int rb = (isA ? blk : blk - ABLK) * 8;
+      const int c = (rb & 8) ? c_odd : c_even;
+      const bool ok = rb + lr < (isA ? mval : nval) && k0 + c * 8 < K;
+      const uint32_t off = (uint32_t)((int64_t)rb * (isA ? lda : ldb) * 2) + (isA ? la : lb) +
+                           (uint32_t)(k0 + c * 8) * 2;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rA : rB,
+                                               (__attribute__((address_space(3))) void*)(base + blk * 512),
+                                               16, ok ? off : kOOB, 0, 0, 0);
+    }
+  };
+
+  const int l32 = lane & 31, hi = lane >> 5;
+  const int swz = (l32 >> 1) & 7;
+  const int arow = (wm * C::WTM + l32) * 64, brow = (wn * C::WTN + l32) * 64;
+  bf16x8 fa[4][C::TM], fb[4][C::TN];
+  auto mem = [&](int k) {
+    const bf16_t* As = lds + (k & 1) * (C::SA + C::SB);
+    const bf16_t* Bs = As + C::SA;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int sw = ((kk * 2 + hi) ^ swz) << 3;
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+        fa[kk][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 32 * 64 + sw));
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+        fb[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
+    }
+  };
+  auto compute = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][i], fb[kk][j], acc[i][j], 0, 0, 0);
+  };
+  // MFMAs are pure register operations and could be moved across the barriers; tying the
+  // accumulators to empty asm statements keeps each compute phase between its two barriers.
+  auto pin = [&]() {
+    static_assert(C::TM == 4 && C::TN == 2, "pin lists the 8 accumulators of a 128x64 wave tile");
+    asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[1][0]), "+v"(acc[1][1]),
+                 "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[3][0]), "+v"(acc[3][1]));
+  };
+  // Group 0, iteration k:  DMA(stage k+1); fragments(k) | MFMA(k); wait for the DMA |
+  // group 1, one phase later: fragments(k) | MFMA(k) |
+  // Stage k+1 goes into the slot of stage k-1, which group 1 finished reading in the phase just
+  // before; group 0 reads it two phases later. Group 1 takes one extra barrier before its loop,
+  // group 0 one after it, so every wave executes 2 nk + 2 barriers.
+  const int nk = (K + 63) / 64;
+  if (grp == 0) dma(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  wg_barrier();
+  if (grp == 0) {
+    for (int k = 0; k < nk; ++k) {
+      if (k + 1 < nk) dma((k + 1) & 1, (k + 1) * 64);
+      mem(k);
+      wg_barrier();
+      pin();
+      compute();
+      pin();
+      __builtin_amdgcn_s_waitcnt(0);
+      wg_barrier();
+    }
+    wg_barrier();
+  } else {
+    wg_barrier();
+    for (int k = 0; k < nk; ++k) {
+      mem(k);
+      wg_barrier();
+      pin();
+      compute();
+      pin();
+      wg_barrier();
+    }
+  }
+}
+
+template <class C>
+__device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                              const bf16_t* __restrict__ B, int64_t ldb, int nval,
+                                              int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
+  if constexpr (C::NT == 512)
+    mfma_mainloop_pp<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
+  else
+    mfma_mainloop_db<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
 }
 
 // Output layout of a 32x32 MFMA accumulator: register r of lane l holds
