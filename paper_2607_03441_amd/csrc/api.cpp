@@ -304,7 +304,7 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
 namespace {
 
 constexpr int64_t kCeRowBlock = 8192;     // rows per backward block
-constexpr int64_t kCeVocabChunk = 8192;   // vocab columns per backward chunk
+constexpr int64_t kCeVocabChunk = 32768;  // vocab columns per backward chunk
 
 struct CePlan {
   CeGemmShape fwd{64, 64}, dz{64, 64}, dh{64, 64};

@@ -656,21 +656,40 @@ __global__ __launch_bounds__(256) void ce_loss_kernel(CeEpBatch b, const float* 
   }
 }
 
+// W [V, d] -> WT [d, Vp] in 64 x 64 tiles: 16-byte global reads along d, 16-byte global writes
+// along V, through an LDS tile whose padded pitch (66) keeps the column reads conflict-free.
 __global__ __launch_bounds__(256) void ce_head_transpose_kernel(const bf16_t* __restrict__ W, int V,
                                                                 int d, int Vp,
                                                                 bf16_t* __restrict__ WT) {
-  __shared__ bf16_t t[64][66];
+  constexpr int P = 66;
+  __shared__ __align__(16) bf16_t t[64 * P];
   const int v0 = blockIdx.x * 64, j0 = blockIdx.y * 64;
-  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
-    const int r = idx >> 6, c = idx & 63;
-    const int v = v0 + r, j = j0 + c;
-    t[r][c] = (v < V && j < d) ? W[(int64_t)v * d + j] : (bf16_t)0;
+  const int r = threadIdx.x >> 2, c = threadIdx.x & 3;  // row r, 16 columns from 16c
+  {
+    const int v = v0 + r, j = j0 + 16 * c;
+    u32x4 x0 = u32x4{0u, 0u, 0u, 0u}, x1 = u32x4{0u, 0u, 0u, 0u};
+    if (v < V && j < d) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(W + (int64_t)v * d + j);
+      x0 = src[0];
+      if (j + 8 < d) x1 = src[1];
+    }
+    uint32_t* dst = reinterpret_cast<uint32_t*>(t + r * P + 16 * c);  // 4-byte aligned: P even
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      dst[e] = x0[e];
+      dst[4 + e] = x1[e];
+    }
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 64 * 64; idx += 256) {
-    const int r = idx >> 6, c = idx & 63;
-    const int j = j0 + r, v = v0 + c;
-    if (j < d && v < Vp) WT[(int64_t)j * Vp + v] = t[c][r];
+  const int j = j0 + r, v = v0 + 16 * c;  // output row j, 16 vocab entries from v
+  if (j < d && v < Vp) {
+    uint32_t w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      w[e] = (uint32_t)t[(16 * c + 2 * e) * P + r] | ((uint32_t)t[(16 * c + 2 * e + 1) * P + r] << 16);
+    u32x4* out = reinterpret_cast<u32x4*>(WT + (int64_t)j * Vp + v);
+    out[0] = u32x4{w[0], w[1], w[2], w[3]};
+    out[1] = u32x4{w[4], w[5], w[6], w[7]};
   }
 }
 
