@@ -46,7 +46,7 @@ static attt_status hip_fail(hipError_t e, const char* where) {
 namespace attt {
 
 static const char* kKernelNames[K_NUM_KERNELS] = {
-    "ngram_build", "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
+    "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "lora_u_du", "lora_dadb", "lora_reduce"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
@@ -165,10 +165,15 @@ static attt_status check_offsets(const char* what, const int64_t* off, int32_t E
 // ------------------------------------------------------------------------------------------
 namespace {
 
+struct NgramEpPlan {
+  int64_t tok_base, hist_base, chunk_base;
+  int32_t L, Q, hist_ngrams, parts, chunks;
+};
+
 struct NgramPlan {
-  std::vector<NgramPart> parts;
-  size_t off_tables = 0, off_counts = 0, off_qcell = 0, total = 0;
-  int64_t total_slots = 0;
+  std::vector<NgramEpPlan> eps;
+  int64_t total_chunks = 0;
+  size_t total = 0;
 };
 
 int next_pow2(int v) {
@@ -189,33 +194,31 @@ attt_status ngram_validate(const int64_t* hoff, const int64_t* toff, int32_t E, 
   return ATTT_OK;
 }
 
+// History chunks: about two workgroups per CU over the whole call, at most 65535 positions
+// per chunk (the per-chunk counts are 16-bit) and at least 2048.
 NgramPlan ngram_plan(const int64_t* hoff, const int64_t* toff, int32_t E, int32_t n) {
   NgramPlan P;
-  int64_t table_slots = 0;
+  int64_t work = 0;
   for (int32_t e = 0; e < E; ++e) {
-    const int64_t L = toff[e + 1] - toff[e];
-    const int64_t H = hoff[e + 1] - hoff[e];
+    const int64_t L = toff[e + 1] - toff[e], H = hoff[e + 1] - hoff[e];
     const int64_t Q = std::max<int64_t>(0, L - n + 1);
-    for (int64_t q0 = 0; q0 < Q; q0 += kQMax) {
-      NgramPart p{};
-      p.tok_base = toff[e];
-      p.hist_base = hoff[e];
-      p.hist_ngrams = (int32_t)std::max<int64_t>(0, H - n + 1);
-      p.q0 = (int32_t)q0;
-      p.qn = (int32_t)std::min<int64_t>(kQMax, Q - q0);
-      p.slots = std::max(64, next_pow2(2 * p.qn));
-      p.table_off = table_slots;
-      p.count_off = (uint32_t)table_slots;
-      table_slots += p.slots;
-      P.parts.push_back(p);
-    }
+    work += ceil_div(Q, kQMax) * std::max<int64_t>(0, H - n + 1);
   }
-  P.total_slots = table_slots;
-  P.off_tables = 0;
-  P.off_counts = align256((size_t)table_slots * 8);
-  P.off_qcell = P.off_counts + align256((size_t)table_slots * 4);
-  P.total = P.off_qcell + align256((size_t)toff[E] * 4);
-  if (P.total == 0) P.total = 256;
+  const int64_t chunk_len = std::min<int64_t>(65535, std::max<int64_t>(2048, ceil_div(work, 512)));
+  for (int32_t e = 0; e < E; ++e) {
+    NgramEpPlan ep{};
+    ep.tok_base = toff[e];
+    ep.hist_base = hoff[e];
+    ep.L = (int32_t)(toff[e + 1] - toff[e]);
+    ep.Q = std::max(0, ep.L - n + 1);
+    ep.hist_ngrams = (int32_t)std::max<int64_t>(0, hoff[e + 1] - hoff[e] - n + 1);
+    ep.parts = (int32_t)ceil_div(ep.Q, kQMax);
+    ep.chunks = ep.hist_ngrams > 0 ? (int32_t)ceil_div(ep.hist_ngrams, chunk_len) : 0;
+    ep.chunk_base = P.total_chunks;
+    P.total_chunks += (int64_t)ep.parts * ep.chunks;
+    P.eps.push_back(ep);
+  }
+  P.total = std::max<size_t>(align256((size_t)P.total_chunks * kQMax * 2), 256);
   return P;
 }
 
@@ -246,8 +249,6 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
   if (T > 0 && !weights) return fail(ATTT_EINVAL, "ngram: weights is null");
   if (history_offsets[E] > 0 && !history) return fail(ATTT_EINVAL, "ngram: history is null");
   NgramPlan P = ngram_plan(history_offsets, token_offsets, E, n);
-  if (P.total_slots >= ((int64_t)1 << 32))
-    return fail(ATTT_EUNSUPPORTED, "ngram: too many table slots (%lld)", (long long)P.total_slots);
   if (workspace_bytes < P.total)
     return fail(ATTT_ENOSPACE, "ngram: workspace %zu bytes, need %zu", workspace_bytes, P.total);
   if (!workspace) return fail(ATTT_EINVAL, "ngram: workspace is null");
@@ -255,45 +256,58 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
   if (T == 0) return ATTT_OK;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  uint8_t* ws = static_cast<uint8_t*>(workspace);
-  uint2* tables = reinterpret_cast<uint2*>(ws + P.off_tables);
-  uint32_t* counts = reinterpret_cast<uint32_t*>(ws + P.off_counts);
-  uint32_t* qcell = reinterpret_cast<uint32_t*>(ws + P.off_qcell);
+  uint16_t* partial = static_cast<uint16_t*>(workspace);
 
-  // Count blocks: spread the history work over about two workgroups per CU.
-  int64_t work = 0;
-  for (auto& p : P.parts) work += p.hist_ngrams;
-  const int64_t chunk_len = std::max<int64_t>(16384, ceil_div(work, 512));
-
-  for (size_t b0 = 0; b0 < P.parts.size(); b0 += kPartBatch) {
-    NgramPartBatch batch{};
-    batch.count = (int32_t)std::min<size_t>(kPartBatch, P.parts.size() - b0);
-    int max_slots = 64, blocks = 0;
-    for (int i = 0; i < batch.count; ++i) {
-      NgramPart p = P.parts[b0 + i];
-      p.chunks = p.hist_ngrams > 0 ? (int32_t)ceil_div(p.hist_ngrams, chunk_len) : 0;
-      p.chunk_begin = blocks;
-      blocks += p.chunks;
-      max_slots = std::max(max_slots, p.slots);
-      batch.p[i] = p;
+  // count kernel: batches of partitions; a partition's chunks are consecutive blocks
+  NgramPartBatch batch{};
+  int blocks = 0, max_slots = 64;
+  auto flush = [&]() -> attt_status {
+    if (batch.count == 0) return ATTT_OK;
+    HIP_TRY(launch_ngram_count(batch, blocks, max_slots, history, tokens, n, partial, s), "ngram_count");
+    batch = NgramPartBatch{};
+    blocks = 0;
+    max_slots = 64;
+    return ATTT_OK;
+  };
+  for (const auto& ep : P.eps) {
+    if (ep.chunks == 0) continue;
+    for (int32_t p = 0; p < ep.parts; ++p) {
+      if (batch.count == kPartBatch) {
+        attt_status st2 = flush();
+        if (st2) return st2;
+      }
+      NgramPart& q = batch.p[batch.count++];
+      q.tok_base = ep.tok_base;
+      q.hist_base = ep.hist_base;
+      q.hist_ngrams = ep.hist_ngrams;
+      q.q0 = p * kQMax;
+      q.qn = std::min(kQMax, ep.Q - p * kQMax);
+      q.slots = std::max(64, next_pow2(2 * q.qn));
+      q.chunks = ep.chunks;
+      q.chunk_begin = blocks;
+      q.chunk_begin_global = ep.chunk_base + (int64_t)p * ep.chunks;
+      blocks += ep.chunks;
+      max_slots = std::max(max_slots, q.slots);
     }
-    HIP_TRY(launch_ngram_build(batch, max_slots, tokens, n, tables, counts, qcell, s), "ngram_build");
-    HIP_TRY(launch_ngram_count(batch, blocks, max_slots, history, tokens, n, tables, counts, s),
-            "ngram_count");
+  }
+  {
+    attt_status st2 = flush();
+    if (st2) return st2;
   }
   for (int32_t e0 = 0; e0 < E; e0 += kEpBatch) {
-    NgramEpBatch batch{};
-    batch.count = std::min<int32_t>(kEpBatch, E - e0);
-    int blocks = 0;
-    for (int i = 0; i < batch.count; ++i) {
-      const int32_t e = e0 + i;
-      batch.e[i].tok_base = token_offsets[e];
-      batch.e[i].L = (int32_t)(token_offsets[e + 1] - token_offsets[e]);
-      batch.e[i].block_begin = blocks;
-      blocks += (int)ceil_div(batch.e[i].L, 256);
+    NgramEpBatch wb{};
+    wb.count = std::min<int32_t>(kEpBatch, E - e0);
+    int wblocks = 0;
+    for (int i = 0; i < wb.count; ++i) {
+      const NgramEpPlan& ep = P.eps[e0 + i];
+      wb.e[i].tok_base = ep.tok_base;
+      wb.e[i].chunk_base = ep.chunk_base;
+      wb.e[i].L = ep.L;
+      wb.e[i].chunks = ep.chunks;
+      wb.e[i].block_begin = wblocks;
+      wblocks += (int)ceil_div(ep.L, 256);
     }
-    HIP_TRY(launch_ngram_weight(batch, blocks, n, w_min, counts, qcell, exposure, weights, s),
-            "ngram_weight");
+    HIP_TRY(launch_ngram_weight(wb, wblocks, n, w_min, partial, exposure, weights, s), "ngram_weight");
   }
   return ATTT_OK;
 }

@@ -9,8 +9,7 @@ namespace attt {
 
 // ---- kernel timing ---------------------------------------------------------------------
 enum KernelId {
-  K_NGRAM_BUILD = 0,
-  K_NGRAM_COUNT,
+  K_NGRAM_COUNT = 0,
   K_NGRAM_WEIGHT,
   K_CE_FWD,
   K_CE_LABEL,
@@ -49,23 +48,21 @@ struct KernelTimer {
 };
 
 // ---- n-gram ----------------------------------------------------------------------------
-constexpr int kQMax = 4096;        // query n-gram starts per partition
-constexpr int kMaxSlots = 8192;    // table slots per partition (load factor <= 1/2)
+constexpr int kQMax = 4096;        // query n-gram starts per partition (12-bit positions)
+constexpr int kMaxN = 16;          // largest n
 constexpr int kPartBatch = 32;     // partitions per launch (kernel-argument descriptors)
 constexpr int kEpBatch = 64;       // episodes per launch
 
 struct NgramPart {
-  int64_t tok_base;     // first update token of the episode in `tokens`
-  int64_t hist_base;    // first history token of the episode in `history`
-  int64_t table_off;    // first slot of this partition's table (uint2 units)
-  uint32_t count_off;   // first counter of this partition (uint32 units)
-  int32_t hist_ngrams;  // history n-gram starts of the episode: max(0, H_e - n + 1)
-  int32_t q0;           // first query start of this partition, relative to the episode
-  int32_t qn;           // query starts in this partition, 1 .. kQMax
-  int32_t slots;        // power of two, >= 2 * qn
-  int32_t chunk_begin;  // first count-kernel block of this partition within the launch
-  int32_t chunks;       // count-kernel blocks of this partition (0 when hist_ngrams == 0)
-  int32_t pad;
+  int64_t tok_base;            // first update token of the episode in `tokens`
+  int64_t hist_base;           // first history token of the episode in `history`
+  int64_t chunk_begin_global;  // first row of this partition in the partial-count array
+  int32_t hist_ngrams;         // history n-gram starts of the episode: max(0, H_e - n + 1)
+  int32_t q0;                  // first query start of this partition, relative to the episode
+  int32_t qn;                  // query starts in this partition, 1 .. kQMax
+  int32_t slots;               // LDS table size, power of two >= 2 * qn
+  int32_t chunk_begin;         // first count-kernel block of this partition within the launch
+  int32_t chunks;              // history chunks (count-kernel blocks) of the partition
 };
 
 struct NgramPartBatch {
@@ -76,8 +73,11 @@ struct NgramPartBatch {
 
 struct NgramEp {
   int64_t tok_base;
+  int64_t chunk_base;  // partial-count row of the episode's first partition, first chunk
   int32_t L;
+  int32_t chunks;      // chunks per partition (the same for every partition of the episode)
   int32_t block_begin;
+  int32_t pad;
 };
 
 struct NgramEpBatch {
@@ -86,16 +86,13 @@ struct NgramEpBatch {
   NgramEp e[kEpBatch];
 };
 
-size_t ngram_build_lds(int slots, int n);
 size_t ngram_count_lds(int slots, int n);
-hipError_t launch_ngram_build(const NgramPartBatch& b, int max_slots, const int32_t* tokens, int n,
-                              uint2* tables, uint32_t* counts, uint32_t* qcell, hipStream_t s);
 hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max_slots,
                               const int32_t* history, const int32_t* tokens, int n,
-                              const uint2* tables, uint32_t* counts, hipStream_t s);
+                              uint16_t* partial, hipStream_t s);
 hipError_t launch_ngram_weight(const NgramEpBatch& b, int total_blocks, int n, float w_min,
-                               const uint32_t* counts, const uint32_t* qcell, uint32_t* exposure,
-                               float* weights, hipStream_t s);
+                               const uint16_t* partial, uint32_t* exposure, float* weights,
+                               hipStream_t s);
 
 // ---- weighted cross-entropy ------------------------------------------------------------
 struct CeEp {
