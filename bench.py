@@ -137,7 +137,8 @@ def algorithmic(cfg, tok, probs):
                 ngram_bytes=float(ngram_bytes), lora_bytes=float(lora_bytes), lora_flops=float(lora_flops))
 
 
-KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_"}
+KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_logit_exp": "attt::ce_logit_exp_",
+                 "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_"}
 
 
 def counter_traffic(config, kernel):
@@ -248,9 +249,9 @@ def main():
     alg = algorithmic(cfg, wl.tokens(), wl.lora())
     bf16 = cfg.dtype == "bf16"
     peak = PEAK_BF16 if bf16 else PEAK_F32_MFMA
-    ce_kernels = ("ce_fwd_lse", "ce_bwd_dz", "ce_bwd_dh")
+    ce_kernels = ("ce_fwd_lse", "ce_logit_exp", "ce_bwd_dz", "ce_bwd_dh")
     dom = max(ce_kernels, key=lambda k: kern.get(k, {}).get("ms_per_step", 0.0))
-    # each of the three LM-head GEMM kernels contracts N x V x d once per step
+    # each LM-head GEMM kernel contracts N x V x d once per step
     per_step_flops = alg["ce_flops_fwd"]
     k = kern[dom]
     per_launch = per_step_flops / k["launches_per_step"]
@@ -260,8 +261,8 @@ def main():
                 "traffic": counter_traffic(args.config, dom),
                 "flops_per_launch": per_launch}
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
-                ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_bwd_dz",
-                 "ce_bwd_dh"))
+                ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_logit_exp",
+                 "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard"))
     ng_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("ngram_count", "ngram_weight"))
     lo_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("lora_u_du", "lora_dadb", "lora_reduce"))
     parts = {

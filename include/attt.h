@@ -107,7 +107,8 @@ attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_of
  * hidden       device [N, d] of dtype
  * lm_head      device [V, d] of dtype (the nn.Linear weight layout)
  * labels       device int32 [N], each in [0, V); a label outside that range is not an error
- *              the host can see: the bf16 path makes that row's loss term NaN
+ *              the host can see: the bf16 path makes that row's loss term NaN (and, with
+ *              grad_hidden, its lse and its gradient row), and never reads W at that label
  * weights      device float [N]
  * row_offsets  HOST int64 [E+1], from 0 to N, non-decreasing; NULL means one episode of N rows
  * num_episodes E >= 1

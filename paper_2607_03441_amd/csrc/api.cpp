@@ -47,7 +47,8 @@ namespace attt {
 
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
-    "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "lora_u_du", "lora_dadb", "lora_reduce"};
+    "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_logit_exp", "ce_overflow_guard", "lora_u_du", "lora_dadb",
+    "lora_reduce"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -321,9 +322,10 @@ constexpr int64_t kCeRowBlock = 8192;     // rows per backward block
 constexpr int64_t kCeVocabChunk = 32768;  // vocab columns per backward chunk
 
 struct CePlan {
-  CeGemmShape fwd{64, 64}, dz{64, 64}, dh{64, 64};
-  int64_t n_vb = 0, R = 0, Vc = 0, Vp = 0;
+  CeGemmShape fwd{64, 64}, lexp{64, 64}, dz{64, 64}, dh{64, 64};
+  int64_t n_vb = 0, n_vb_exp = 0, R = 0, Vc = 0, Vp = 0;
   size_t off_part = 0, off_label = 0, off_lse = 0, off_coef = 0, off_rowloss = 0;
+  size_t off_sa = 0, off_sb = 0, off_flag = 0;
   size_t off_wt = 0, off_dz = 0, off_acc = 0, total = 0;
 };
 
@@ -349,6 +351,7 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
     P.fwd = mfma_shape(N, V);
     P.Vc = std::min<int64_t>(round_up(V, 256), kCeVocabChunk);
     P.R = std::min<int64_t>(std::max<int64_t>(N, 1), kCeRowBlock);
+    P.lexp = mfma_shape(P.Vc, P.R);
     P.dz = mfma_shape(P.R, P.Vc);
     P.dh = mfma_shape(P.R, d);
     P.Vp = round_up(V, 256);
@@ -358,14 +361,21 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
     P.Vp = V;
   }
   P.n_vb = ceil_div(V, P.fwd.bn);
+  P.n_vb_exp = ceil_div(V, P.lexp.bm);
+  // The (max, sum) partials of the three-GEMM path and the sigma partials of the
+  // label-referenced path share one region: the second is consumed before the first is written.
+  const size_t part = std::max((size_t)N * P.n_vb * 8, (size_t)N * P.n_vb_exp * 4);
   size_t o = 0;
-  P.off_part = o;    o += align256((size_t)N * P.n_vb * 8);
+  P.off_part = o;    o += align256(part);
   P.off_label = o;   o += align256((size_t)N * 4);
   P.off_lse = o;     o += align256((size_t)N * 4);
   P.off_coef = o;    o += align256((size_t)N * 4);
   P.off_rowloss = o; o += align256((size_t)N * 4);
   if (grad && N > 0) {
     if (dtype == ATTT_BF16) {
+      P.off_sa = o;   o += align256((size_t)N * 4);
+      P.off_sb = o;   o += align256((size_t)N * 4);
+      P.off_flag = o; o += 256;
       P.off_wt = o;
       o += align256((size_t)d * P.Vp * 2);
     }
@@ -433,50 +443,114 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
   float* coef = reinterpret_cast<float*>(ws + P.off_coef);
   float* rowloss = reinterpret_cast<float*>(ws + P.off_rowloss);
   const int E = num_episodes;
-
-  HIP_TRY(launch_ce_fwd(dtype, P.fwd, hidden, lm_head, labels, (int)N, (int)d, (int)V, part,
-                        (int)P.n_vb, label_logit, s),
-          "ce_fwd_lse");
-  for (int e0 = 0; e0 < E; e0 += kEpBatch) {
-    CeEpBatch b{};
-    b.count = std::min(kEpBatch, E - e0);
-    b.first = e0;
-    int blocks = 0;
-    for (int i = 0; i < b.count; ++i) {
-      b.e[i].row0 = off[e0 + i];
-      b.e[i].L = (int32_t)(off[e0 + i + 1] - off[e0 + i]);
-      b.e[i].block_begin = blocks;
-      blocks += (int)ceil_div(b.e[i].L, 4);
+  if (N == 0) {
+    // every episode is empty: loss 0
+    for (int e0 = 0; e0 < E; e0 += kEpBatch) {
+      CeEpBatch b{};
+      b.count = std::min(kEpBatch, E - e0);
+      b.first = e0;
+      for (int i = 0; i < b.count; ++i) b.e[i].row0 = 0;
+      HIP_TRY(launch_ce_loss(b, rowloss, loss, nullptr, s), "ce_loss");
     }
-    HIP_TRY(launch_ce_row_reduce(b, blocks, part, (int)P.n_vb, label_logit, weights, lse_buf, coef,
-                                 rowloss, s),
-            "ce_row_reduce");
-    HIP_TRY(launch_ce_loss(b, rowloss, loss, s), "ce_loss");
+    return ATTT_OK;
   }
-  if (!grad || N == 0) return ATTT_OK;
-
+  auto batches = [&](int rows_per_block, auto&& fn) -> attt_status {
+    for (int e0 = 0; e0 < E; e0 += kEpBatch) {
+      CeEpBatch b{};
+      b.count = std::min(kEpBatch, E - e0);
+      b.first = e0;
+      int blocks = 0;
+      for (int i = 0; i < b.count; ++i) {
+        b.e[i].row0 = off[e0 + i];
+        b.e[i].L = (int32_t)(off[e0 + i + 1] - off[e0 + i]);
+        b.e[i].block_begin = blocks;
+        blocks += (int)ceil_div(b.e[i].L, rows_per_block);
+      }
+      attt_status st2 = fn(b, blocks);
+      if (st2) return st2;
+    }
+    return ATTT_OK;
+  };
+  // The three-GEMM algorithm: forward (max, sum exp) partials -> lse, w CE, loss; then per
+  // (row block, vocab chunk) dZ = coef (softmax - onehot) and dH (+)= dZ W. With `gate` set it
+  // runs only when the flag is raised.
   void* dz = ws + P.off_dz;
-  void* wt = nullptr;
+  void* wt = (grad && dtype == ATTT_BF16) ? ws + P.off_wt : nullptr;
   float* acc = P.off_acc ? reinterpret_cast<float*>(ws + P.off_acc) : nullptr;
+  auto three_gemm = [&](const int* gate) -> attt_status {
+    HIP_TRY(launch_ce_fwd(dtype, P.fwd, hidden, lm_head, labels, (int)N, (int)d, (int)V, part,
+                          (int)P.n_vb, label_logit, gate, s),
+            "ce_fwd_lse");
+    attt_status st2 = batches(4, [&](const CeEpBatch& b, int blocks) -> attt_status {
+      HIP_TRY(launch_ce_row_reduce(b, blocks, part, (int)P.n_vb, label_logit, weights, lse_buf, coef,
+                                   rowloss, gate, s),
+              "ce_row_reduce");
+      HIP_TRY(launch_ce_loss(b, rowloss, loss, gate, s), "ce_loss");
+      return ATTT_OK;
+    });
+    if (st2 || !grad) return st2;
+    for (int64_t r0 = 0; r0 < N; r0 += P.R) {
+      const int64_t R = std::min(P.R, N - r0);
+      for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
+        const int64_t width = std::min(P.Vc, V - c0);
+        const bool first = c0 == 0, last = c0 + P.Vc >= V;
+        HIP_TRY(launch_ce_bwd_dz(dtype, P.dz, hidden, lm_head, labels, lse_buf, coef, (int)r0, (int)R,
+                                 (int)d, (int)c0, (int)width, (int)V, dz, (int)P.Vc, gate, s),
+                "ce_bwd_dz");
+        const int64_t K = dtype == ATTT_BF16 ? round_up(width, 64) : round_up(width, 16);
+        HIP_TRY(launch_ce_bwd_dh(dtype, P.dh, dz, (int)P.Vc, lm_head, wt, (int)P.Vp, (int)r0, (int)R,
+                                 (int)d, (int)c0, (int)K, (int)V, acc, grad_hidden, first, last,
+                                 CeRowScale{}, gate, s),
+                "ce_bwd_dh");
+      }
+    }
+    return ATTT_OK;
+  };
+
   if (dtype == ATTT_BF16) {
-    wt = ws + P.off_wt;
-    HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)P.Vp, wt, s), "ce_head_transpose");
+    int* flag = grad ? reinterpret_cast<int*>(ws + P.off_flag) : nullptr;
+    HIP_TRY(launch_ce_label(hidden, lm_head, labels, (int)N, (int)d, (int)V, label_logit, flag, s),
+            "ce_label_logit");
   }
+  if (!grad || dtype != ATTT_BF16) return three_gemm(nullptr);
+
+  // bf16 forward + backward: the label-referenced two-GEMM pass, then the guard.
+  int* flag = reinterpret_cast<int*>(ws + P.off_flag);
+  float* sig_part = reinterpret_cast<float*>(ws + P.off_part);
+  float* sa = reinterpret_cast<float*>(ws + P.off_sa);
+  float* sb = reinterpret_cast<float*>(ws + P.off_sb);
+  st = batches(256, [&](const CeEpBatch& b, int blocks) -> attt_status {
+    HIP_TRY(launch_ce_coef(b, blocks, weights, coef, s), "ce_coef");
+    return ATTT_OK;
+  });
+  if (st) return st;
+  HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)P.Vp, wt, s), "ce_head_transpose");
+  const CeRowScale rs{sa, sb, labels};
   for (int64_t r0 = 0; r0 < N; r0 += P.R) {
     const int64_t R = std::min(P.R, N - r0);
     for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
       const int64_t width = std::min(P.Vc, V - c0);
       const bool first = c0 == 0, last = c0 + P.Vc >= V;
-      HIP_TRY(launch_ce_bwd_dz(dtype, P.dz, hidden, lm_head, labels, lse_buf, coef, (int)r0, (int)R,
-                               (int)d, (int)c0, (int)width, (int)V, dz, (int)P.Vc, s),
-              "ce_bwd_dz");
-      const int64_t K = dtype == ATTT_BF16 ? round_up(width, 64) : round_up(width, 16);
+      HIP_TRY(launch_ce_logit_exp(P.lexp, hidden, lm_head, labels, label_logit, (int)r0, (int)R, (int)d,
+                                  (int)c0, (int)width, (int)V, sig_part, (int)P.n_vb_exp, dz, (int)P.Vc,
+                                  flag, s),
+              "ce_logit_exp");
+      if (last)
+        HIP_TRY(launch_ce_row_final((int)r0, (int)R, sig_part, (int)P.n_vb_exp, label_logit, weights, coef,
+                                    lse_buf, rowloss, sa, sb, s),
+                "ce_row_final");
       HIP_TRY(launch_ce_bwd_dh(dtype, P.dh, dz, (int)P.Vc, lm_head, wt, (int)P.Vp, (int)r0, (int)R,
-                               (int)d, (int)c0, (int)K, (int)V, acc, grad_hidden, first, last, s),
+                               (int)d, (int)c0, (int)round_up(width, 64), (int)V, acc, grad_hidden, first,
+                               last, rs, nullptr, s),
               "ce_bwd_dh");
     }
   }
-  return ATTT_OK;
+  st = batches(4, [&](const CeEpBatch& b, int) -> attt_status {
+    HIP_TRY(launch_ce_loss(b, rowloss, loss, nullptr, s), "ce_loss");
+    return ATTT_OK;
+  });
+  if (st) return st;
+  return three_gemm(flag);
 }
 
 // ------------------------------------------------------------------------------------------

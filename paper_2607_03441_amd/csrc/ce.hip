@@ -1,15 +1,26 @@
 // Token-weighted cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10), forward and
 // backward with respect to the hidden states, on gfx950.
 //
-// Forward (logits never leave the chip): one GEMM z = h W^T over (row tile, vocab tile)
-// whose epilogue reduces every row of the tile to (max, sum exp(z - max)) and picks the
-// label logit. A row kernel merges the partials into lse and w * CE; an episode kernel sums
-// those in a fixed order into loss_e = (1/L_e) sum w_t CE_t.
+// Forward only (logits never leave the chip): one GEMM z = h W^T over (vocab tile, row tile)
+// whose epilogue reduces every row of the tile to (max, sum exp(z - max)). A row kernel merges
+// the partials into lse and w * CE; an episode kernel sums those in a fixed order into
+// loss_e = (1/L_e) sum w_t CE_t.
 //
-// Backward, per vocab chunk: a GEMM recomputes the chunk's logits and its epilogue forms
-// dZ = (w_t / L_e)(exp(z - lse_t) - [v == y_t]) directly from the accumulators, stored in
-// the GEMM operand dtype into a bounded staging buffer; a second GEMM accumulates
-// dH += dZ_chunk W_chunk in float32 and the last chunk writes dH in the output dtype.
+// Forward + backward (bf16): two GEMMs over the vocabulary, the algorithmic 4 N V d flops.
+// Every row takes its own label logit r_t = z_{t,y_t} as the exponent reference, so the first
+// GEMM can form e_tv = exp(z_tv - r_t) without knowing lse:
+//     sigma_t = sum_{v != y_t} e_tv,   lse_t = r_t + log1p(sigma_t),   CE_t = log1p(sigma_t)
+//     dL/dh_t = (w_t / L_e) (U_t - sigma_t W_{y_t}) / (1 + sigma_t),  U_t = sum_{v != y_t} e_tv W_v
+// which is (w_t / L_e)(softmax(z_t) - onehot(y_t)) W rewritten; the label term is kept out of
+// the sums, so nothing cancels when p_y is close to 1. Per vocab chunk, the first GEMM
+// (ce_logit_exp) stores e (bf16) into a bounded staging buffer and the per-row sums of its
+// tile; the second (ce_bwd_dh) accumulates U += e_chunk W_chunk in float32. After the last
+// chunk's first GEMM a row kernel forms sigma, lse and CE, and the last dh epilogue applies
+// the row scale and the label term. r_t is one of the row's logits, so sigma never
+// underflows; a logit more than kExpRange above r_t (a label with probability below e^-64)
+// could overflow e, and sets a flag on which the exact three-GEMM path (forward lse, then
+// dZ = (w/L)(exp(z - lse) - onehot) and dH = dZ W) reruns in full, overwriting the outputs.
+// Its kernels read the flag first and return at once when it is clear.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16. A 256x256 tile runs on 8 waves (2x4, 128x64
 // each, two waves per SIMD); small problems use 128x128 on 4 waves. K advances 64 per stage,
@@ -20,7 +31,8 @@
 // XCD-aware: workgroup i runs on XCD i%8, each XCD takes a contiguous range of the order, and
 // the order walks groups of 8 row tiles column by column, so the workgroups resident on one
 // XCD share a few hidden and LM-head panels in its L2.
-// f32 path: plain VALU tiles (64x64, 4x4 per thread); it serves the float32 configuration.
+// f32 path: plain VALU tiles (64x64, 4x4 per thread) running the three-GEMM algorithm; it
+// serves the float32 configuration.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -318,7 +330,8 @@ __global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(const bf16_t* __rest
                                                             const bf16_t* __restrict__ W,
                                                             int N, int d, int V, int tiles_v,
                                                             int tiles_t, float2* __restrict__ partials,
-                                                            int n_vb) {
+                                                            int n_vb, const int* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   extern __shared__ __align__(16) uint8_t smem[];
   int tv, tt;
   tile_of(blockIdx.x, tiles_v, tiles_t, tv, tt);
@@ -372,8 +385,10 @@ __global__ __launch_bounds__(256) void ce_label_logit_bf16_kernel(const bf16_t* 
                                                                   const bf16_t* __restrict__ W,
                                                                   const int32_t* __restrict__ labels,
                                                                   int N, int d, int V,
-                                                                  float* __restrict__ label_logit) {
+                                                                  float* __restrict__ label_logit,
+                                                                  int* __restrict__ flag) {
   const int lane = threadIdx.x & 63;
+  if (flag && blockIdx.x == 0 && threadIdx.x == 0) *flag = 0;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= N) return;
   const int y = labels[row];
@@ -402,7 +417,9 @@ template <class C>
 __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
     const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
     const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
-    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
+    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz,
+    const int* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   extern __shared__ __align__(16) uint8_t smem[];
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -433,7 +450,9 @@ __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
   }
 }
 
-// bf16 backward part 2: dH[r0 + m, n] (+)= sum_k dZ[m, k] WT[n, c0 + k].
+// bf16 backward part 2: acc[m, n] (+)= sum_k S[m, k] WT[n, c0 + k] over the staged chunk S.
+// The last chunk writes dH: acc itself (S = dZ), or, with row scales (S = e),
+// dH_t = sa_t acc_t - sb_t W_{y_t} (sa = coef / (1 + sigma), sb = coef sigma / (1 + sigma)).
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restrict__ dz, int ldz,
                                                            const bf16_t* __restrict__ WT, int Vp,
@@ -441,7 +460,12 @@ __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restr
                                                            int tiles_m, int tiles_n,
                                                            float* __restrict__ accbuf,
                                                            bf16_t* __restrict__ grad, int first,
-                                                           int last) {
+                                                           int last, const float* __restrict__ sa,
+                                                           const float* __restrict__ sb,
+                                                           const int32_t* __restrict__ labels,
+                                                           const bf16_t* __restrict__ W, int V,
+                                                           const int* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   extern __shared__ __align__(16) uint8_t smem[];
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -457,6 +481,16 @@ __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restr
     for (int r = 0; r < 16; ++r) {
       const int rl = m0 + wm * C::WTM + i * 32 + mfma_row(r, lane);
       if (rl >= R) continue;
+      float a = 1.0f, b = 0.0f;
+      const bf16_t* wy = nullptr;
+      if (last && sa) {
+        const int row = r0 + rl;
+        a = sa[row];
+        b = sb[row];
+        const int y = labels[row];
+        if (y >= 0 && y < V) wy = W + (int64_t)y * d;
+        else a = __int_as_float(0x7FC00000);  // outside the contract: NaN row, no read
+      }
 #pragma unroll
       for (int j = 0; j < C::TN; ++j) {
         const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
@@ -464,13 +498,159 @@ __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restr
         float v = acc[i][j][r];
         const int64_t o = (int64_t)rl * d + col;
         if (!first) v += accbuf[o];
-        if (last)
+        if (last) {
+          if (sa) v = a * v - (wy ? b * bf16_bits_to_f32(wy[col]) : 0.0f);
           grad[(int64_t)(r0 + rl) * d + col] = (bf16_t)f32_to_bf16_bits(v);
-        else
+        } else {
           accbuf[o] = v;
+        }
       }
     }
   }
+}
+
+// bf16 backward part 1, label-referenced: the chunk's logits transposed (vocab rows x token
+// columns, as in the forward), then for token t (local row of the block), with r_t its label
+// logit, e_tv = exp(z_tv - r_t) for v != y_t and v < V, zero otherwise. e goes in bf16 into
+// staging [R, ldz] (vocab contiguous), each lane storing 32 bytes per MFMA tile after one
+// half-wave exchange; the tile's per-token sum of e (float32) goes to sig_part[t][vocab tile].
+// A logit above r_t + kExpRange sets *flag.
+constexpr float kExpRange = 64.0f;
+
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_logit_exp_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
+    const float* __restrict__ label_logit, int r0, int R, int d, int c0, int cend, int tiles_v,
+    int tiles_t, float* __restrict__ sig_part, int n_vb, bf16_t* __restrict__ ez, int ldz,
+    int* __restrict__ flag) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  int tv, tt;
+  tile_of(blockIdx.x, tiles_v, tiles_t, tv, tt);
+  const int v0 = c0 + tv * C::BM, t0 = tt * C::BN;
+  f32x16 acc[C::TM][C::TN];
+  mfma_mainloop<C>(W + (int64_t)v0 * d, d, cend - v0, h + (int64_t)(r0 + t0) * d, d, R - t0, d,
+                   reinterpret_cast<bf16_t*>(smem), acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  float* red = reinterpret_cast<float*>(smem);  // [WGM][BN]
+  const int vb = v0 + wm * C::WTM;              // vocab id of this wave's first tile row
+  const bool full = v0 + C::BM <= cend;         // no tile row past the chunk
+  constexpr float kLog2e = 1.4426950408889634f;
+  constexpr float kOverSum = 6.2351491e27f;  // e^kExpRange
+  bool over = false;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int tl = wn * C::WTN + j * 32 + (lane & 31);
+    const int t = t0 + tl;
+    const bool tok = t < R;
+    float ref = 0.0f;
+    int y = -1;
+    if (tok) {
+      ref = label_logit[r0 + t];
+      y = labels[r0 + t];
+    }
+    const float nref = -ref * kLog2e;
+    const int ylane = y - vb - 4 * (lane >> 5);
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      // Register r holds vocab row 8 (r/4) + 4 (lane/32) + r%4 of the 32-row MFMA tile. The
+      // per-element label and range tests run only when some lane's label lies in this MFMA
+      // tile or the tile crosses the chunk's end.
+      const int yl = ylane - i * 32;
+      const bool mine = yl >= 0 && yl < 32 && (yl & 4) == 0;
+      float e[16];
+      if (!full || __ballot(mine) != 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = vb + i * 32 + mfma_row(r, lane);
+          e[r] = (v < cend && v != y) ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, nref)) : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, nref));
+      }
+      uint32_t pk[8];
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        sum += e[r];
+        sum += e[r + 1];
+        pk[r >> 1] = pack_bf16x2(e[r], e[r + 1]);
+      }
+      // Lanes 0-31 hold rows {0-3, 8-11, 16-19, 24-27}, lanes 32-63 the other four groups.
+      // Swapping groups {16-19, 24-27} of the low half with {4-7, 12-15} of the high half
+      // leaves rows 0-15 in the low lanes and rows 16-31 in the high lanes, in the same
+      // register order for both.
+      uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
+        P[k] = sw[0];
+        Q[k] = sw[1];
+      }
+      if (tok) {
+        u32x4* dst = reinterpret_cast<u32x4*>(ez + (int64_t)t * ldz + (vb - c0) + i * 32 + (lane >> 5) * 16);
+        dst[0] = u32x4{P[0], P[1], Q[0], Q[1]};
+        dst[1] = u32x4{P[2], P[3], Q[2], Q[3]};
+      }
+    }
+    // A single e above e^64 makes the lane's sum exceed it; a sum above it from several
+    // smaller terms only runs the exact path needlessly.
+    over |= sum > kOverSum;
+    sum += __shfl_xor(sum, 32, 64);
+    if (lane < 32) red[wm * C::BN + tl] = sum;
+  }
+  if (over) *flag = 1;
+  __syncthreads();
+  for (int tl = threadIdx.x; tl < C::BN; tl += C::NT) {
+    const int t = t0 + tl;
+    if (t >= R) continue;
+    float sum = red[tl];
+#pragma unroll
+    for (int w = 1; w < C::WGM; ++w) sum += red[w * C::BN + tl];
+    sig_part[(int64_t)(r0 + t) * n_vb + v0 / C::BM] = sum;
+  }
+}
+
+// Rows [r0, r0 + R) after the last chunk's first GEMM: sigma_t = sum of the vocab-tile
+// partials (fixed order), lse_t = r_t + log1p(sigma_t), row loss w_t log1p(sigma_t), and the
+// row scales of the dH epilogue. One wave per row.
+__global__ __launch_bounds__(256) void ce_row_final_kernel(int r0, int R, const float* __restrict__ sig_part,
+                                                           int n_vb, const float* __restrict__ label_logit,
+                                                           const float* __restrict__ weights,
+                                                           const float* __restrict__ coef,
+                                                           float* __restrict__ lse,
+                                                           float* __restrict__ rowloss,
+                                                           float* __restrict__ sa, float* __restrict__ sb) {
+  const int lane = threadIdx.x & 63;
+  const int local = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (local >= R) return;
+  const int64_t row = (int64_t)r0 + local;
+  float sum = 0.0f;
+  for (int i = lane; i < n_vb; i += 64) sum += sig_part[row * n_vb + i];
+  sum = group_sum<64>(sum);
+  if (lane == 0) {
+    const float ce = log1pf(sum);
+    const float inv = __fdiv_rn(1.0f, 1.0f + sum);
+    const float c = coef[row];
+    lse[row] = label_logit[row] + ce;
+    rowloss[row] = weights[row] * ce;
+    sa[row] = c * inv;
+    sb[row] = c * (sum * inv);
+  }
+}
+
+// coef_t = w_t / L_e for every row of the batch's episodes, 256 rows per block.
+__global__ __launch_bounds__(256) void ce_coef_kernel(CeEpBatch b, const float* __restrict__ weights,
+                                                      float* __restrict__ coef) {
+  int ei = 0;
+  while (ei + 1 < b.count && b.e[ei + 1].block_begin <= (int)blockIdx.x) ++ei;
+  const CeEp E = b.e[ei];
+  const int local = ((int)blockIdx.x - E.block_begin) * 256 + threadIdx.x;
+  if (local >= E.L) return;
+  const int64_t row = E.row0 + local;
+  coef[row] = __fdiv_rn(weights[row], (float)E.L);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -613,7 +793,9 @@ __global__ __launch_bounds__(256) void ce_row_reduce_kernel(CeEpBatch b,
                                                             const float* __restrict__ weights,
                                                             float* __restrict__ lse,
                                                             float* __restrict__ coef,
-                                                            float* __restrict__ rowloss) {
+                                                            float* __restrict__ rowloss,
+                                                            const int* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   int ei = 0;
   while (ei + 1 < b.count && b.e[ei + 1].block_begin <= (int)blockIdx.x) ++ei;
   const CeEp E = b.e[ei];
@@ -641,7 +823,9 @@ __global__ __launch_bounds__(256) void ce_row_reduce_kernel(CeEpBatch b,
 }
 
 __global__ __launch_bounds__(256) void ce_loss_kernel(CeEpBatch b, const float* __restrict__ rowloss,
-                                                      float* __restrict__ loss) {
+                                                      float* __restrict__ loss,
+                                                      const int* __restrict__ gate) {
+  if (gate && *gate == 0) return;
   const CeEp E = b.e[blockIdx.x];
   double acc = 0.0;
   for (int i = threadIdx.x; i < E.L; i += blockDim.x) acc += (double)rowloss[E.row0 + i];
@@ -703,8 +887,8 @@ static hipError_t allow_big_lds(Kern k) {
 }
 
 template <class C>
-static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, int N, int d,
-                           int V, float2* partials, int n_vb, float* label_logit, hipStream_t s) {
+static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, int N, int d, int V, float2* partials,
+                           int n_vb, const int* gate, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_fwd_bf16_kernel<C>);
@@ -712,28 +896,21 @@ static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labe
     attr = true;
   }
   const int tv = (V + C::BM - 1) / C::BM, tt = (N + C::BN - 1) / C::BN;
-  {
-    KernelTimer t(K_CE_FWD, s);
-    hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V, tv,
-                       tt, partials, n_vb);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  KernelTimer t(K_CE_LABEL, s);
-  hipLaunchKernelGGL(ce_label_logit_bf16_kernel, dim3((N + 3) / 4), dim3(256), 0, s, h, W, labels, N, d,
-                     V, label_logit);
+  KernelTimer t(gate ? K_CE_GUARD : K_CE_FWD, s);
+  hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V, tv,
+                     tt, partials, n_vb, gate);
   return hipGetLastError();
 }
 
 hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
                          const int32_t* labels, int N, int d, int V, float2* partials, int n_vb,
-                         float* label_logit, hipStream_t s) {
+                         float* label_logit, const int* gate, hipStream_t s) {
   if (N == 0) return hipSuccess;
   if (dtype == 1) {
     const bf16_t* hb = static_cast<const bf16_t*>(h);
     const bf16_t* Wb = static_cast<const bf16_t*>(W);
-    if (t.bm == 256) return fwd_bf16<CfgBig>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
-    return fwd_bf16<CfgSmall>(hb, Wb, labels, N, d, V, partials, n_vb, label_logit, s);
+    if (t.bm == 256) return fwd_bf16<CfgBig>(hb, Wb, N, d, V, partials, n_vb, gate, s);
+    return fwd_bf16<CfgSmall>(hb, Wb, N, d, V, partials, n_vb, gate, s);
   }
   const int tm = (N + kVT - 1) / kVT, tn = (V + kVT - 1) / kVT;
   KernelTimer tt(K_CE_FWD, s);
@@ -743,20 +920,40 @@ hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
   return hipGetLastError();
 }
 
-hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const float2* partials,
-                                int n_vb, const float* label_logit, const float* weights,
-                                float* lse, float* coef, float* rowloss, hipStream_t s) {
-  if (total_blocks <= 0) return hipSuccess;
-  KernelTimer t(K_CE_ROW_REDUCE, s);
-  hipLaunchKernelGGL(ce_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
-                     label_logit, weights, lse, coef, rowloss);
+hipError_t launch_ce_label(const void* h, const void* W, const int32_t* labels, int N, int d, int V,
+                           float* label_logit, int* flag, hipStream_t s) {
+  if (N == 0) return hipSuccess;
+  KernelTimer t(K_CE_LABEL, s);
+  hipLaunchKernelGGL(ce_label_logit_bf16_kernel, dim3((N + 3) / 4), dim3(256), 0, s,
+                     static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(W), labels, N, d, V,
+                     label_logit, flag);
   return hipGetLastError();
 }
 
-hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, hipStream_t s) {
+hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const float2* partials,
+                                int n_vb, const float* label_logit, const float* weights,
+                                float* lse, float* coef, float* rowloss, const int* gate,
+                                hipStream_t s) {
+  if (total_blocks <= 0) return hipSuccess;
+  KernelTimer t(gate ? K_CE_GUARD : K_CE_ROW_REDUCE, s);
+  hipLaunchKernelGGL(ce_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
+                     label_logit, weights, lse, coef, rowloss, gate);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, const int* gate,
+                          hipStream_t s) {
   if (b.count <= 0) return hipSuccess;
-  KernelTimer t(K_CE_LOSS, s);
-  hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss);
+  KernelTimer t(gate ? K_CE_GUARD : K_CE_LOSS, s);
+  hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss, gate);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_coef(const CeEpBatch& b, int total_blocks, const float* weights, float* coef,
+                          hipStream_t s) {
+  if (total_blocks <= 0) return hipSuccess;
+  KernelTimer t(K_CE_ROW_REDUCE, s);
+  hipLaunchKernelGGL(ce_coef_kernel, dim3(total_blocks), dim3(256), 0, s, b, weights, coef);
   return hipGetLastError();
 }
 
@@ -768,9 +965,52 @@ hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* W
 }
 
 template <class C>
+static hipError_t logit_exp_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels,
+                                 const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
+                                 float* sig_part, int n_vb, bf16_t* ez, int ldz, int* flag,
+                                 hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = allow_big_lds(ce_logit_exp_bf16_kernel<C>);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int tv = (Vc + C::BM - 1) / C::BM, tt = (R + C::BN - 1) / C::BN;
+  const int cend = min(c0 + Vc, V);
+  KernelTimer t(K_CE_LOGIT_EXP, s);
+  hipLaunchKernelGGL(ce_logit_exp_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, labels,
+                     label_logit, r0, R, d, c0, cend, tv, tt, sig_part, n_vb, ez, ldz, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_logit_exp(CeGemmShape t, const void* h, const void* W, const int32_t* labels,
+                               const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
+                               float* sig_part, int n_vb, void* ez, int ldz, int* flag, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  const bf16_t* hb = static_cast<const bf16_t*>(h);
+  const bf16_t* Wb = static_cast<const bf16_t*>(W);
+  bf16_t* z = static_cast<bf16_t*>(ez);
+  if (t.bm == 256)
+    return logit_exp_bf16<CfgBig>(hb, Wb, labels, label_logit, r0, R, d, c0, Vc, V, sig_part, n_vb, z, ldz,
+                                  flag, s);
+  return logit_exp_bf16<CfgSmall>(hb, Wb, labels, label_logit, r0, R, d, c0, Vc, V, sig_part, n_vb, z, ldz,
+                                  flag, s);
+}
+
+hipError_t launch_ce_row_final(int r0, int R, const float* sig_part, int n_vb, const float* label_logit,
+                               const float* weights, const float* coef, float* lse, float* rowloss,
+                               float* sa, float* sb, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  KernelTimer t(K_CE_ROW_REDUCE, s);
+  hipLaunchKernelGGL(ce_row_final_kernel, dim3((R + 3) / 4), dim3(256), 0, s, r0, R, sig_part, n_vb,
+                     label_logit, weights, coef, lse, rowloss, sa, sb);
+  return hipGetLastError();
+}
+
+template <class C>
 static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, const float* lse,
                           const float* coef, int r0, int R, int d, int c0, int Vc, int V, bf16_t* dz,
-                          int ldz, hipStream_t s) {
+                          int ldz, const int* gate, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_dz_bf16_kernel<C>);
@@ -779,22 +1019,23 @@ static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* label
   }
   const int tm = (R + C::BM - 1) / C::BM, tn = (Vc + C::BN - 1) / C::BN;
   const int cend = min(c0 + Vc, V);
-  KernelTimer t(K_CE_BWD_DZ, s);
+  KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DZ, s);
   hipLaunchKernelGGL(ce_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
-                     coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz);
+                     coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz, gate);
   return hipGetLastError();
 }
 
 hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
                             const int32_t* labels, const float* lse, const float* coef, int r0,
-                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, hipStream_t s) {
+                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, const int* gate,
+                            hipStream_t s) {
   if (R == 0) return hipSuccess;
   if (dtype == 1) {
     const bf16_t* hb = static_cast<const bf16_t*>(h);
     const bf16_t* Wb = static_cast<const bf16_t*>(W);
     bf16_t* z = static_cast<bf16_t*>(dz);
-    if (t.bm == 256) return dz_bf16<CfgBig>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
-    return dz_bf16<CfgSmall>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, s);
+    if (t.bm == 256) return dz_bf16<CfgBig>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, gate, s);
+    return dz_bf16<CfgSmall>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, gate, s);
   }
   const int tm = (R + kVT - 1) / kVT, tn = (Vc + kVT - 1) / kVT;
   const int cend = min(c0 + Vc, V);
@@ -808,7 +1049,7 @@ hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void*
 template <class C>
 static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, int r0, int R, int d,
                           int c0, int K, float* acc, bf16_t* grad, bool first, bool last,
-                          hipStream_t s) {
+                          const CeRowScale& rs, const bf16_t* W, int V, const int* gate, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_dh_bf16_kernel<C>);
@@ -816,22 +1057,25 @@ static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, i
     attr = true;
   }
   const int tm = (R + C::BM - 1) / C::BM, tn = (d + C::BN - 1) / C::BN;
-  KernelTimer t(K_CE_BWD_DH, s);
+  KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
   hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
-                     R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0);
+                     R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb, rs.labels,
+                     W, V, gate);
   return hipGetLastError();
 }
 
 hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
                             const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
-                            float* acc, void* grad, bool first, bool last, hipStream_t s) {
+                            float* acc, void* grad, bool first, bool last, const CeRowScale& rs,
+                            const int* gate, hipStream_t s) {
   if (R == 0) return hipSuccess;
   if (dtype == 1) {
     const bf16_t* z = static_cast<const bf16_t*>(dz);
     const bf16_t* wt = static_cast<const bf16_t*>(WT);
+    const bf16_t* w = static_cast<const bf16_t*>(W);
     bf16_t* g = static_cast<bf16_t*>(grad);
-    if (t.bm == 256) return dh_bf16<CfgBig>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
-    return dh_bf16<CfgSmall>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, s);
+    if (t.bm == 256) return dh_bf16<CfgBig>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, rs, w, V, gate, s);
+    return dh_bf16<CfgSmall>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, rs, w, V, gate, s);
   }
   const int tm = (R + kVT - 1) / kVT, tn = (d + kVT - 1) / kVT;
   KernelTimer tt(K_CE_BWD_DH, s);

@@ -18,6 +18,8 @@ enum KernelId {
   K_CE_HEAD_T,
   K_CE_BWD_DZ,
   K_CE_BWD_DH,
+  K_CE_LOGIT_EXP,
+  K_CE_GUARD,
   K_LORA_U,
   K_LORA_DADB,
   K_LORA_REDUCE,
@@ -112,26 +114,54 @@ struct CeGemmShape {
   int bm, bn;
 };
 
-// Forward: per (row, vocab tile) partial (max, sum exp) and the label logit.
+// Forward: per (row, vocab tile) partial (max, sum exp); the f32 kernel also writes the label
+// logits. `gate` (nullable): when non-null the kernels return at once unless *gate != 0.
 hipError_t launch_ce_fwd(int dtype, CeGemmShape t, const void* h, const void* W,
                          const int32_t* labels, int N, int d, int V, float2* partials, int n_vb,
-                         float* label_logit, hipStream_t s);
+                         float* label_logit, const int* gate, hipStream_t s);
+// bf16 label logits z_{t, y_t}; NaN for a label outside [0, V). Clears *flag when non-null.
+hipError_t launch_ce_label(const void* h, const void* W, const int32_t* labels, int N, int d, int V,
+                           float* label_logit, int* flag, hipStream_t s);
 hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const float2* partials,
                                 int n_vb, const float* label_logit, const float* weights,
-                                float* lse, float* coef, float* rowloss, hipStream_t s);
-hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, hipStream_t s);
+                                float* lse, float* coef, float* rowloss, const int* gate,
+                                hipStream_t s);
+hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss, const int* gate,
+                          hipStream_t s);
+// coef_t = w_t / L_e (256 rows per block).
+hipError_t launch_ce_coef(const CeEpBatch& b, int total_blocks, const float* weights, float* coef,
+                          hipStream_t s);
 // W [V, d] -> WT [d, Vp] (bf16 only), zero columns V .. Vp-1.
 hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* WT, hipStream_t s);
+// bf16, label-referenced: e = exp(z - z_y) (0 at the label and past V) for rows [r0, r0+R) x
+// vocab [c0, c0+Vc) into staging [R, ldz]; per (row, vocab tile of t.bm) sums into
+// sig_part [N, n_vb]; sets *flag when a logit exceeds its reference by more than 64.
+hipError_t launch_ce_logit_exp(CeGemmShape t, const void* h, const void* W, const int32_t* labels,
+                               const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
+                               float* sig_part, int n_vb, void* ez, int ldz, int* flag, hipStream_t s);
+// Rows [r0, r0+R): sigma, lse, row loss and the dH row scales (sa, sb).
+hipError_t launch_ce_row_final(int r0, int R, const float* sig_part, int n_vb, const float* label_logit,
+                               const float* weights, const float* coef, float* lse, float* rowloss,
+                               float* sa, float* sb, hipStream_t s);
 // dZ chunk: rows [r0, r0+R) x vocab [c0, c0+Vc) of coef * (softmax - onehot), into
 // staging [R, ldz] (dtype), zero past V.
 hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
                             const int32_t* labels, const float* lse, const float* coef, int r0,
-                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, hipStream_t s);
-// dH rows [r0, r0+R) (+)= dZ chunk . W[c0 : c0+K]: f32 path reads W [V, d]; bf16 path reads
-// WT [d, Vp]. first: no accumulator read; last: write grad (dtype) instead of acc (f32).
+                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, const int* gate,
+                            hipStream_t s);
+// Row scales of the label-referenced dH epilogue; all null for the plain dZ chunks.
+struct CeRowScale {
+  const float* sa = nullptr;
+  const float* sb = nullptr;
+  const int32_t* labels = nullptr;
+};
+// dH rows [r0, r0+R) (+)= staged chunk . W[c0 : c0+K]: f32 path reads W [V, d]; bf16 path reads
+// WT [d, Vp]. first: no accumulator read; last: write grad (dtype) instead of acc (f32), with
+// the row scales when rs.sa is set (bf16 only).
 hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
                             const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
-                            float* acc, void* grad, bool first, bool last, hipStream_t s);
+                            float* acc, void* grad, bool first, bool last, const CeRowScale& rs,
+                            const int* gate, hipStream_t s);
 
 // ---- LoRA ------------------------------------------------------------------------------
 constexpr int kLoraBatch = 16;

@@ -11,7 +11,7 @@ from gpu_util import cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
 from oracle import ce as oce
 from oracle import lora as olora
 from oracle import ngram as ongram
-from workloads import Workload, pack_episodes, random_dense
+from workloads import Dense, Workload, pack_episodes, random_dense
 
 pytestmark = pytest.mark.gpu
 
@@ -170,6 +170,53 @@ def test_ce_forward_only_matches(attt):
     b = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
                                  dev_f32(w), want_grad=True)
     assert host(a[0]).tobytes() == host(b[0]).tobytes()
+
+
+def test_ce_bf16_overflow_guard(attt):
+    """Label logits far below the row maximum (gaps beyond 90 nats): exp(z - z_y) would
+    overflow float32, so the result must come from the exact three-GEMM path."""
+    N, d, V = 301, 128, 3000
+    h = random_dense((N, d), 60.0, True, 31)
+    W = random_dense((V, d), 0.05, True, 32)
+    rng = np.random.default_rng(33)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    z = h.f32.astype(np.float64) @ W.f32.astype(np.float64).T
+    gap = z.max(1) - z[np.arange(N), labels]
+    assert np.sum(gap > 90) >= 10          # the label-referenced sums alone would overflow
+    weights = rng.uniform(0.05, 1, N).astype(np.float32)
+    note("ce bf16 overflow guard")
+    _ce_case(attt, h, W, labels, weights, np.array([0, 100, N], np.int64), True)
+
+
+def test_ce_bf16_confident_labels(attt):
+    """p_y within about 1e-5 of 1: the gradient rows are small differences, computed without
+    cancellation (the label term is kept out of the sums)."""
+    N, d, V = 257, 128, 3000
+    W = random_dense((V, d), 0.05, True, 41)
+    rng = np.random.default_rng(42)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    Wy = W.f32[labels].astype(np.float64)
+    hv = 20.0 * Wy / np.sum(Wy * Wy, 1, keepdims=True) + rng.normal(0, 0.2, (N, d))
+    h = Dense(hv.astype(np.float32), True)
+    z = h.f32.astype(np.float64) @ W.f32.astype(np.float64).T
+    zy = z[np.arange(N), labels]
+    zo = z.copy()
+    zo[np.arange(N), labels] = -np.inf
+    assert np.median(zy - zo.max(1)) > 10   # the label wins by a wide margin
+    weights = np.ones(N, np.float32)
+    note("ce bf16 confident labels")
+    _ce_case(attt, h, W, labels, weights, np.array([0, N], np.int64), True)
+
+
+def test_ce_bf16_forward_only_agrees(attt):
+    wl = Workload("c2")
+    ce = wl.ce()
+    w = np.random.default_rng(6).uniform(0.05, 1, 2048).astype(np.float32)
+    args = (dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]), dev_f32(w))
+    fo = [host(t) for t in attt.weighted_ce_fwd_bwd(*args, want_grad=False)[:2]]
+    fb = [host(t) for t in attt.weighted_ce_fwd_bwd(*args, want_grad=True)[:2]]
+    assert np.max(np.abs(fo[0] - fb[0]) / np.abs(fb[0])) <= 1e-5
+    assert np.max(np.abs(fo[1] - fb[1]) / np.abs(fb[1])) <= 1e-5
 
 
 def test_ce_deterministic(attt):
