@@ -141,11 +141,11 @@ KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_logit_exp": "attt::ce_logit_
                  "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_"}
 
 
-def counter_traffic(config, kernel):
+def counter_traffic(workload, kernel):
     """HBM bytes per dispatch of `kernel` from the committed rocprofv3 counter summary of this
     workload, or None when there is none or the kernel sources changed since it was taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"{config}_kernels_hbm.md")
+    path = os.path.join(ROOT, "profiles", f"{workload}_kernels_hbm.md")
     if not os.path.exists(path):
         return None
     rec = None
@@ -258,7 +258,7 @@ def main():
     achieved = per_launch / (k["avg_launch_ms"] * 1e-3)
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": peak / 1e12,
                 "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": counter_traffic(args.config, dom),
+                "traffic": counter_traffic(cfg.name, dom),
                 "flops_per_launch": per_launch}
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
                 ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_logit_exp",

@@ -326,12 +326,9 @@ __device__ __forceinline__ int mfma_row(int r, int lane) { return ((r >> 2) << 3
 // two-wave merge in LDS, instead of a 32-lane shuffle tree per row.
 // ------------------------------------------------------------------------------------------
 template <class C>
-__global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(const bf16_t* __restrict__ h,
-                                                            const bf16_t* __restrict__ W,
-                                                            int N, int d, int V, int tiles_v,
-                                                            int tiles_t, float2* __restrict__ partials,
-                                                            int n_vb, const int* __restrict__ gate) {
-  if (gate && *gate == 0) return;
+__device__ __forceinline__ void ce_fwd_bf16_body(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, int N, int d, int V, int tiles_v,
+    int tiles_t, float2* __restrict__ partials, int n_vb) {
   extern __shared__ __align__(16) uint8_t smem[];
   int tv, tt;
   tile_of(blockIdx.x, tiles_v, tiles_t, tv, tt);
@@ -379,6 +376,20 @@ __global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(const bf16_t* __rest
     partials[(int64_t)t * n_vb + tv] = make_float2(m, s);
   }
 }
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, int N, int d, int V, int tiles_v,
+    int tiles_t, float2* __restrict__ partials, int n_vb) {
+  ce_fwd_bf16_body<C>(h, W, N, d, V, tiles_v, tiles_t, partials, n_vb);
+}
+// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_guard_fwd_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, int N, int d, int V, int tiles_v,
+    int tiles_t, float2* __restrict__ partials, int n_vb, const int* __restrict__ gate) {
+  if (*gate == 0) return;
+  ce_fwd_bf16_body<C>(h, W, N, d, V, tiles_v, tiles_t, partials, n_vb);
+}
 
 // Label logit z_{t, y_t} = h_t . W_{y_t} (float32 accumulation), one wave per row.
 __global__ __launch_bounds__(256) void ce_label_logit_bf16_kernel(const bf16_t* __restrict__ h,
@@ -414,12 +425,10 @@ __global__ __launch_bounds__(256) void ce_label_logit_bf16_kernel(const bf16_t* 
 
 // bf16 backward part 1: dZ for rows [r0, r0+R) x vocab [c0, c0 + tiles_n*BN) into staging.
 template <class C>
-__global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
+__device__ __forceinline__ void ce_dz_bf16_body(
     const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
     const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
-    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz,
-    const int* __restrict__ gate) {
-  if (gate && *gate == 0) return;
+    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
   extern __shared__ __align__(16) uint8_t smem[];
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -449,23 +458,34 @@ __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
     }
   }
 }
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
+    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
+    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
+  ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
+}
+// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_guard_dz_bf16_kernel(
+    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
+    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
+    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz,
+    const int* __restrict__ gate) {
+  if (*gate == 0) return;
+  ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
+}
 
 // bf16 backward part 2: acc[m, n] (+)= sum_k S[m, k] WT[n, c0 + k] over the staged chunk S.
 // The last chunk writes dH: acc itself (S = dZ), or, with row scales (S = e),
 // dH_t = sa_t acc_t - sb_t W_{y_t} (sa = coef / (1 + sigma), sb = coef sigma / (1 + sigma)).
 template <class C>
-__global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restrict__ dz, int ldz,
-                                                           const bf16_t* __restrict__ WT, int Vp,
-                                                           int r0, int R, int d, int c0, int K,
-                                                           int tiles_m, int tiles_n,
-                                                           float* __restrict__ accbuf,
-                                                           bf16_t* __restrict__ grad, int first,
-                                                           int last, const float* __restrict__ sa,
-                                                           const float* __restrict__ sb,
-                                                           const int32_t* __restrict__ labels,
-                                                           const bf16_t* __restrict__ W, int V,
-                                                           const int* __restrict__ gate) {
-  if (gate && *gate == 0) return;
+__device__ __forceinline__ void ce_dh_bf16_body(
+    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
+    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
+    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
+    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
+    int V) {
   extern __shared__ __align__(16) uint8_t smem[];
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
@@ -507,6 +527,28 @@ __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(const bf16_t* __restr
       }
     }
   }
+}
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(
+    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
+    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
+    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
+    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
+    int V) {
+  ce_dh_bf16_body<C>(dz, ldz, WT, Vp, r0, R, d, c0, K, tiles_m, tiles_n, accbuf, grad, first, last,
+                     sa, sb, labels, W, V);
+}
+// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
+template <class C>
+__global__ __launch_bounds__(C::NT) void ce_guard_dh_bf16_kernel(
+    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
+    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
+    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
+    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
+    int V, const int* __restrict__ gate) {
+  if (*gate == 0) return;
+  ce_dh_bf16_body<C>(dz, ldz, WT, Vp, r0, R, d, c0, K, tiles_m, tiles_n, accbuf, grad, first, last,
+                     sa, sb, labels, W, V);
 }
 
 // bf16 backward part 1, label-referenced: the chunk's logits transposed (vocab rows x token
@@ -786,16 +828,10 @@ __global__ __launch_bounds__(256) void ce_dh_f32_kernel(const float* __restrict_
 // ------------------------------------------------------------------------------------------
 // Row and episode reductions, LM-head transpose.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void ce_row_reduce_kernel(CeEpBatch b,
-                                                            const float2* __restrict__ partials,
-                                                            int n_vb,
-                                                            const float* __restrict__ label_logit,
-                                                            const float* __restrict__ weights,
-                                                            float* __restrict__ lse,
-                                                            float* __restrict__ coef,
-                                                            float* __restrict__ rowloss,
-                                                            const int* __restrict__ gate) {
-  if (gate && *gate == 0) return;
+__device__ __forceinline__ void ce_row_reduce_body(
+    CeEpBatch b, const float2* __restrict__ partials, int n_vb,
+    const float* __restrict__ label_logit, const float* __restrict__ weights,
+    float* __restrict__ lse, float* __restrict__ coef, float* __restrict__ rowloss) {
   int ei = 0;
   while (ei + 1 < b.count && b.e[ei + 1].block_begin <= (int)blockIdx.x) ++ei;
   const CeEp E = b.e[ei];
@@ -821,11 +857,24 @@ __global__ __launch_bounds__(256) void ce_row_reduce_kernel(CeEpBatch b,
     rowloss[row] = w * (l - label_logit[row]);
   }
 }
+__global__ __launch_bounds__(256) void ce_row_reduce_kernel(
+    CeEpBatch b, const float2* __restrict__ partials, int n_vb,
+    const float* __restrict__ label_logit, const float* __restrict__ weights,
+    float* __restrict__ lse, float* __restrict__ coef, float* __restrict__ rowloss) {
+  ce_row_reduce_body(b, partials, n_vb, label_logit, weights, lse, coef, rowloss);
+}
+// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
+__global__ __launch_bounds__(256) void ce_guard_row_reduce_kernel(
+    CeEpBatch b, const float2* __restrict__ partials, int n_vb,
+    const float* __restrict__ label_logit, const float* __restrict__ weights,
+    float* __restrict__ lse, float* __restrict__ coef, float* __restrict__ rowloss,
+    const int* __restrict__ gate) {
+  if (*gate == 0) return;
+  ce_row_reduce_body(b, partials, n_vb, label_logit, weights, lse, coef, rowloss);
+}
 
-__global__ __launch_bounds__(256) void ce_loss_kernel(CeEpBatch b, const float* __restrict__ rowloss,
-                                                      float* __restrict__ loss,
-                                                      const int* __restrict__ gate) {
-  if (gate && *gate == 0) return;
+__device__ __forceinline__ void ce_loss_body(
+    CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss) {
   const CeEp E = b.e[blockIdx.x];
   double acc = 0.0;
   for (int i = threadIdx.x; i < E.L; i += blockDim.x) acc += (double)rowloss[E.row0 + i];
@@ -838,6 +887,17 @@ __global__ __launch_bounds__(256) void ce_loss_kernel(CeEpBatch b, const float* 
     const double t = (part[0] + part[1]) + (part[2] + part[3]);
     loss[b.first + blockIdx.x] = E.L > 0 ? (float)(t / (double)E.L) : 0.0f;
   }
+}
+__global__ __launch_bounds__(256) void ce_loss_kernel(
+    CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss) {
+  ce_loss_body(b, rowloss, loss);
+}
+// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
+__global__ __launch_bounds__(256) void ce_guard_loss_kernel(
+    CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss,
+    const int* __restrict__ gate) {
+  if (*gate == 0) return;
+  ce_loss_body(b, rowloss, loss);
 }
 
 // W [V, d] -> WT [d, Vp] in 64 x 64 tiles: 16-byte global reads along d, 16-byte global writes
@@ -892,13 +952,18 @@ static hipError_t fwd_bf16(const bf16_t* h, const bf16_t* W, int N, int d, int V
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_fwd_bf16_kernel<C>);
+    if (e == hipSuccess) e = allow_big_lds(ce_guard_fwd_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int tv = (V + C::BM - 1) / C::BM, tt = (N + C::BN - 1) / C::BN;
   KernelTimer t(gate ? K_CE_GUARD : K_CE_FWD, s);
-  hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V, tv,
-                     tt, partials, n_vb, gate);
+  if (gate)
+    hipLaunchKernelGGL(ce_guard_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V,
+                       tv, tt, partials, n_vb, gate);
+  else
+    hipLaunchKernelGGL(ce_fwd_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, N, d, V, tv,
+                       tt, partials, n_vb);
   return hipGetLastError();
 }
 
@@ -936,8 +1001,12 @@ hipError_t launch_ce_row_reduce(const CeEpBatch& b, int total_blocks, const floa
                                 hipStream_t s) {
   if (total_blocks <= 0) return hipSuccess;
   KernelTimer t(gate ? K_CE_GUARD : K_CE_ROW_REDUCE, s);
-  hipLaunchKernelGGL(ce_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
-                     label_logit, weights, lse, coef, rowloss, gate);
+  if (gate)
+    hipLaunchKernelGGL(ce_guard_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
+                       label_logit, weights, lse, coef, rowloss, gate);
+  else
+    hipLaunchKernelGGL(ce_row_reduce_kernel, dim3(total_blocks), dim3(256), 0, s, b, partials, n_vb,
+                       label_logit, weights, lse, coef, rowloss);
   return hipGetLastError();
 }
 
@@ -945,7 +1014,10 @@ hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss,
                           hipStream_t s) {
   if (b.count <= 0) return hipSuccess;
   KernelTimer t(gate ? K_CE_GUARD : K_CE_LOSS, s);
-  hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss, gate);
+  if (gate)
+    hipLaunchKernelGGL(ce_guard_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss, gate);
+  else
+    hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss);
   return hipGetLastError();
 }
 
@@ -1014,14 +1086,19 @@ static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* label
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_dz_bf16_kernel<C>);
+    if (e == hipSuccess) e = allow_big_lds(ce_guard_dz_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int tm = (R + C::BM - 1) / C::BM, tn = (Vc + C::BN - 1) / C::BN;
   const int cend = min(c0 + Vc, V);
   KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DZ, s);
-  hipLaunchKernelGGL(ce_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
-                     coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz, gate);
+  if (gate)
+    hipLaunchKernelGGL(ce_guard_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
+                       coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz, gate);
+  else
+    hipLaunchKernelGGL(ce_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
+                       coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz);
   return hipGetLastError();
 }
 
@@ -1053,14 +1130,20 @@ static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, i
   static bool attr = false;
   if (!attr) {
     hipError_t e = allow_big_lds(ce_dh_bf16_kernel<C>);
+    if (e == hipSuccess) e = allow_big_lds(ce_guard_dh_bf16_kernel<C>);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int tm = (R + C::BM - 1) / C::BM, tn = (d + C::BN - 1) / C::BN;
   KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
-  hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
-                     R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb, rs.labels,
-                     W, V, gate);
+  if (gate)
+    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp,
+                       r0, R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
+                       rs.labels, W, V, gate);
+  else
+    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
+                       R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
+                       rs.labels, W, V);
   return hipGetLastError();
 }
 
