@@ -83,9 +83,7 @@ using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
 // instead of branching. Valid offsets stay far below kRsrcBytes (a tile spans < 256 rows).
 constexpr uint32_t kOOB = 0x7FFFFFF0u;
 constexpr int kRsrcBytes = 0x40000000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, kRsrcBytes, 0x00020000);
-}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p) { return buffer_rsrc(p, kRsrcBytes); }
 __device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
