@@ -353,7 +353,7 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
     P.R = std::min<int64_t>(std::max<int64_t>(N, 1), kCeRowBlock);
     P.lexp = mfma_shape(P.Vc, P.R);
     P.dz = mfma_shape(P.R, P.Vc);
-    P.dh = mfma_shape(P.R, d);
+    P.dh = mfma_shape(d, P.R);
     P.Vp = round_up(V, 256);
   } else {
     P.Vc = std::min<int64_t>(round_up(V, 64), kCeVocabChunk);
@@ -383,8 +383,9 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
     o += align256((size_t)P.R * P.Vc * esz);
     const bool chunks = V > P.Vc;
     if (dtype == ATTT_BF16 && chunks) {
+      // float32 partial dH in the dH kernel's tile layout: whole bm x bn tiles
       P.off_acc = o;
-      o += align256((size_t)P.R * d * 4);
+      o += align256((size_t)ceil_div(d, P.dh.bm) * ceil_div(P.R, P.dh.bn) * P.dh.bm * P.dh.bn * 4);
     }
   }
   P.total = std::max<size_t>(o, 256);

@@ -374,12 +374,14 @@ __device__ __forceinline__ void ce_fwd_bf16_body(
     partials[(int64_t)t * n_vb + tv] = make_float2(m, s);
   }
 }
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_fwd_bf16_kernel(
     const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, int N, int d, int V, int tiles_v,
     int tiles_t, float2* __restrict__ partials, int n_vb) {
   ce_fwd_bf16_body<C>(h, W, N, d, V, tiles_v, tiles_t, partials, n_vb);
 }
+
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_guard_fwd_bf16_kernel(
@@ -456,6 +458,7 @@ __device__ __forceinline__ void ce_dz_bf16_body(
     }
   }
 }
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
     const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
@@ -463,6 +466,7 @@ __global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
     int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
   ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
 }
+
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_guard_dz_bf16_kernel(
@@ -474,9 +478,11 @@ __global__ __launch_bounds__(C::NT) void ce_guard_dz_bf16_kernel(
   ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
 }
 
-// bf16 backward part 2: acc[m, n] (+)= sum_k S[m, k] WT[n, c0 + k] over the staged chunk S.
-// The last chunk writes dH: acc itself (S = dZ), or, with row scales (S = e),
-// dH_t = sa_t acc_t - sb_t W_{y_t} (sa = coef / (1 + sigma), sb = coef sigma / (1 + sigma)).
+// bf16 backward part 2, transposed like the forward: acc[n, t] (+)= sum_k WT[n, c0 + k] S[t, k]
+// over the staged chunk S (n a column of dH, t a row of the block), so every lane holds one
+// row t and runs of four consecutive columns. The last chunk writes dH: acc itself (S = dZ),
+// or, with row scales (S = e), dH_t = sa_t acc_t - sb_t W_{y_t} (sa = coef / (1 + sigma),
+// sb = coef sigma / (1 + sigma)), as 32-byte stores.
 template <class C>
 __device__ __forceinline__ void ce_dh_bf16_body(
     const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
@@ -487,45 +493,102 @@ __device__ __forceinline__ void ce_dh_bf16_body(
   extern __shared__ __align__(16) uint8_t smem[];
   int tm, tn;
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * C::BM, n0 = tn * C::BN;
+  const int m0 = tm * C::BM, n0 = tn * C::BN;  // m0: first column of dH, n0: first row of the block
   f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(dz + (int64_t)m0 * ldz, ldz, R - m0, WT + (int64_t)n0 * Vp + c0, Vp, d - n0, K,
+  mfma_mainloop<C>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
                    reinterpret_cast<bf16_t*>(smem), acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WGN, wn = wave % C::WGN;
+  // The float32 partial sums between chunks keep the accumulators' register layout: per tile,
+  // per (MFMA tile i, j, quarter q of the 16 registers), the workgroup's threads hold 16
+  // contiguous bytes each, so every read and write is a coalesced 16-byte access. Every launch
+  // of one call uses the same tiling, so a tile reads back exactly what it wrote.
+  // Buffer accesses: the per-slot offset is a scalar, the lane's offset the only vector operand.
+  // The first chunk reads through an empty range (zeros), so the add needs no branch.
+  float* tbase = accbuf + (size_t)(tm * tiles_n + tn) * (C::BM * C::BN);
+  const __amdgpu_buffer_rsrc_t racc = buffer_rsrc(tbase, C::BM * C::BN * 4);
+  const __amdgpu_buffer_rsrc_t rprev = buffer_rsrc(tbase, first ? 0 : C::BM * C::BN * 4);
+  const uint32_t voff = threadIdx.x * 16u;
+  auto soff = [](int i, int j, int q) { return (uint32_t)(((i * C::TN + j) * 4 + q) * C::NT * 16); };
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
+  for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = m0 + wm * C::WTM + i * 32 + mfma_row(r, lane);
-      if (rl >= R) continue;
-      float a = 1.0f, b = 0.0f;
-      const bf16_t* wy = nullptr;
-      if (last && sa) {
-        const int row = r0 + rl;
-        a = sa[row];
-        b = sb[row];
-        const int y = labels[row];
-        if (y >= 0 && y < V) wy = W + (int64_t)y * d;
-        else a = __int_as_float(0x7FC00000);  // outside the contract: NaN row, no read
+    for (int j = 0; j < C::TN; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 p = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rprev, voff, soff(i, j, q), 0));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += p[e];
       }
+      __builtin_amdgcn_sched_barrier(0);  // one MFMA tile's partials in flight at a time: no spills
+    }
+  if (!last) {
 #pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int col = n0 + wn * C::WTN + j * 32 + (lane & 31);
-        if (col >= d) continue;
-        float v = acc[i][j][r];
-        const int64_t o = (int64_t)rl * d + col;
-        if (!first) v += accbuf[o];
-        if (last) {
-          if (sa) v = a * v - (wy ? b * bf16_bits_to_f32(wy[col]) : 0.0f);
-          grad[(int64_t)(r0 + rl) * d + col] = (bf16_t)f32_to_bf16_bits(v);
-        } else {
-          accbuf[o] = v;
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), racc, voff, soff(i, j, q), 0);
         }
+    return;
+  }
+  const int hi = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < C::TN; ++j) {
+    const int tl = n0 + wn * C::WTN + j * 32 + (lane & 31);  // row of the block
+    const bool tok = tl < R;
+    float a = 1.0f, b = 0.0f;
+    const bf16_t* wy = nullptr;
+    if (tok && sa) {
+      const int row = r0 + tl;
+      a = sa[row];
+      b = sb[row];
+      const int y = labels[row];
+      if (y >= 0 && y < V) wy = W + (int64_t)y * d;
+      else a = __int_as_float(0x7FC00000);  // outside the contract: NaN row, no read
+    }
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      const int cb = m0 + wm * C::WTM + i * 32;  // column of the MFMA tile's first row
+      // register r holds column cb + 8 (r/4) + 4 (lane/32) + r%4: four runs of four columns
+      uint32_t pk[8];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = cb + 8 * g + 4 * hi;
+        float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (wy && c + 4 <= d) {
+          const uint2 u = *reinterpret_cast<const uint2*>(wy + c);
+          wv[0] = bf16_bits_to_f32(u.x & 0xFFFFu);
+          wv[1] = bf16_bits_to_f32(u.x >> 16);
+          wv[2] = bf16_bits_to_f32(u.y & 0xFFFFu);
+          wv[3] = bf16_bits_to_f32(u.y >> 16);
+        }
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = a * acc[i][j][4 * g + e] - b * wv[e];
+        pk[2 * g] = pack_bf16x2(v[0], v[1]);
+        pk[2 * g + 1] = pack_bf16x2(v[2], v[3]);
+      }
+      // same half-wave exchange as the first GEMM: low lanes get columns 0-15, high 16-31
+      uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
+        P[k] = sw[0];
+        Q[k] = sw[1];
+      }
+      const int c0w = cb + 16 * hi;  // d % 8 == 0: a run of 16 is whole, half, or absent
+      if (tok && c0w + 8 <= d) {
+        u32x4* dst = reinterpret_cast<u32x4*>(grad + (int64_t)(r0 + tl) * d + c0w);
+        dst[0] = u32x4{P[0], P[1], Q[0], Q[1]};
+        if (c0w + 16 <= d) dst[1] = u32x4{P[2], P[3], Q[2], Q[3]};
       }
     }
   }
 }
+
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(
     const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
@@ -536,6 +599,7 @@ __global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(
   ce_dh_bf16_body<C>(dz, ldz, WT, Vp, r0, R, d, c0, K, tiles_m, tiles_n, accbuf, grad, first, last,
                      sa, sb, labels, W, V);
 }
+
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_guard_dh_bf16_kernel(
@@ -855,12 +919,14 @@ __device__ __forceinline__ void ce_row_reduce_body(
     rowloss[row] = w * (l - label_logit[row]);
   }
 }
+
 __global__ __launch_bounds__(256) void ce_row_reduce_kernel(
     CeEpBatch b, const float2* __restrict__ partials, int n_vb,
     const float* __restrict__ label_logit, const float* __restrict__ weights,
     float* __restrict__ lse, float* __restrict__ coef, float* __restrict__ rowloss) {
   ce_row_reduce_body(b, partials, n_vb, label_logit, weights, lse, coef, rowloss);
 }
+
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
 __global__ __launch_bounds__(256) void ce_guard_row_reduce_kernel(
     CeEpBatch b, const float2* __restrict__ partials, int n_vb,
@@ -886,10 +952,12 @@ __device__ __forceinline__ void ce_loss_body(
     loss[b.first + blockIdx.x] = E.L > 0 ? (float)(t / (double)E.L) : 0.0f;
   }
 }
+
 __global__ __launch_bounds__(256) void ce_loss_kernel(
     CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss) {
   ce_loss_body(b, rowloss, loss);
 }
+
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
 __global__ __launch_bounds__(256) void ce_guard_loss_kernel(
     CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss,
@@ -1132,7 +1200,7 @@ static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, i
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int tm = (R + C::BM - 1) / C::BM, tn = (d + C::BN - 1) / C::BN;
+  const int tm = (d + C::BM - 1) / C::BM, tn = (R + C::BN - 1) / C::BN;  // transposed tiles
   KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
   if (gate)
     hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp,
