@@ -559,8 +559,14 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
 // ------------------------------------------------------------------------------------------
 namespace {
 
+struct LoraProb {
+  int64_t bt_off, ut_off, dut_off, pa_off, pb_off;
+  int32_t rp, rows_pad, splits;
+};
+
 struct LoraPlan {
-  std::vector<LoraJob> jobs;
+  std::vector<LoraProb> prob;           // per problem (entries of problems with rows > 0 used)
+  std::vector<std::vector<int>> chunks;  // problems sharing x, d_in and rows; <= 4 rank tiles each
   size_t total = 0;
 };
 
@@ -574,7 +580,7 @@ attt_status lora_validate(const attt_lora_problem* p, int32_t count, int32_t dty
       return fail(ATTT_EINVAL, "lora[%d]: rank must be in [1, %d] (got %d)", i, ATTT_LORA_MAX_RANK, q.rank);
     if (q.rows < 0 || q.d_in < 1 || q.d_out < 1 || q.d_in % 8 || q.d_out % 8)
       return fail(ATTT_EINVAL, "lora[%d]: need rows >= 0 and d_in, d_out positive multiples of 8", i);
-    if (q.rows >= ((int64_t)1 << 30) || q.d_in >= ((int64_t)1 << 24) || q.d_out >= ((int64_t)1 << 24))
+    if (q.rows >= ((int64_t)1 << 30) || q.d_in >= ((int64_t)1 << 20) || q.d_out >= ((int64_t)1 << 20))
       return fail(ATTT_EUNSUPPORTED, "lora[%d]: dimensions beyond this build's limits", i);
     if (!std::isfinite(q.scale)) return fail(ATTT_EINVAL, "lora[%d]: scale is not finite", i);
     if (!q.dA || !q.dB) return fail(ATTT_EINVAL, "lora[%d]: dA / dB is null", i);
@@ -588,34 +594,60 @@ attt_status lora_validate(const attt_lora_problem* p, int32_t count, int32_t dty
 LoraPlan lora_plan(const attt_lora_problem* p, int32_t count, int32_t dtype) {
   LoraPlan P;
   const size_t esz = dtype == ATTT_BF16 ? 2 : 4;
-  int64_t colblocks = 0;
-  for (int32_t i = 0; i < count; ++i)
-    if (p[i].rows > 0)
-      colblocks += ceil_div(p[i].d_in, kLoraColTile) + ceil_div(p[i].d_out, kLoraColTile);
+  P.prob.resize(count);
+  // Problems reading the same x (same pointer, d_in and rows) share pass-1 and dA jobs.
+  std::vector<int> tiles(count, 0);
+  for (int32_t i = 0; i < count; ++i) {
+    if (p[i].rows == 0) continue;
+    tiles[i] = (int)ceil_div(p[i].rank, 16);
+    bool placed = false;
+    for (auto& ch : P.chunks) {
+      const attt_lora_problem& f = p[ch[0]];
+      int used = 0;
+      for (int m : ch) used += tiles[m];
+      if (f.x == p[i].x && f.d_in == p[i].d_in && f.rows == p[i].rows && used + tiles[i] <= kLoraMaxTiles) {
+        ch.push_back(i);
+        placed = true;
+        break;
+      }
+    }
+    if (!placed) P.chunks.push_back({i});
+  }
+  // Row splits of pass 2: about 512 rows (eight steps of 64) per workgroup, at most 16 splits;
+  // shorter chains of dependent loads for more float32 partials.
   size_t o = 0;
   for (int32_t i = 0; i < count; ++i) {
     const attt_lora_problem& q = p[i];
     if (q.rows == 0) continue;
-    LoraJob J{};
-    J.x = q.x; J.dy = q.dy; J.A = q.A; J.B = q.B; J.dA = q.dA; J.dB = q.dB;
-    J.rows = (int32_t)q.rows;
-    J.rows_pad = (int32_t)round_up(q.rows, kLoraRowTile);
-    J.d_in = (int32_t)q.d_in;
-    J.d_out = (int32_t)q.d_out;
-    J.rank = q.rank;
-    J.rp = (int32_t)round_up(q.rank, 16);
-    J.scale = q.scale;
-    // Row splits of pass 2: about 1024 blocks over the whole group, at least 256 rows each.
-    const int64_t want = std::max<int64_t>(1, ceil_div(1024, std::max<int64_t>(colblocks, 1)));
-    J.splits = (int32_t)std::max<int64_t>(1, std::min<int64_t>(want, J.rows_pad / 256));
-    J.ut_off = (int64_t)o;  o += align256((size_t)J.rp * J.rows_pad * esz);
-    J.dut_off = (int64_t)o; o += align256((size_t)J.rp * J.rows_pad * esz);
-    J.pa_off = (int64_t)o;  o += align256((size_t)J.splits * J.rp * J.d_in * 4);
-    J.pb_off = (int64_t)o;  o += align256((size_t)J.splits * J.rp * J.d_out * 4);
-    P.jobs.push_back(J);
+    LoraProb& Q = P.prob[i];
+    Q.rp = tiles[i] * 16;
+    Q.rows_pad = (int32_t)round_up(q.rows, kLoraRowTile);
+    Q.splits = std::max(1, std::min(16, Q.rows_pad / 512));
+    Q.bt_off = (int64_t)o;  o += align256((size_t)Q.rp * q.d_out * esz);
+    Q.ut_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.rows_pad * esz);
+    Q.dut_off = (int64_t)o; o += align256((size_t)Q.rp * Q.rows_pad * esz);
+    Q.pa_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.splits * q.d_in * 4);
+    Q.pb_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.splits * q.d_out * 4);
   }
   P.total = std::max<size_t>(o, 256);
   return P;
+}
+
+// Launches `jobs` in batches of kLoraJobBatch; blocks(job) gives each job's workgroup count.
+template <class Job, class Blocks, class Launch>
+attt_status lora_launch_all(const std::vector<Job>& jobs, Blocks blocks, Launch launch, const char* name) {
+  for (size_t j0 = 0; j0 < jobs.size(); j0 += kLoraJobBatch) {
+    LoraBatchOf<Job> b{};
+    b.count = (int32_t)std::min<size_t>(kLoraJobBatch, jobs.size() - j0);
+    int total = 0;
+    for (int i = 0; i < b.count; ++i) {
+      b.j[i] = jobs[j0 + i];
+      b.j[i].b_begin = total;
+      total += blocks(b.j[i]);
+    }
+    HIP_TRY(launch(b, total), name);
+  }
+  return ATTT_OK;
 }
 
 }  // namespace
@@ -640,23 +672,110 @@ extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t
   if (!aligned256(workspace)) return fail(ATTT_EINVAL, "lora: workspace must be 256-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  for (size_t j0 = 0; j0 < P.jobs.size(); j0 += kLoraBatch) {
-    LoraBatch b{};
-    b.count = (int32_t)std::min<size_t>(kLoraBatch, P.jobs.size() - j0);
-    int b1 = 0, b2 = 0, b3 = 0;
-    for (int i = 0; i < b.count; ++i) {
-      LoraJob J = P.jobs[j0 + i];
-      J.b1_begin = b1;
-      b1 += 2 * (J.rows_pad / kLoraRowTile);
-      J.b2_begin = b2;
-      b2 += J.splits * (int)(ceil_div(J.d_in, kLoraColTile) + ceil_div(J.d_out, kLoraColTile));
-      J.b3_begin = b3;
-      b3 += (int)ceil_div((int64_t)J.rank * J.d_in + (int64_t)J.d_out * J.rank, 256);
-      b.j[i] = J;
+  const int64_t esz = dtype == ATTT_BF16 ? 2 : 4;
+
+  std::vector<LoraBTJob> bt;
+  std::vector<LoraP1Job> p1;
+  std::vector<LoraP2Job> p2;
+  std::vector<LoraRedJob> red;
+  auto add_tile1 = [](LoraP1Job& J, const void* op, int valid, float scale, int64_t out_off) {
+    LoraP1Tile& T = J.t[J.nt++];
+    T.op = op;
+    T.valid = valid;
+    T.scale = scale;
+    T.out_off = out_off;
+  };
+  auto add_tile2 = [](LoraP2Job& J, int64_t lt_off, int64_t part_off) {
+    LoraP2Tile& T = J.t[J.nt++];
+    T.lt_off = lt_off;
+    T.part_off = part_off;
+  };
+  // x jobs (shared by a chunk's problems): U tiles in pass 1, dA tiles in pass 2
+  for (const auto& ch : P.chunks) {
+    const attt_lora_problem& f = problems[ch[0]];
+    const LoraProb& F = P.prob[ch[0]];
+    LoraP1Job J1{};
+    J1.src = f.x;
+    J1.rows = (int32_t)f.rows;
+    J1.rows_pad = F.rows_pad;
+    J1.kdim = (int32_t)f.d_in;
+    LoraP2Job J2{};
+    J2.src = f.x;
+    J2.rows = (int32_t)f.rows;
+    J2.rows_pad = F.rows_pad;
+    J2.cols = (int32_t)f.d_in;
+    J2.splits = F.splits;
+    for (int i : ch) {
+      const attt_lora_problem& q = problems[i];
+      const LoraProb& Q = P.prob[i];
+      for (int t = 0; t < Q.rp / 16; ++t) {
+        add_tile1(J1, static_cast<const uint8_t*>(q.A) + (int64_t)16 * t * q.d_in * esz,
+                  std::min(16, q.rank - 16 * t), q.scale, Q.ut_off + (int64_t)16 * t * Q.rows_pad * esz);
+        add_tile2(J2, Q.dut_off + (int64_t)16 * t * Q.rows_pad * esz,
+                  Q.pa_off + (int64_t)t * Q.splits * 16 * q.d_in * 4);
+      }
     }
-    HIP_TRY(launch_lora_pass1(dtype, b, b1, ws, s), "lora_u_du");
-    HIP_TRY(launch_lora_pass2(dtype, b, b2, ws, s), "lora_dadb");
-    HIP_TRY(launch_lora_reduce(b, b3, ws, s), "lora_reduce");
+    p1.push_back(J1);
+    p2.push_back(J2);
   }
-  return ATTT_OK;
+  // dy jobs (one per problem): dU tiles in pass 1, dB tiles in pass 2; B^T; reduction
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_problem& q = problems[i];
+    if (q.rows == 0) continue;
+    const LoraProb& Q = P.prob[i];
+    LoraBTJob JB{};
+    JB.B = q.B;
+    JB.bt_off = Q.bt_off;
+    JB.rank = q.rank;
+    JB.rp = Q.rp;
+    JB.d_out = (int32_t)q.d_out;
+    bt.push_back(JB);
+    LoraP1Job J1{};
+    J1.src = q.dy;
+    J1.rows = (int32_t)q.rows;
+    J1.rows_pad = Q.rows_pad;
+    J1.kdim = (int32_t)q.d_out;
+    LoraP2Job J2{};
+    J2.src = q.dy;
+    J2.rows = (int32_t)q.rows;
+    J2.rows_pad = Q.rows_pad;
+    J2.cols = (int32_t)q.d_out;
+    J2.splits = Q.splits;
+    for (int t = 0; t < Q.rp / 16; ++t) {
+      add_tile1(J1, ws + Q.bt_off + (int64_t)16 * t * q.d_out * esz, 16, q.scale,
+                Q.dut_off + (int64_t)16 * t * Q.rows_pad * esz);
+      add_tile2(J2, Q.ut_off + (int64_t)16 * t * Q.rows_pad * esz,
+                Q.pb_off + (int64_t)t * Q.splits * 16 * q.d_out * 4);
+    }
+    p1.push_back(J1);
+    p2.push_back(J2);
+    LoraRedJob JR{};
+    JR.dA = q.dA;
+    JR.dB = q.dB;
+    JR.pa_off = Q.pa_off;
+    JR.pb_off = Q.pb_off;
+    JR.rank = q.rank;
+    JR.d_in = (int32_t)q.d_in;
+    JR.d_out = (int32_t)q.d_out;
+    JR.sa = Q.splits;
+    JR.sb = Q.splits;
+    red.push_back(JR);
+  }
+  st = lora_launch_all(
+      bt, [](const LoraBTJob& J) { return (int)ceil_div((int64_t)J.rp * J.d_out, 256); },
+      [&](const LoraBTBatch& b, int n) { return launch_lora_bt(dtype, b, n, ws, s); }, "lora_bt");
+  if (st) return st;
+  // pass 1: jobs sorted by tile count, each launch specialised on its batch's largest count
+  std::stable_sort(p1.begin(), p1.end(), [](const LoraP1Job& a, const LoraP1Job& b) { return a.nt > b.nt; });
+  st = lora_launch_all(
+      p1, [](const LoraP1Job& J) { return J.rows_pad / kLoraP1Rows; },
+      [&](const LoraP1Batch& b, int n) { return launch_lora_pass1(dtype, b.j[0].nt, b, n, ws, s); }, "lora_u_du");
+  if (st) return st;
+  st = lora_launch_all(
+      p2, [](const LoraP2Job& J) { return J.splits * (int)ceil_div(J.cols, kLoraColTile); },
+      [&](const LoraP2Batch& b, int n) { return launch_lora_pass2(dtype, b, n, ws, s); }, "lora_dadb");
+  if (st) return st;
+  return lora_launch_all(
+      red, [](const LoraRedJob& J) { return (int)ceil_div((int64_t)J.rank * J.d_in + (int64_t)J.d_out * J.rank, 256); },
+      [&](const LoraRedBatch& b, int n) { return launch_lora_reduce(b, n, ws, s); }, "lora_reduce");
 }

@@ -17,7 +17,7 @@
 // tile; the second (ce_bwd_dh) accumulates U += e_chunk W_chunk in float32. After the last
 // chunk's first GEMM a row kernel forms sigma, lse and CE, and the last dh epilogue applies
 // the row scale and the label term. r_t is one of the row's logits, so sigma never
-// underflows; a logit more than kExpRange above r_t (a label with probability below e^-64)
+// underflows; a logit more than 64 above r_t (a label with probability below e^-64)
 // could overflow e, and sets a flag on which the exact three-GEMM path (forward lse, then
 // dZ = (w/L)(exp(z - lse) - onehot) and dH = dZ W) reruns in full, overwriting the outputs.
 // Its kernels read the flag first and return at once when it is clear.
@@ -618,8 +618,7 @@ __global__ __launch_bounds__(C::NT) void ce_guard_dh_bf16_kernel(
 // logit, e_tv = exp(z_tv - r_t) for v != y_t and v < V, zero otherwise. e goes in bf16 into
 // staging [R, ldz] (vocab contiguous), each lane storing 32 bytes per MFMA tile after one
 // half-wave exchange; the tile's per-token sum of e (float32) goes to sig_part[t][vocab tile].
-// A logit above r_t + kExpRange sets *flag.
-constexpr float kExpRange = 64.0f;
+// A lane whose sum of e exceeds e^64 sets *flag.
 
 template <class C>
 __global__ __launch_bounds__(C::NT) void ce_logit_exp_bf16_kernel(
@@ -641,7 +640,7 @@ __global__ __launch_bounds__(C::NT) void ce_logit_exp_bf16_kernel(
   const int vb = v0 + wm * C::WTM;              // vocab id of this wave's first tile row
   const bool full = v0 + C::BM <= cend;         // no tile row past the chunk
   constexpr float kLog2e = 1.4426950408889634f;
-  constexpr float kOverSum = 6.2351491e27f;  // e^kExpRange
+  constexpr float kOverSum = 6.2351491e27f;  // e^64
   bool over = false;
 #pragma unroll
   for (int j = 0; j < C::TN; ++j) {

@@ -164,39 +164,77 @@ hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, c
                             const int* gate, hipStream_t s);
 
 // ---- LoRA ------------------------------------------------------------------------------
-constexpr int kLoraBatch = 16;
+constexpr int kLoraRowTile = 128;  // row padding of the transposed pass-1 results
+constexpr int kLoraP1Rows = 32;    // pass-1 rows per workgroup
+constexpr int kLoraKBlock = 128;   // pass-1 contraction step
+constexpr int kLoraColTile = 64;   // pass-2 output columns per workgroup
+constexpr int kLoraTStep = 64;     // pass-2 rows per step
+constexpr int kLoraMaxTiles = 4;   // rank tiles of 16 per job (64 ranks)
+constexpr int kLoraJobBatch = 16;  // jobs per launch (kernel-argument descriptors)
 
-struct LoraJob {
-  const void* x;
-  const void* dy;
-  const void* A;
-  const void* B;
+// Pass 1: rows of `src` [rows, kdim] times up to four rank tiles of row-major adapter
+// operands [rank, kdim] (A, or B^T in the workspace); tile t writes scale * (src op^T)^T as
+// [16, rows_pad] (operand dtype) at workspace offset out_off.
+struct LoraP1Tile {
+  const void* op;   // first row of the tile in its operand
+  int64_t out_off;
+  float scale;
+  int32_t valid;    // operand rows in the tile (rank - 16 t, at most 16); the rest read as zero
+};
+struct LoraP1Job {
+  const void* src;
+  int32_t rows, rows_pad, kdim, nt;
+  int32_t b_begin, pad;
+  LoraP1Tile t[kLoraMaxTiles];
+};
+
+// Pass 2: out[c, k] = sum_t L[c, t] src[t, k] per rank tile; L is a pass-1 result [16, rows_pad]
+// at lt_off; float32 partials [splits, 16, cols] at part_off.
+struct LoraP2Tile {
+  int64_t lt_off;
+  int64_t part_off;
+};
+struct LoraP2Job {
+  const void* src;
+  int32_t rows, rows_pad, cols, splits, nt;
+  int32_t b_begin;
+  LoraP2Tile t[kLoraMaxTiles];
+};
+
+// Reduce: dA [rank, d_in] += sum of the dA partials ([tiles, sa, 16, d_in] at pa_off), and
+// dB [d_out, rank] += the transposed sum of the dB partials ([tiles, sb, 16, d_out] at pb_off).
+struct LoraRedJob {
   float* dA;
   float* dB;
-  int64_t ut_off;    // workspace byte offset of s*U^T  [rp, rows_pad] (dtype)
-  int64_t dut_off;   // workspace byte offset of s*(dy B)^T [rp, rows_pad] (dtype)
-  int64_t pa_off;    // workspace byte offset of dA partials [splits, rp, d_in] f32
-  int64_t pb_off;    // workspace byte offset of dB partials [splits, rp, d_out] f32
-  int32_t rows, rows_pad, d_in, d_out, rank, rp, splits;
-  float scale;
-  int32_t b1_begin;  // first pass-1 block (U and dU row tiles)
-  int32_t b2_begin;  // first pass-2 block (dA / dB column blocks x splits)
-  int32_t b3_begin;  // first reduce block
-  int32_t pad;
+  int64_t pa_off, pb_off;
+  int32_t rank, d_in, d_out, sa, sb;
+  int32_t b_begin;
 };
 
-struct LoraBatch {
+// B [d_out, rank] -> B^T [rp, d_out] at bt_off.
+struct LoraBTJob {
+  const void* B;
+  int64_t bt_off;
+  int32_t rank, rp, d_out;
+  int32_t b_begin;
+};
+
+template <class J>
+struct LoraBatchOf {
   int32_t count;
   int32_t pad;
-  LoraJob j[kLoraBatch];
+  J j[kLoraJobBatch];
 };
+using LoraP1Batch = LoraBatchOf<LoraP1Job>;
+using LoraP2Batch = LoraBatchOf<LoraP2Job>;
+using LoraRedBatch = LoraBatchOf<LoraRedJob>;
+using LoraBTBatch = LoraBatchOf<LoraBTJob>;
 
-constexpr int kLoraRowTile = 128;   // pass-1 rows per block
-constexpr int kLoraColTile = 64;    // pass-2 output columns per block
-constexpr int kLoraTStep = 32;      // pass-2 contraction step over rows
-
-hipError_t launch_lora_pass1(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
-hipError_t launch_lora_pass2(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
-hipError_t launch_lora_reduce(const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+hipError_t launch_lora_bt(int dtype, const LoraBTBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+// nt: the largest rank-tile count of the batch's jobs (bf16 kernels are specialised on it)
+hipError_t launch_lora_pass1(int dtype, int nt, const LoraP1Batch& b, int blocks, uint8_t* ws,
+                             hipStream_t s);
+hipError_t launch_lora_pass2(int dtype, const LoraP2Batch& b, int blocks, uint8_t* ws, hipStream_t s);
+hipError_t launch_lora_reduce(const LoraRedBatch& b, int blocks, uint8_t* ws, hipStream_t s);
 
 }  // namespace attt

@@ -1,120 +1,160 @@
 // LoRA adapter gradients (episode-specific adapter, Sec. 3.1; rank / alpha, Appendix C) on
-// gfx950, for a group of adapted projections in one launch per pass.
+// gfx950, for a group of adapted projections.
 //
 // With U = x A^T and scale s:   dB = s dy^T U,   dA = (s dy B)^T x.
-// Pass 1 (lora_u_kernel): per 128-row tile, sU^T = s (x A^T)^T and dU^T = s (dy B)^T,
-//   contractions over d_in / d_out on MFMA 16x16x32 (rank padded to 16). Each lane streams
-//   64 contiguous bytes of an x (dy) row per step; the four MFMAs of the step take the four
-//   16-byte pieces, and the adapter operand in LDS is read with the same k order, so the
-//   result is the same sum while the row reads stay fully coalesced. The two results are
-//   stored transposed ([rank_pad, rows]) in the operand dtype for pass 2.
-// Pass 2 (lora_dadb_kernel): dA^T-style products over the rows: out[c, k] = sum_t
-//   dU^T[c, t] x[t, k] (and U^T dy for dB). The contraction runs over rows, which are the
-//   slow index of x, so a 32-row x 64-column tile of x is written transposed into LDS
-//   (16-bit stores) and read back as K-contiguous MFMA operands. Rows are split into
-//   `splits` ranges whose float32 partials go to the workspace.
-// Reduce (lora_reduce_kernel): sums the split partials in a fixed order and adds them to
-//   dA [r, d_in] and dB [d_out, r]. No float atomics: results are bit-reproducible.
-// The float32 path uses plain VALU loops with the same workspace layout.
+// Work is cut into rank tiles of 16 (rank padded to 16). Projections that read the same
+// input x (q, k, v of one layer) form one job of up to four tiles, so x is streamed once per
+// pass for all of them; dy differs per projection.
+//   B^T (lora_bt_kernel): B [d_out, r] -> B^T [r_pad, d_out] (zero rows past r), so both
+//     adapter operands are row-major [rank, k].
+//   Pass 1 (lora_p1_*): per 32 rows of x (or dy), s U^T = s (x A^T)^T (or s (dy B)^T) for all
+//     tiles of the job, on MFMA 16x16x32; the workgroup's four waves take a quarter of the
+//     contraction each. Operands are 16-byte loads in the MFMA's own k order (each instruction
+//     covers 64 contiguous bytes of 16 rows); the adapter fragments come from L2 straight into
+//     registers. The next step's rows are in flight while the current step's MFMAs run.
+//     Results are stored transposed ([16, rows_pad] per tile).
+//   Pass 2 (lora_p2_*): out[c, k] = sum_t L[c, t] src[t, k] with (L, src) = (s dU^T, x) for dA
+//     and (s U^T, dy) for dB. The contraction runs over rows, the slow index of src, so 64-row
+//     x 64-column tiles of src are written transposed into LDS (two rows per 32-bit store,
+//     double-buffered, one barrier per step) and read back as K-contiguous MFMA operands.
+//     Rows are split into `splits` ranges whose float32 partials go to the workspace.
+//   Reduce (lora_reduce_kernel): sums the split partials in a fixed order and adds them to
+//     dA [r, d_in] and dB [d_out, r]. No float atomics: results are bit-reproducible.
+// The float32 path runs the same jobs with plain VALU loops.
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace attt {
 
-template <class T>
-__device__ __forceinline__ int find_job(const LoraBatch& b, int bid, T member) {
+// Job of workgroup `bid`; wave-uniform (made explicit so the descriptors built from the job's
+// pointers live in scalar registers).
+template <class Batch>
+__device__ __forceinline__ int find_job(const Batch& b, int bid) {
   int j = 0;
-  while (j + 1 < b.count && b.j[j + 1].*member <= bid) ++j;
-  return j;
+  while (j + 1 < b.count && b.j[j + 1].b_begin <= bid) ++j;
+  return __builtin_amdgcn_readfirstlane(j);
 }
 
-constexpr int kP1KB = 128;  // pass-1 contraction block
-constexpr int kP1Pitch = kP1KB + 8;
+// ------------------------------------------------------------------------------------------
+// B [d_out, rank] -> B^T [rp, d_out], zero rows rank .. rp-1 (bf16 or float, by element size).
+// ------------------------------------------------------------------------------------------
+template <class T>
+__global__ __launch_bounds__(256) void lora_bt_kernel(LoraBTBatch b, uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraBTJob J = b.j[ji];
+  const int64_t idx = (int64_t)((int)blockIdx.x - J.b_begin) * 256 + threadIdx.x;
+  if (idx >= (int64_t)J.rp * J.d_out) return;
+  const int c = (int)(idx / J.d_out), k = (int)(idx % J.d_out);
+  const T* B = static_cast<const T*>(J.B);
+  T v = T(0);
+  if (c < J.rank) v = B[(int64_t)k * J.rank + c];
+  reinterpret_cast<T*>(ws + J.bt_off)[idx] = v;
+}
 
 // ------------------------------------------------------------------------------------------
 // bf16 pass 1
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void lora_u_bf16_kernel(LoraBatch b, uint8_t* __restrict__ ws) {
-  const int ji = find_job(b, (int)blockIdx.x, &LoraJob::b1_begin);
-  const LoraJob J = b.j[ji];
-  const int local = (int)blockIdx.x - J.b1_begin;
-  const int tiles = J.rows_pad / kLoraRowTile;
-  const int kind = local / tiles;  // 0: U from (x, A); 1: dU from (dy, B)
-  const int rt = local % tiles;
-  const bf16_t* src = static_cast<const bf16_t*>(kind == 0 ? J.x : J.dy);
-  const int kdim = kind == 0 ? J.d_in : J.d_out;
-  const bf16_t* Al = static_cast<const bf16_t*>(J.A);  // [rank, d_in]
-  const bf16_t* Bl = static_cast<const bf16_t*>(J.B);  // [d_out, rank]
-  bf16_t* outT = reinterpret_cast<bf16_t*>(ws + (kind == 0 ? J.ut_off : J.dut_off));
+constexpr uint32_t kOOB = 0x7FFFFFF0u;  // offset past every descriptor's range: loads return 0
 
-  __shared__ __align__(16) bf16_t lop[64 * kP1Pitch];  // adapter operand [c][k] for this block
+// A workgroup takes 32 rows; its four waves split the contraction into four ranges and their
+// partial sums meet in LDS, so each wave's chain of dependent loads is a quarter as long.
+// NT is the largest tile count of the batch; a job with fewer tiles skips the rest.
+template <int NT>
+__global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraP1Job& Jr = b.j[ji];
+  const int rt = (int)blockIdx.x - Jr.b_begin;
+  const int kdim = Jr.kdim, nt = Jr.nt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  const int nct = J.rp / 16;
-  f32x4 acc[2][4];
+  // this workgroup's 32 rows; rows past the input read as zero through the descriptor range
+  const int row0 = rt * kLoraP1Rows;
+  const int nrows = max(0, min(kLoraP1Rows, Jr.rows - row0));
+  const bf16_t* src = static_cast<const bf16_t*>(Jr.src) + (int64_t)row0 * kdim;
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, nrows * kdim * 2);
+  __amdgpu_buffer_rsrc_t ro[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    ro[t] = buffer_rsrc(t < nt ? Jr.t[t].op : src, t < nt ? Jr.t[t].valid * kdim * 2 : 0);
+  // this wave's contraction range, in whole pairs of steps
+  const int kq = ((kdim + 4 * 2 * kLoraKBlock - 1) / (4 * 2 * kLoraKBlock)) * 2 * kLoraKBlock;
+  const int kbeg = wave * kq, kend = min(kdim, kbeg + kq);
+
+  f32x4 acc[2][NT];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[a][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int row_base = rt * kLoraRowTile + wave * 32;
+    for (int t = 0; t < NT; ++t) acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kb = 0; kb < kdim; kb += kP1KB) {
-    __syncthreads();
-    if (kind == 0) {
-      for (int idx = tid; idx < J.rp * 16; idx += 256) {
-        const int c = idx >> 4, ch = idx & 15;
-        const int k = kb + ch * 8;
-        u32x4 v = u32x4{0u, 0u, 0u, 0u};
-        if (c < J.rank && k < kdim) v = *reinterpret_cast<const u32x4*>(Al + (int64_t)c * J.d_in + k);
-        *reinterpret_cast<u32x4*>(lop + c * kP1Pitch + ch * 8) = v;
-      }
-    } else {
-      for (int idx = tid; idx < J.rp * kP1KB; idx += 256) {
-        const int k = idx / J.rp, c = idx % J.rp;
-        bf16_t v = 0;
-        if (c < J.rank && kb + k < kdim) v = Bl[(int64_t)(kb + k) * J.rank + c];
-        lop[c * kP1Pitch + k] = v;
-      }
-    }
-    __syncthreads();
-    u32x4 xa[2][4];
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      const int row = row_base + a * 16 + l16;
-      const bf16_t* p = src + (int64_t)row * kdim + kb + g * 32;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int k = kb + g * 32 + q * 8;
-        xa[a][q] = (row < J.rows && k < kdim) ? *reinterpret_cast<const u32x4*>(p + q * 8)
-                                              : u32x4{0u, 0u, 0u, 0u};
-      }
-    }
+  // Step kb: for MFMA q, lane (l16, g) holds rows a*16 + l16 at k = kb + q*32 + g*8 .. +7 (the
+  // MFMA's own k order; one load instruction covers 64 contiguous bytes of 16 rows), and for
+  // every tile the adapter row l16 at the same k. k at or past kend reads as zero.
+  auto load = [&](int kb, u32x4 (&xa)[2][4], u32x4 (&oa)[NT][4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
+      const int k = kb + q * 32 + g * 8;
+      const bool kin = k < kend;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        if (c >= nct) break;
-        const bf16x8 bv = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(lop + (c * 16 + l16) * kP1Pitch + g * 32 + q * 8));
+      for (int a = 0; a < 2; ++a)
+        xa[a][q] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, kin ? (uint32_t)((a * 16 + l16) * kdim + k) * 2u : kOOB, 0, 0));
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        oa[t][q] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(ro[t], kin ? (uint32_t)(l16 * kdim + k) * 2u : kOOB, 0, 0));
+    }
+  };
+  auto mma = [&](const u32x4 (&xa)[2][4], const u32x4 (&oa)[NT][4]) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t >= nt) break;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
-          acc[a][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[a][q]),
-                                                              bv, acc[a][c], 0, 0, 0);
+          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[a][q]),
+                                                              __builtin_bit_cast(bf16x8, oa[t][q]), acc[a][t], 0, 0, 0);
       }
+  };
+  u32x4 xa0[2][4], oa0[NT][4], xa1[2][4], oa1[NT][4];
+  if (kbeg < kend) {
+    load(kbeg, xa0, oa0);
+    for (int kb = kbeg; kb < kend; kb += 2 * kLoraKBlock) {
+      load(kb + kLoraKBlock, xa1, oa1);  // past kend: zeros
+      mma(xa0, oa0);
+      load(kb + 2 * kLoraKBlock, xa0, oa0);
+      mma(xa1, oa1);
     }
   }
-  // D[i][j] of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16.
+  // waves 1-3 hand their sums to wave 0 through LDS (fixed order: wave 0 + 1 + 2 + 3)
+  __shared__ f32x4 red[3][2 * NT][64];
+  if (wave > 0) {
 #pragma unroll
-  for (int a = 0; a < 2; ++a) {
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      if (c >= nct) break;
-      const int col = c * 16 + l16;
-      const int row0 = row_base + a * 16 + g * 4;
+      for (int t = 0; t < NT; ++t) red[wave - 1][a * NT + t][lane] = acc[a][t];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[a][t] += red[w][a * NT + t][lane];
+  // D of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16.
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t >= nt) break;
+    bf16_t* outT = reinterpret_cast<bf16_t*>(ws + Jr.t[t].out_off);
+    const float s = Jr.t[t].scale;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int r = row0 + a * 16 + g * 4;
       uint2 pk;
-      pk.x = pack_bf16x2(J.scale * acc[a][c][0], J.scale * acc[a][c][1]);
-      pk.y = pack_bf16x2(J.scale * acc[a][c][2], J.scale * acc[a][c][3]);
-      *reinterpret_cast<uint2*>(outT + (int64_t)col * J.rows_pad + row0) = pk;
+      pk.x = pack_bf16x2(s * acc[a][t][0], s * acc[a][t][1]);
+      pk.y = pack_bf16x2(s * acc[a][t][2], s * acc[a][t][3]);
+      *reinterpret_cast<uint2*>(outT + (int64_t)l16 * Jr.rows_pad + r) = pk;
     }
   }
 }
@@ -124,172 +164,206 @@ __global__ __launch_bounds__(256) void lora_u_bf16_kernel(LoraBatch b, uint8_t* 
 // ------------------------------------------------------------------------------------------
 constexpr int kP2Pitch = kLoraTStep + 8;  // LDS row pitch (bf16) of the transposed tile
 
-__global__ __launch_bounds__(256) void lora_dadb_bf16_kernel(LoraBatch b, uint8_t* __restrict__ ws) {
-  const int ji = find_job(b, (int)blockIdx.x, &LoraJob::b2_begin);
-  const LoraJob J = b.j[ji];
-  int local = (int)blockIdx.x - J.b2_begin;
-  const int cba = (J.d_in + kLoraColTile - 1) / kLoraColTile;
-  const int cbb = (J.d_out + kLoraColTile - 1) / kLoraColTile;
-  const int sp = local / (cba + cbb);
-  local %= (cba + cbb);
-  const int kind = local < cba ? 0 : 1;  // 0: dA from (dU^T, x); 1: dB from (sU^T, dy)
-  const int cb = kind == 0 ? local : local - cba;
-  const int cols = kind == 0 ? J.d_in : J.d_out;
-  const bf16_t* src = static_cast<const bf16_t*>(kind == 0 ? J.x : J.dy);
-  const bf16_t* lt = reinterpret_cast<const bf16_t*>(ws + (kind == 0 ? J.dut_off : J.ut_off));
-  float* part = reinterpret_cast<float*>(ws + (kind == 0 ? J.pa_off : J.pb_off));
+__global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraP2Job& Jr = b.j[ji];
+  const int cols = Jr.cols, nt = Jr.nt;
+  const int ncb = (cols + kLoraColTile - 1) / kLoraColTile;
+  const int local = (int)blockIdx.x - Jr.b_begin;
+  const int sp = local / ncb, cb = local % ncb;
   const int col0 = cb * kLoraColTile;
-  const int tper = ((J.rows_pad / J.splits + kLoraTStep - 1) / kLoraTStep) * kLoraTStep;
+  const int tper = ((Jr.rows_pad / Jr.splits + kLoraTStep - 1) / kLoraTStep) * kLoraTStep;
   const int t_begin = sp * tper;
-  const int t_end = min(J.rows_pad, t_begin + tper);
+  const int t_end = min(Jr.rows_pad, t_begin + tper);
 
-  __shared__ __align__(16) bf16_t xs[kLoraColTile * kP2Pitch];
+  __shared__ __align__(16) bf16_t xs[2][kLoraColTile * kP2Pitch];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  const int nct = J.rp / 16;
-  const int ld_t = tid >> 3, ld_c = (tid & 7) * 8;  // staging: row t, 8 columns
-  f32x4 acc[4];
+  // staging: rows 2*pr, 2*pr+1 of the step, columns 8*cg .. 8*cg+7 of the tile
+  const int pr = tid >> 3, cg = tid & 7;
+  const bool cin = col0 + cg * 8 < cols;  // cols % 8 == 0: a column chunk is whole or absent
+  const bf16_t* src = static_cast<const bf16_t*>(Jr.src);
+  __amdgpu_buffer_rsrc_t rl[kLoraMaxTiles];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < kLoraMaxTiles; ++t)
+    rl[t] = buffer_rsrc(ws + (t < nt ? Jr.t[t].lt_off : 0), t < nt ? 16 * Jr.rows_pad * 2 : 0);
 
-  for (int t0 = t_begin; t0 < t_end; t0 += kLoraTStep) {
-    const int t = t0 + ld_t;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (t < J.rows && col0 + ld_c < cols)
-      v = *reinterpret_cast<const u32x4*>(src + (int64_t)t * cols + col0 + ld_c);
-    __syncthreads();
+  f32x4 acc[kLoraMaxTiles];
+#pragma unroll
+  for (int t = 0; t < kLoraMaxTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Rows of step t0 go through a descriptor based at row t0 (offsets stay small) whose range
+  // ends at the input's last row.
+  auto load = [&](int t0, u32x4 (&v)[2], u32x4 (&la)[2][kLoraMaxTiles]) {
+    const int nr = max(0, min(kLoraTStep, Jr.rows - t0));
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src + (int64_t)t0 * cols, nr * cols * 2);
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+      v[e] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, cin ? (uint32_t)((2 * pr + e) * cols + col0 + cg * 8) * 2u : kOOB, 0, 0));
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int t = 0; t < kLoraMaxTiles; ++t)
+        la[ks][t] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rl[t], (uint32_t)(l16 * Jr.rows_pad + t0 + ks * 32 + g * 8) * 2u, 0, 0));
+  };
+  u32x4 v0[2], v1[2], la0[2][kLoraMaxTiles], la1[2][kLoraMaxTiles];
+  // One step: store its rows transposed (row pairs as 32-bit words) into buffer `buf`, one
+  // barrier, two MFMA k-steps of 32 rows. Buffer `buf` was last read two steps earlier,
+  // before the previous step's barrier.
+  auto step = [&](int buf, const u32x4 (&v)[2], const u32x4 (&la)[2][kLoraMaxTiles]) {
+    uint32_t* dst = reinterpret_cast<uint32_t*>(xs[buf]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      xs[(ld_c + 2 * e) * kP2Pitch + ld_t] = (bf16_t)(v[e] & 0xFFFFu);
-      xs[(ld_c + 2 * e + 1) * kP2Pitch + ld_t] = (bf16_t)(v[e] >> 16);
+      const uint32_t lo0 = v[0][e] & 0xFFFFu, hi0 = v[0][e] >> 16;
+      const uint32_t lo1 = v[1][e] & 0xFFFFu, hi1 = v[1][e] >> 16;
+      dst[((cg * 8 + 2 * e) * kP2Pitch + 2 * pr) >> 1] = lo0 | (lo1 << 16);
+      dst[((cg * 8 + 2 * e + 1) * kP2Pitch + 2 * pr) >> 1] = hi0 | (hi1 << 16);
     }
     __syncthreads();
-    const bf16x8 bv = __builtin_bit_cast(
-        bf16x8, *reinterpret_cast<const u32x4*>(xs + (wave * 16 + l16) * kP2Pitch + g * 8));
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      if (c >= nct) break;
-      const bf16x8 av = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(lt + (int64_t)(c * 16 + l16) * J.rows_pad + t0 + g * 8));
-      acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[c], 0, 0, 0);
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 bv = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(xs[buf] + (wave * 16 + l16) * kP2Pitch + ks * 32 + g * 8));
+#pragma unroll
+      for (int t = 0; t < kLoraMaxTiles; ++t) {
+        if (t >= nt) break;
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, la[ks][t]), bv, acc[t], 0, 0, 0);
+      }
     }
+  };
+  if (t_begin < t_end) load(t_begin, v0, la0);
+  for (int t0 = t_begin; t0 < t_end; t0 += 2 * kLoraTStep) {
+    const bool two = t0 + kLoraTStep < t_end;
+    if (two) load(t0 + kLoraTStep, v1, la1);
+    step(0, v0, la0);
+    if (!two) break;
+    if (t0 + 2 * kLoraTStep < t_end) load(t0 + 2 * kLoraTStep, v0, la0);
+    step(1, v1, la1);
   }
   const int col = col0 + wave * 16 + l16;
   if (col < cols) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      if (c >= nct) break;
+    for (int t = 0; t < kLoraMaxTiles; ++t) {
+      if (t >= nt) break;
+      float* part = reinterpret_cast<float*>(ws + Jr.t[t].part_off) + (int64_t)sp * 16 * cols;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = c * 16 + g * 4 + v;
-        part[((int64_t)sp * J.rp + r) * cols + col] = acc[c][v];
-      }
+      for (int v = 0; v < 4; ++v) part[(int64_t)(g * 4 + v) * cols + col] = acc[t][v];
     }
   }
 }
 
 // ------------------------------------------------------------------------------------------
-// f32 passes (VALU)
+// f32 passes (VALU), same jobs and workspace layout
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void lora_u_f32_kernel(LoraBatch b, uint8_t* __restrict__ ws) {
-  const int ji = find_job(b, (int)blockIdx.x, &LoraJob::b1_begin);
-  const LoraJob J = b.j[ji];
-  const int local = (int)blockIdx.x - J.b1_begin;
-  const int tiles = J.rows_pad / kLoraRowTile;
-  const int kind = local / tiles, rt = local % tiles;
-  const float* src = static_cast<const float*>(kind == 0 ? J.x : J.dy);
-  const int kdim = kind == 0 ? J.d_in : J.d_out;
-  const float* Al = static_cast<const float*>(J.A);
-  const float* Bl = static_cast<const float*>(J.B);
-  float* outT = reinterpret_cast<float*>(ws + (kind == 0 ? J.ut_off : J.dut_off));
-  for (int idx = threadIdx.x; idx < kLoraRowTile * J.rp; idx += blockDim.x) {
-    const int rl = idx % kLoraRowTile, c = idx / kLoraRowTile;
-    const int row = rt * kLoraRowTile + rl;
+__global__ __launch_bounds__(256) void lora_p1_f32_kernel(LoraP1Batch b, uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraP1Job& J = b.j[ji];
+  const int rt = (int)blockIdx.x - J.b_begin;
+  const float* src = static_cast<const float*>(J.src);
+  for (int idx = threadIdx.x; idx < kLoraP1Rows * 16 * J.nt; idx += blockDim.x) {
+    const int rl = idx % kLoraP1Rows, c = idx / kLoraP1Rows;  // c: rank within the job
+    const int t = c >> 4, cr = c & 15;
+    const int row = rt * kLoraP1Rows + rl;
     float s = 0.0f;
-    if (row < J.rows && c < J.rank) {
-      const float* xr = src + (int64_t)row * kdim;
-      if (kind == 0)
-        for (int k = 0; k < kdim; ++k) s = fmaf(xr[k], Al[(int64_t)c * J.d_in + k], s);
-      else
-        for (int k = 0; k < kdim; ++k) s = fmaf(xr[k], Bl[(int64_t)k * J.rank + c], s);
+    if (row < J.rows && cr < J.t[t].valid) {
+      const float* xr = src + (int64_t)row * J.kdim;
+      const float* op = static_cast<const float*>(J.t[t].op) + (int64_t)cr * J.kdim;
+      for (int k = 0; k < J.kdim; ++k) s = fmaf(xr[k], op[k], s);
     }
-    outT[(int64_t)c * J.rows_pad + row] = J.scale * s;
+    reinterpret_cast<float*>(ws + J.t[t].out_off)[(int64_t)cr * J.rows_pad + row] = J.t[t].scale * s;
   }
 }
 
-__global__ __launch_bounds__(256) void lora_dadb_f32_kernel(LoraBatch b, uint8_t* __restrict__ ws) {
-  const int ji = find_job(b, (int)blockIdx.x, &LoraJob::b2_begin);
-  const LoraJob J = b.j[ji];
-  int local = (int)blockIdx.x - J.b2_begin;
-  const int cba = (J.d_in + kLoraColTile - 1) / kLoraColTile;
-  const int cbb = (J.d_out + kLoraColTile - 1) / kLoraColTile;
-  const int sp = local / (cba + cbb);
-  local %= (cba + cbb);
-  const int kind = local < cba ? 0 : 1;
-  const int cb = kind == 0 ? local : local - cba;
-  const int cols = kind == 0 ? J.d_in : J.d_out;
-  const float* src = static_cast<const float*>(kind == 0 ? J.x : J.dy);
-  const float* lt = reinterpret_cast<const float*>(ws + (kind == 0 ? J.dut_off : J.ut_off));
-  float* part = reinterpret_cast<float*>(ws + (kind == 0 ? J.pa_off : J.pb_off));
+__global__ __launch_bounds__(256) void lora_p2_f32_kernel(LoraP2Batch b, uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraP2Job& J = b.j[ji];
+  const int ncb = (J.cols + kLoraColTile - 1) / kLoraColTile;
+  const int local = (int)blockIdx.x - J.b_begin;
+  const int sp = local / ncb, cb = local % ncb;
   const int tper = ((J.rows_pad / J.splits + kLoraTStep - 1) / kLoraTStep) * kLoraTStep;
   const int t_begin = sp * tper;
   const int t_end = min(J.rows, t_begin + tper);
   const int col = cb * kLoraColTile + (threadIdx.x & 63);
-  for (int c = threadIdx.x >> 6; c < J.rp; c += 4) {
+  const float* src = static_cast<const float*>(J.src);
+  for (int c = threadIdx.x >> 6; c < 16 * J.nt; c += 4) {
+    const int t = c >> 4, cr = c & 15;
+    const float* lt = reinterpret_cast<const float*>(ws + J.t[t].lt_off) + (int64_t)cr * J.rows_pad;
     float s = 0.0f;
-    if (col < cols)
-      for (int t = t_begin; t < t_end; ++t)
-        s = fmaf(lt[(int64_t)c * J.rows_pad + t], src[(int64_t)t * cols + col], s);
-    if (col < cols) part[((int64_t)sp * J.rp + c) * cols + col] = s;
+    if (col < J.cols)
+      for (int r = t_begin; r < t_end; ++r) s = fmaf(lt[r], src[(int64_t)r * J.cols + col], s);
+    if (col < J.cols)
+      reinterpret_cast<float*>(ws + J.t[t].part_off)[((int64_t)sp * 16 + cr) * J.cols + col] = s;
   }
 }
 
 // ------------------------------------------------------------------------------------------
-// Ordered reduction of the split partials into dA, dB (+=).
+// Ordered reduction of the split partials into dA, dB (+=). Partials of rank c of a problem
+// live in its tile c/16: [tile][split][16][cols].
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void lora_reduce_kernel(LoraBatch b, const uint8_t* __restrict__ ws) {
-  const int ji = find_job(b, (int)blockIdx.x, &LoraJob::b3_begin);
-  const LoraJob J = b.j[ji];
-  const int64_t idx = (int64_t)((int)blockIdx.x - J.b3_begin) * blockDim.x + threadIdx.x;
+__global__ __launch_bounds__(256) void lora_reduce_kernel(LoraRedBatch b, const uint8_t* __restrict__ ws) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraRedJob J = b.j[ji];
+  const int64_t idx = (int64_t)((int)blockIdx.x - J.b_begin) * blockDim.x + threadIdx.x;
   const int64_t na = (int64_t)J.rank * J.d_in, nb = (int64_t)J.d_out * J.rank;
   if (idx < na) {
     const int c = (int)(idx / J.d_in), k = (int)(idx % J.d_in);
-    const float* p = reinterpret_cast<const float*>(ws + J.pa_off);
+    const float* p = reinterpret_cast<const float*>(ws + J.pa_off) +
+                     ((int64_t)(c >> 4) * J.sa * 16 + (c & 15)) * J.d_in + k;
     float s = 0.0f;
-    for (int sp = 0; sp < J.splits; ++sp) s += p[((int64_t)sp * J.rp + c) * J.d_in + k];
+    for (int sp = 0; sp < J.sa; ++sp) s += p[(int64_t)sp * 16 * J.d_in];
     J.dA[idx] += s;
   } else if (idx < na + nb) {
     const int64_t i2 = idx - na;
     const int o = (int)(i2 / J.rank), c = (int)(i2 % J.rank);
-    const float* p = reinterpret_cast<const float*>(ws + J.pb_off);
+    const float* p = reinterpret_cast<const float*>(ws + J.pb_off) +
+                     ((int64_t)(c >> 4) * J.sb * 16 + (c & 15)) * J.d_out + o;
     float s = 0.0f;
-    for (int sp = 0; sp < J.splits; ++sp) s += p[((int64_t)sp * J.rp + c) * J.d_out + o];
+    for (int sp = 0; sp < J.sb; ++sp) s += p[(int64_t)sp * 16 * J.d_out];
     J.dB[i2] += s;
   }
 }
 
 // ------------------------------------------------------------------------------------------
-hipError_t launch_lora_pass1(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
+hipError_t launch_lora_bt(int dtype, const LoraBTBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   KernelTimer t(K_LORA_U, s);
   if (dtype == 1)
-    hipLaunchKernelGGL(lora_u_bf16_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+    hipLaunchKernelGGL(lora_bt_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, b, ws);
   else
-    hipLaunchKernelGGL(lora_u_f32_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+    hipLaunchKernelGGL(lora_bt_kernel<float>, dim3(blocks), dim3(256), 0, s, b, ws);
   return hipGetLastError();
 }
 
-hipError_t launch_lora_pass2(int dtype, const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
+hipError_t launch_lora_pass1(int dtype, int nt, const LoraP1Batch& b, int blocks, uint8_t* ws,
+                             hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
+  KernelTimer t(K_LORA_U, s);
+  if (dtype != 1) {
+    hipLaunchKernelGGL(lora_p1_f32_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+  } else {
+    switch (nt) {
+      case 1: hipLaunchKernelGGL(lora_p1_bf16_kernel<1>, dim3(blocks), dim3(256), 0, s, b, ws); break;
+      case 2: hipLaunchKernelGGL(lora_p1_bf16_kernel<2>, dim3(blocks), dim3(256), 0, s, b, ws); break;
+      case 3: hipLaunchKernelGGL(lora_p1_bf16_kernel<3>, dim3(blocks), dim3(256), 0, s, b, ws); break;
+      default: hipLaunchKernelGGL(lora_p1_bf16_kernel<4>, dim3(blocks), dim3(256), 0, s, b, ws); break;
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_pass2(int dtype, const LoraP2Batch& b, int blocks, uint8_t* ws, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   KernelTimer t(K_LORA_DADB, s);
   if (dtype == 1)
-    hipLaunchKernelGGL(lora_dadb_bf16_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+    hipLaunchKernelGGL(lora_p2_bf16_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
   else
-    hipLaunchKernelGGL(lora_dadb_f32_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+    hipLaunchKernelGGL(lora_p2_f32_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
   return hipGetLastError();
 }
 
-hipError_t launch_lora_reduce(const LoraBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
+hipError_t launch_lora_reduce(const LoraRedBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   KernelTimer t(K_LORA_REDUCE, s);
   hipLaunchKernelGGL(lora_reduce_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
