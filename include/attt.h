@@ -143,8 +143,11 @@ attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* lm_head, co
  *   B      device [d_out, rank] of dtype
  *   dA     device float [rank, d_in]   (+=)
  *   dB     device float [d_out, rank]  (+=)
- *   rows >= 0, d_in and d_out >= 1 and multiples of 8, 1 <= rank <= ATTT_LORA_MAX_RANK
- *   Outputs of different problems must not overlap.
+ *   rows >= 0, d_in and d_out >= 1 and multiples of 8, 1 <= rank <= ATTT_LORA_MAX_RANK;
+ *   rows < 2^30 and d_in, d_out < 2^20 (ATTT_EUNSUPPORTED beyond)
+ *   Outputs of different problems must not overlap. Problems with the same x pointer, d_in
+ *   and rows (the q, k and v projections of one layer) are computed together, x being read
+ *   once per pass for up to 64 of their combined (16-padded) ranks.
  * ------------------------------------------------------------------------------------ */
 typedef struct attt_lora_problem {
   const void* x;

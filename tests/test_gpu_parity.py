@@ -234,11 +234,14 @@ def test_ce_deterministic(attt):
 # LoRA gradients
 # ------------------------------------------------------------------------------------------
 def _lora_case(attt, problems, bf16, zero_dA=False):
+    """Problems whose x is the same host array share one device copy (as q, k, v do)."""
     import torch
-    dev = []
+    dev, xs = [], {}
     for p in problems:
         r, d_in, d_out = p["A"].shape[0], p["A"].shape[1], p["B"].shape[0]
-        dev.append(dict(x=dev_dense(p["x"]), dy=dev_dense(p["dy"]), A=dev_dense(p["A"]),
+        if id(p["x"]) not in xs:
+            xs[id(p["x"])] = dev_dense(p["x"])
+        dev.append(dict(x=xs[id(p["x"])], dy=dev_dense(p["dy"]), A=dev_dense(p["A"]),
                         B=dev_dense(p["B"]), scale=p["scale"],
                         dA=torch.zeros(r, d_in, dtype=torch.float32, device="cuda"),
                         dB=torch.zeros(d_out, r, dtype=torch.float32, device="cuda")))
@@ -280,6 +283,27 @@ def test_lora_ranks_and_ragged_rows(attt, bf16, rank):
                           A=random_dense((rank, d_in), 0.05, bf16, s + 2),
                           B=random_dense((d_out, rank), 0.05, bf16, s + 3), scale=16.0 / rank))
     _lora_case(attt, probs, bf16)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_lora_shared_x_grouping(attt, bf16):
+    """Projections reading one x are processed together, at most four rank tiles of 16 per
+    group: ranks 8, 16, 32, 24 on one x need two groups; a projection on another x of the same
+    shape, and one with no rows, stay apart."""
+    rows, d_in = 777, 264
+    x = random_dense((rows, d_in), 1.0, bf16, 61)
+    x2 = random_dense((rows, d_in), 1.0, bf16, 62)
+    probs = []
+    for i, (r, d_out, xx) in enumerate([(8, 264, x), (16, 64, x), (32, 136, x), (24, 264, x), (16, 64, x2)]):
+        probs.append(dict(x=xx, dy=random_dense((rows, d_out), 0.1, bf16, 70 + i),
+                          A=random_dense((r, d_in), 0.05, bf16, 80 + i),
+                          B=random_dense((d_out, r), 0.05, bf16, 90 + i), scale=16.0 / r))
+    probs.append(dict(x=random_dense((0, d_in), 1.0, bf16, 63), dy=random_dense((0, 64), 0.1, bf16, 64),
+                      A=random_dense((8, d_in), 0.05, bf16, 65), B=random_dense((64, 8), 0.05, bf16, 66),
+                      scale=2.0))
+    note(f"lora shared x bf16={bf16}")
+    dev = _lora_case(attt, probs, bf16)
+    assert np.all(host(dev[-1]["dA"]) == 0.0) and np.all(host(dev[-1]["dB"]) == 0.0)
 
 
 def test_lora_accumulates(attt):
