@@ -188,7 +188,13 @@ __device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, i
 // phase) while the other runs its 32 MFMAs (compute phase).
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <class C>
+// With PF, group 1 (which issues no tile loads) touches every row's cache line of stage k+2 in
+// its memory phase of iteration k: one 4-byte load per row into a 256-byte LDS scratch area
+// past the two stages, which nothing reads. Group 0's loads of that stage then mostly hit L2.
+// It pays off where each tile's panels are long (the dH GEMM, K = one vocab chunk).
+constexpr size_t kPfScratch = 256;
+
+template <class C, bool PF>
 __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                                  const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                                  int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
@@ -292,7 +298,17 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     wg_barrier();
   } else {
     wg_barrier();
+    bf16_t* scratch = lds + 2 * (C::SA + C::SB);
+    const int prow = (wave & 3) * 64 + lane;
+    const uint32_t pa = (uint32_t)((int64_t)prow * lda * 2), pb = (uint32_t)((int64_t)prow * ldb * 2);
     for (int k = 0; k < nk; ++k) {
+      if (PF && k + 2 < nk) {
+        const int k0 = (k + 2) * 64;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (__attribute__((address_space(3))) void*)scratch, 4,
+                                                 prow < mval ? pa + (uint32_t)k0 * 2 : kOOB, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (__attribute__((address_space(3))) void*)scratch, 4,
+                                                 prow < nval ? pb + (uint32_t)k0 * 2 : kOOB, 0, 0, 0);
+      }
       mem(k);
       wg_barrier();
       pin();
@@ -300,15 +316,16 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
       pin();
       wg_barrier();
     }
+    if (PF) __builtin_amdgcn_s_waitcnt(0);  // scratch writes land before the LDS is released
   }
 }
 
-template <class C>
+template <class C, bool PF = false>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                               const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                               int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
   if constexpr (C::NT == 512)
-    mfma_mainloop_pp<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
+    mfma_mainloop_pp<C, PF>(A, lda, mval, B, ldb, nval, K, lds, acc);
   else
     mfma_mainloop_db<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
 }
@@ -495,8 +512,8 @@ __device__ __forceinline__ void ce_dh_bf16_body(
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * C::BM, n0 = tn * C::BN;  // m0: first column of dH, n0: first row of the block
   f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
-                   reinterpret_cast<bf16_t*>(smem), acc);
+  mfma_mainloop<C, true>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
+                         reinterpret_cast<bf16_t*>(smem), acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   // The float32 partial sums between chunks keep the accumulators' register layout: per tile,
@@ -1200,13 +1217,14 @@ static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, i
     attr = true;
   }
   const int tm = (d + C::BM - 1) / C::BM, tn = (R + C::BN - 1) / C::BN;  // transposed tiles
+  const size_t lds = C::LDS + (C::NT == 512 ? kPfScratch : 0);
   KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
   if (gate)
-    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp,
+    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), lds, s, dz, ldz, WT, Vp,
                        r0, R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
                        rs.labels, W, V, gate);
   else
-    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
+    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), lds, s, dz, ldz, WT, Vp, r0,
                        R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
                        rs.labels, W, V);
   return hipGetLastError();
