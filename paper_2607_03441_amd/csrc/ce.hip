@@ -74,7 +74,8 @@ struct Cfg {
   static constexpr int RPL = NT / 8;  // rows one load round covers (8 x 16-byte chunks per row)
   static constexpr int AL = BM / RPL, BL = BN / RPL;
   static constexpr int SA = BM * BK, SB = BN * BK;
-  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);
+  // two stages; the 8-wave ping-pong adds a 256-byte scratch area for its L2 prefetch
+  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t) + (NT == 512 ? 256 : 0);
 };
 using CfgBig = Cfg<256, 256, 2, 4>;    // 8 waves, 128x64 per wave
 using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
@@ -188,12 +189,12 @@ __device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, i
 // phase) while the other runs its 32 MFMAs (compute phase).
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// With PF, group 1 (which issues no tile loads) touches every row's cache line of stage k+2 in
-// its memory phase of iteration k: one 4-byte load per row into a 256-byte LDS scratch area
+// With PF, group 1 (which issues no tile loads) touches every A row's cache line of stage k+2
+// in its memory phase of iteration k: one 4-byte load per row into a 256-byte LDS scratch area
 // past the two stages, which nothing reads. Group 0's loads of that stage then mostly hit L2.
-// It pays off where each tile's panels are long (the dH GEMM, K = one vocab chunk).
-constexpr size_t kPfScratch = 256;
-
+// Only A: its lines are shared by half as many of an XCD's workgroups as B's (4 against 8), so
+// more of them miss; prefetching B as well measured slower. It pays in the dH GEMM, whose
+// panels span a whole vocab chunk; in the first GEMM it measured neutral to slower.
 template <class C, bool PF>
 __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                                  const bf16_t* __restrict__ B, int64_t ldb, int nval,
@@ -300,15 +301,11 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     wg_barrier();
     bf16_t* scratch = lds + 2 * (C::SA + C::SB);
     const int prow = (wave & 3) * 64 + lane;
-    const uint32_t pa = (uint32_t)((int64_t)prow * lda * 2), pb = (uint32_t)((int64_t)prow * ldb * 2);
+    const uint32_t pa = (uint32_t)((int64_t)prow * lda * 2);
     for (int k = 0; k < nk; ++k) {
-      if (PF && k + 2 < nk) {
-        const int k0 = (k + 2) * 64;
+      if (PF && k + 2 < nk)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (__attribute__((address_space(3))) void*)scratch, 4,
-                                                 prow < mval ? pa + (uint32_t)k0 * 2 : kOOB, 0, 0, 0);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (__attribute__((address_space(3))) void*)scratch, 4,
-                                                 prow < nval ? pb + (uint32_t)k0 * 2 : kOOB, 0, 0, 0);
-      }
+                                                 prow < mval ? pa + (uint32_t)(k + 2) * 128 : kOOB, 0, 0, 0);
       mem(k);
       wg_barrier();
       pin();
@@ -1217,14 +1214,13 @@ static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, i
     attr = true;
   }
   const int tm = (d + C::BM - 1) / C::BM, tn = (R + C::BN - 1) / C::BN;  // transposed tiles
-  const size_t lds = C::LDS + (C::NT == 512 ? kPfScratch : 0);
   KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
   if (gate)
-    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), lds, s, dz, ldz, WT, Vp,
+    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp,
                        r0, R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
                        rs.labels, W, V, gate);
   else
-    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), lds, s, dz, ldz, WT, Vp, r0,
+    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
                        R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
                        rs.labels, W, V);
   return hipGetLastError();
