@@ -74,8 +74,7 @@ struct Cfg {
   static constexpr int RPL = NT / 8;  // rows one load round covers (8 x 16-byte chunks per row)
   static constexpr int AL = BM / RPL, BL = BN / RPL;
   static constexpr int SA = BM * BK, SB = BN * BK;
-  // two stages; the 8-wave ping-pong adds a 256-byte scratch area for its L2 prefetch
-  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t) + (NT == 512 ? 256 : 0);
+  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);  // two stages
 };
 using CfgBig = Cfg<256, 256, 2, 4>;    // 8 waves, 128x64 per wave
 using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
@@ -189,13 +188,18 @@ __device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, i
 // phase) while the other runs its 32 MFMAs (compute phase).
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// With PF, group 1 (which issues no tile loads) touches every A row's cache line of stage k+2
-// in its memory phase of iteration k: one 4-byte load per row into a 256-byte LDS scratch area
-// past the two stages, which nothing reads. Group 0's loads of that stage then mostly hit L2.
-// Only A: its lines are shared by half as many of an XCD's workgroups as B's (4 against 8), so
-// more of them miss; prefetching B as well measured slower. It pays in the dH GEMM, whose
-// panels span a whole vocab chunk; in the first GEMM it measured neutral to slower.
-template <class C, bool PF>
+// Tile loads are issued only in memory phases: a wave stalls at a load instruction until the
+// load path accepts it (about 1 KiB per 25 cycles per CU here), and a stall in a compute phase
+// idles the SIMD's matrix core. A stage is 64 instructions of 1 KiB; both groups share them:
+//  * group 0 issues blocks [0, kG0) of stage k+1 at the start of its memory phase of stage k
+//    (slot (k+1)&1 was last read by group 1 in the phase before) and waits for them at the end
+//    of its compute phase of stage k;
+//  * group 1 issues blocks [kG0, 16) of stage k+2 at the end of its memory phase of stage k,
+//    after its own fragment reads of slot k&1 have completed (group 0 finished reading that
+//    slot before the barrier that opened the phase), and waits for them one memory phase later.
+// Group 1's share thus has three phases to land instead of one, and neither group's memory
+// phase carries a whole stage of load issue.
+template <class C>
 __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                                  const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                                  int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
@@ -211,24 +215,24 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // Only group 0 (waves 0-3) loads tiles: each of its waves fills 16 of the stage's 64 blocks,
-  // in its memory phase, so no load instruction ever sits in front of an MFMA of the wave that
-  // is computing on the same SIMD.
+  // A stage's 64 blocks of 8 rows x 128 bytes: block (wave & 3) + 4 j for j in [0, 16). Blocks
+  // j < 8 are A rows, the rest B rows; both groups use the same numbering.
   const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
-  constexpr int LW = 4;                               // loading waves
+  constexpr int LW = 4;                               // waves per group
   constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
-  constexpr int BPW = (ABLK + BBLK) / LW;             // blocks per loading wave per stage
-  static_assert(ABLK % LW == 0 && BBLK % LW == 0, "stage blocks must split evenly");
+  constexpr int BPW = (ABLK + BBLK) / LW;             // blocks per wave of a group per stage
+  constexpr int kG0 = 6;                              // group 0's share per wave
+  static_assert(ABLK % LW == 0 && BBLK % LW == 0 && kG0 < BPW, "stage blocks must split evenly");
   // Offsets are formed per load: the block's first row is wave-uniform, and the swizzled chunk
   // of a lane depends only on the lane and on the parity of the block (rows 8b .. 8b+7).
   const int lr = lane >> 3;
   const int c_even = (lane & 7) ^ ((lr >> 1) & 7);
   const int c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
   const uint32_t la = (uint32_t)(lr * lda * 2), lb = (uint32_t)(lr * ldb * 2);
-  auto dma = [&](int st, int k0) {
+  auto dma = [&](int st, int k0, int j0, int j1) {
     bf16_t* base = lds + st * (C::SA + C::SB);
 #pragma unroll
-    for (int j = 0; j < BPW; ++j) {
+    for (int j = j0; j < j1; ++j) {
       const int blk = (wave & 3) + j * LW;
       const bool isA = blk < ABLK;
       const int rb = (isA ? blk : blk - ABLK) * 8;
@@ -276,19 +280,22 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[1][0]), "+v"(acc[1][1]),
                  "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[3][0]), "+v"(acc[3][1]));
   };
-  // Group 0, iteration k:  DMA(stage k+1); fragments(k) | MFMA(k); wait for the DMA |
-  // group 1, one phase later: fragments(k) | MFMA(k) |
-  // Stage k+1 goes into the slot of stage k-1, which group 1 finished reading in the phase just
-  // before; group 0 reads it two phases later. Group 1 takes one extra barrier before its loop,
-  // group 0 one after it, so every wave executes 2 nk + 2 barriers.
+  // Group 0, iteration k:  loads [0, kG0) of stage k+1; fragments(k); wait for own reads |
+  //                        MFMA(k); wait for own loads |
+  // group 1, one phase later: fragments(k); wait for own reads and loads; loads [kG0, 16) of
+  //                        stage k+2 | MFMA(k) |
+  // Group 1 takes one extra barrier before its loop, group 0 one after it, so every wave
+  // executes 2 nk + 2 barriers. Group 1's share of stage 1 is issued before the loop.
   const int nk = (K + 63) / 64;
-  if (grp == 0) dma(0, 0);
+  if (grp == 0) dma(0, 0, 0, BPW);
   __builtin_amdgcn_s_waitcnt(0);
+  if (grp == 1 && nk > 1) dma(1, 64, kG0, BPW);
   wg_barrier();
   if (grp == 0) {
     for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) dma((k + 1) & 1, (k + 1) * 64);
+      if (k + 1 < nk) dma((k + 1) & 1, (k + 1) * 64, 0, kG0);
       mem(k);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
       pin();
       compute();
@@ -299,30 +306,25 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     wg_barrier();
   } else {
     wg_barrier();
-    bf16_t* scratch = lds + 2 * (C::SA + C::SB);
-    const int prow = (wave & 3) * 64 + lane;
-    const uint32_t pa = (uint32_t)((int64_t)prow * lda * 2);
     for (int k = 0; k < nk; ++k) {
-      if (PF && k + 2 < nk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (__attribute__((address_space(3))) void*)scratch, 4,
-                                                 prow < mval ? pa + (uint32_t)(k + 2) * 128 : kOOB, 0, 0, 0);
       mem(k);
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      if (k + 2 < nk) dma(k & 1, (k + 2) * 64, kG0, BPW);
       wg_barrier();
       pin();
       compute();
       pin();
       wg_barrier();
     }
-    if (PF) __builtin_amdgcn_s_waitcnt(0);  // scratch writes land before the LDS is released
   }
 }
 
-template <class C, bool PF = false>
+template <class C>
 __device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                               const bf16_t* __restrict__ B, int64_t ldb, int nval,
                                               int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
   if constexpr (C::NT == 512)
-    mfma_mainloop_pp<C, PF>(A, lda, mval, B, ldb, nval, K, lds, acc);
+    mfma_mainloop_pp<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
   else
     mfma_mainloop_db<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
 }
@@ -509,7 +511,7 @@ __device__ __forceinline__ void ce_dh_bf16_body(
   tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * C::BM, n0 = tn * C::BN;  // m0: first column of dH, n0: first row of the block
   f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C, true>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
+  mfma_mainloop<C>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
                          reinterpret_cast<bf16_t*>(smem), acc);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / C::WGN, wn = wave % C::WGN;
