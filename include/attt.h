@@ -9,6 +9,8 @@
  * LoRA adapter. This library computes the data-parallel part of that step on one GPU:
  *
  *   attt_ngram_weights        exposure f and weights w of every update token (Eq. 8-9)
+ *   attt_ngram_set_*          the same weights from persistent per-episode n-gram counts that
+ *                             grow with every update (the history update of Algorithm 1)
  *   attt_weighted_ce_fwd_bwd  weighted CE through the frozen LM head, loss and dL/dh (Eq. 10)
  *   attt_lora_grad            LoRA dA / dB of the adapted projections (Sec. 3.1, Appendix C)
  *
@@ -90,6 +92,45 @@ attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_of
                                int32_t num_episodes, int32_t n, float w_min,
                                uint32_t* exposure, float* weights,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * Persistent n-gram sets: the history update of Algorithm 1 (H^tok_{k+1} = H^tok_k followed by
+ * x_k) kept as device-resident n-gram counts, so that the weights of the next update (Eq. 8-9)
+ * cost O(|x_k|) lookups instead of a pass over the whole history.
+ *
+ * A set holds count(g, H) for every n-gram g of one episode's history H. Appending x adds the
+ * n-grams whose last token lies in x, including the n-1 that start in the last n-1 tokens of
+ * H (n-grams straddling two updates count, as in attt_ngram_weights; overlapping occurrences
+ * all count). attt_ngram_set_weights then gives, for an update x and the set's history H,
+ * exactly the f and w that attt_ngram_weights gives for x and the flat history H. Algorithm 1
+ * per update: attt_ngram_set_weights(x_k), the gradient step, attt_ngram_set_append(x_k).
+ *
+ * A set is a caller-owned device buffer of attt_ngram_set_size(capacity, n) bytes, 256-byte
+ * aligned, valid after attt_ngram_set_init (an empty history). capacity is the number of
+ * distinct n-grams it can hold (at most the number of tokens ever appended is always enough);
+ * the table is sized to stay at most half full. Every call on a set must pass the capacity
+ * and n it was initialised with.
+ *
+ * sets           HOST array of num_sets device pointers, one set per episode (distinct buffers)
+ * tokens         device int32 [token_offsets[num_sets]]: one text per set, back to back
+ * token_offsets  HOST int64 [num_sets+1], starting at 0, non-decreasing
+ * capacity       1 .. 2^30;  n: 1 <= n <= ATTT_NGRAM_MAX_N;  w_min as for attt_ngram_weights
+ * set_bytes      size of every set buffer (init only; ATTT_ENOSPACE if below the size query)
+ * exposure       device uint32 [T] or NULL;  weights: device float [T]
+ * Errors the host cannot see without a synchronisation are reported in the outputs: a set that
+ * received more distinct n-grams than its capacity, whose 64-bit n-gram keys collided (two
+ * different n-grams, never observed), or that is used with another n or capacity than it was
+ * initialised for, gives exposure 0xFFFFFFFF and weight NaN for every token queried against
+ * it, until it is initialised again. Calls on one set must be ordered (one stream).
+ * ------------------------------------------------------------------------------------ */
+attt_status attt_ngram_set_size(int64_t capacity, int32_t n, size_t* bytes);
+attt_status attt_ngram_set_init(void* const* sets, int32_t num_sets, int64_t capacity, int32_t n,
+                                size_t set_bytes, void* stream);
+attt_status attt_ngram_set_append(void* const* sets, const int32_t* tokens, const int64_t* token_offsets,
+                                  int32_t num_sets, int64_t capacity, int32_t n, void* stream);
+attt_status attt_ngram_set_weights(void* const* sets, const int32_t* tokens, const int64_t* token_offsets,
+                                   int32_t num_sets, int64_t capacity, int32_t n, float w_min,
+                                   uint32_t* exposure, float* weights, void* stream);
 
 /* --------------------------------------------------------------------------------------
  * Token-weighted next-token cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10;

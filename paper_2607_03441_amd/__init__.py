@@ -12,6 +12,7 @@ import os
 import numpy as np
 
 __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_workspace_size",
+           "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
            "weighted_ce_fwd_bwd", "ce_workspace_size", "lora_grad", "lora_workspace_size",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
            "F32", "BF16", "LoraProblem"]
@@ -63,6 +64,15 @@ def load():
     L.attt_ngram_workspace_size.argtypes = [p64, p64, i32, i32, psz]
     L.attt_ngram_weights.restype = i32
     L.attt_ngram_weights.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp, sz, vp]
+    vpp = ctypes.POINTER(ctypes.c_void_p)
+    L.attt_ngram_set_size.restype = i32
+    L.attt_ngram_set_size.argtypes = [i64, i32, psz]
+    L.attt_ngram_set_init.restype = i32
+    L.attt_ngram_set_init.argtypes = [vpp, i32, i64, i32, sz, vp]
+    L.attt_ngram_set_append.restype = i32
+    L.attt_ngram_set_append.argtypes = [vpp, vp, p64, i32, i64, i32, vp]
+    L.attt_ngram_set_weights.restype = i32
+    L.attt_ngram_set_weights.argtypes = [vpp, vp, p64, i32, i64, i32, f32, vp, vp, vp]
     L.attt_ce_workspace_size.restype = i32
     L.attt_ce_workspace_size.argtypes = [i64, i64, i64, i32, i32, psz]
     L.attt_weighted_ce_fwd_bwd.restype = i32
@@ -166,6 +176,65 @@ def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.
     ws = _workspace(need.value, dev, workspace)
     _check(L.attt_ngram_weights(_dptr(history), hp, _dptr(tokens), tp, E, n, float(w_min), _dptr(f),
                                 _dptr(w), _dptr(ws), ws.numel(), _stream_ptr()))
+    return f, w
+
+
+# ------------------------------------------------------------------------------------------
+def ngram_set_size(capacity, n):
+    """Bytes of one persistent n-gram set holding up to `capacity` distinct n-grams."""
+    L = load()
+    out = ctypes.c_size_t(0)
+    _check(L.attt_ngram_set_size(int(capacity), int(n), ctypes.byref(out)))
+    return out.value
+
+
+def _set_ptrs(sets):
+    arr = (ctypes.c_void_p * len(sets))()
+    for i, t in enumerate(sets):
+        _dev(t, "set")
+        arr[i] = t.data_ptr()
+    return arr
+
+
+def ngram_set_init(sets, capacity, n):
+    """Empty history for every set (uint8 device tensors of at least ngram_set_size bytes)."""
+    L = load()
+    nbytes = min(t.numel() * t.element_size() for t in sets)
+    _check(L.attt_ngram_set_init(_set_ptrs(sets), len(sets), int(capacity), int(n), nbytes, _stream_ptr()))
+
+
+def ngram_set_append(sets, tokens, token_offsets, capacity, n):
+    """Append text e (tokens[token_offsets[e]:token_offsets[e+1]]) to the history of set e."""
+    torch = _torch()
+    L = load()
+    _dev(tokens, "tokens")
+    if tokens.dtype != torch.int32:
+        raise TypeError("tokens must be int32")
+    to, tp = _offsets(token_offsets)
+    if len(to) - 1 != len(sets):
+        raise ValueError("one text per set")
+    _check(L.attt_ngram_set_append(_set_ptrs(sets), _dptr(tokens), tp, len(sets), int(capacity), int(n),
+                                   _stream_ptr()))
+
+
+def ngram_set_weights(sets, tokens, token_offsets, capacity, n, w_min=0.05, want_exposure=True, out=None):
+    """Eq. 8-9 of text e against the history held by set e. Returns (f, w) like ngram_weights."""
+    torch = _torch()
+    L = load()
+    _dev(tokens, "tokens")
+    if tokens.dtype != torch.int32:
+        raise TypeError("tokens must be int32")
+    to, tp = _offsets(token_offsets)
+    if len(to) - 1 != len(sets):
+        raise ValueError("one text per set")
+    T = int(to[-1])
+    if out is not None:
+        f, w = out
+    else:
+        f = torch.empty(T, dtype=torch.int32, device=tokens.device) if want_exposure else None
+        w = torch.empty(T, dtype=torch.float32, device=tokens.device)
+    _check(L.attt_ngram_set_weights(_set_ptrs(sets), _dptr(tokens), tp, len(sets), int(capacity), int(n),
+                                    float(w_min), _dptr(f), _dptr(w), _stream_ptr()))
     return f, w
 
 

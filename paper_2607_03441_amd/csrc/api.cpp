@@ -48,7 +48,7 @@ namespace attt {
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_logit_exp", "ce_overflow_guard", "lora_u_du", "lora_dadb",
-    "lora_reduce"};
+    "lora_reduce", "ngram_set", "ngram_set_weight"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -311,6 +311,122 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
     HIP_TRY(launch_ngram_weight(wb, wblocks, n, w_min, partial, exposure, weights, s), "ngram_weight");
   }
   return ATTT_OK;
+}
+
+// ------------------------------------------------------------------------------------------
+// Persistent n-gram sets
+// ------------------------------------------------------------------------------------------
+namespace {
+constexpr int64_t kSetMaxCapacity = (int64_t)1 << 30;
+
+// Table slots: a power of two at least twice the capacity (load factor at most 1/2).
+int64_t set_slots(int64_t capacity) {
+  int64_t S = 64;
+  while (S < 2 * capacity) S *= 2;
+  return S;
+}
+
+attt_status set_validate(void* const* sets, int32_t num_sets, int64_t capacity, int32_t n) {
+  if (num_sets < 1) return fail(ATTT_EINVAL, "ngram_set: num_sets must be >= 1 (got %d)", num_sets);
+  if (n < 1 || n > ATTT_NGRAM_MAX_N)
+    return fail(ATTT_EINVAL, "ngram_set: n must be in [1, %d] (got %d)", ATTT_NGRAM_MAX_N, n);
+  if (capacity < 1 || capacity > kSetMaxCapacity)
+    return fail(ATTT_EINVAL, "ngram_set: capacity must be in [1, 2^30] (got %lld)", (long long)capacity);
+  if (!sets) return fail(ATTT_EINVAL, "ngram_set: sets is null");
+  for (int32_t e = 0; e < num_sets; ++e) {
+    if (!sets[e]) return fail(ATTT_EINVAL, "ngram_set: set %d is null", e);
+    if (!aligned256(sets[e])) return fail(ATTT_EINVAL, "ngram_set: set %d must be 256-byte aligned", e);
+  }
+  return ATTT_OK;
+}
+
+// Episode batches of the append and weights calls: ceil(L/256) blocks per set.
+template <class Fn>
+attt_status set_batches(void* const* sets, const int64_t* toff, int32_t E, Fn&& fn) {
+  for (int32_t e0 = 0; e0 < E; e0 += kEpBatch) {
+    NgramSetBatch b{};
+    b.count = std::min<int32_t>(kEpBatch, E - e0);
+    int blocks = 0;
+    for (int i = 0; i < b.count; ++i) {
+      const int64_t L = toff[e0 + i + 1] - toff[e0 + i];
+      b.j[i].set = sets[e0 + i];
+      b.j[i].tok_base = toff[e0 + i];
+      b.j[i].L = (int32_t)L;
+      b.j[i].block_begin = blocks;
+      blocks += (int)ceil_div(L, 256);
+    }
+    attt_status st = fn(b, blocks);
+    if (st) return st;
+  }
+  return ATTT_OK;
+}
+}  // namespace
+
+extern "C" attt_status attt_ngram_set_size(int64_t capacity, int32_t n, size_t* bytes) {
+  if (n < 1 || n > ATTT_NGRAM_MAX_N)
+    return fail(ATTT_EINVAL, "ngram_set: n must be in [1, %d] (got %d)", ATTT_NGRAM_MAX_N, n);
+  if (capacity < 1 || capacity > kSetMaxCapacity)
+    return fail(ATTT_EINVAL, "ngram_set: capacity must be in [1, 2^30] (got %lld)", (long long)capacity);
+  if (!bytes) return fail(ATTT_EINVAL, "ngram_set: bytes is null");
+  *bytes = ngram_set_bytes(set_slots(capacity), n);
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ngram_set_init(void* const* sets, int32_t num_sets, int64_t capacity, int32_t n,
+                                           size_t set_bytes, void* stream) {
+  attt_status st = set_validate(sets, num_sets, capacity, n);
+  if (st) return st;
+  const int64_t S = set_slots(capacity);
+  if (set_bytes < ngram_set_bytes(S, n))
+    return fail(ATTT_ENOSPACE, "ngram_set: %zu bytes per set, need %zu", set_bytes, ngram_set_bytes(S, n));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int32_t e0 = 0; e0 < num_sets; e0 += kEpBatch) {
+    NgramSetBatch b{};
+    b.count = std::min<int32_t>(kEpBatch, num_sets - e0);
+    for (int i = 0; i < b.count; ++i) b.j[i].set = sets[e0 + i];
+    HIP_TRY(launch_ngram_set_init(b, S, n, s), "ngram_set_init");
+  }
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ngram_set_append(void* const* sets, const int32_t* tokens,
+                                             const int64_t* token_offsets, int32_t num_sets,
+                                             int64_t capacity, int32_t n, void* stream) {
+  attt_status st = set_validate(sets, num_sets, capacity, n);
+  if (st) return st;
+  st = check_offsets("ngram_set tokens", token_offsets, num_sets, INT32_MAX);
+  if (st) return st;
+  if (token_offsets[num_sets] > 0 && !tokens) return fail(ATTT_EINVAL, "ngram_set: tokens is null");
+  if (token_offsets[num_sets] >= ((int64_t)1 << 31))
+    return fail(ATTT_EUNSUPPORTED, "ngram_set: more than 2^31-1 tokens in one call");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t S = set_slots(capacity);
+  return set_batches(sets, token_offsets, num_sets, [&](const NgramSetBatch& b, int blocks) -> attt_status {
+    HIP_TRY(launch_ngram_set_append(b, blocks, tokens, S, capacity, n, s), "ngram_set_append");
+    return ATTT_OK;
+  });
+}
+
+extern "C" attt_status attt_ngram_set_weights(void* const* sets, const int32_t* tokens,
+                                              const int64_t* token_offsets, int32_t num_sets,
+                                              int64_t capacity, int32_t n, float w_min,
+                                              uint32_t* exposure, float* weights, void* stream) {
+  attt_status st = set_validate(sets, num_sets, capacity, n);
+  if (st) return st;
+  if (!(w_min >= 0x1p-20f && w_min <= 1.0f))
+    return fail(ATTT_EINVAL, "ngram_set: w_min must be in [2^-20, 1] (got %g)", (double)w_min);
+  st = check_offsets("ngram_set tokens", token_offsets, num_sets, INT32_MAX);
+  if (st) return st;
+  const int64_t T = token_offsets[num_sets];
+  if (T >= ((int64_t)1 << 31)) return fail(ATTT_EUNSUPPORTED, "ngram_set: more than 2^31-1 tokens in one call");
+  if (T > 0 && !tokens) return fail(ATTT_EINVAL, "ngram_set: tokens is null");
+  if (T > 0 && !weights) return fail(ATTT_EINVAL, "ngram_set: weights is null");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t S = set_slots(capacity);
+  return set_batches(sets, token_offsets, num_sets, [&](const NgramSetBatch& b, int blocks) -> attt_status {
+    HIP_TRY(launch_ngram_set_weights(b, blocks, tokens, S, n, w_min, exposure, weights, s), "ngram_set_weights");
+    return ATTT_OK;
+  });
 }
 
 // ------------------------------------------------------------------------------------------

@@ -23,6 +23,8 @@ enum KernelId {
   K_LORA_U,
   K_LORA_DADB,
   K_LORA_REDUCE,
+  K_NGRAM_SET,
+  K_NGRAM_SET_WEIGHT,
   K_NUM_KERNELS
 };
 
@@ -95,6 +97,27 @@ hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max
 hipError_t launch_ngram_weight(const NgramEpBatch& b, int total_blocks, int n, float w_min,
                                const uint16_t* partial, uint32_t* exposure, float* weights,
                                hipStream_t s);
+
+// ---- persistent n-gram set ---------------------------------------------------------------
+struct NgramSetJob {
+  void* set;         // the episode's set buffer
+  int64_t tok_base;  // first token of the episode's x in `tokens`
+  int32_t L;         // tokens of x
+  int32_t block_begin;
+};
+
+struct NgramSetBatch {
+  int32_t count;
+  int32_t pad;
+  NgramSetJob j[kEpBatch];
+};
+
+size_t ngram_set_bytes(int64_t slots, int n);
+hipError_t launch_ngram_set_init(const NgramSetBatch& b, int64_t slots, int n, hipStream_t s);
+hipError_t launch_ngram_set_append(const NgramSetBatch& b, int blocks, const int32_t* tokens, int64_t slots,
+                                   int64_t capacity, int n, hipStream_t s);
+hipError_t launch_ngram_set_weights(const NgramSetBatch& b, int blocks, const int32_t* tokens, int64_t slots,
+                                    int n, float w_min, uint32_t* exposure, float* weights, hipStream_t s);
 
 // ---- weighted cross-entropy ------------------------------------------------------------
 struct CeEp {

@@ -138,3 +138,47 @@ def test_timing_api_without_launches(L):
     assert attt.timing_read("ce_fwd_lse") == (0.0, 0)
     with pytest.raises(attt.AtttError):
         attt.timing_read("no_such_kernel")
+
+
+# ---- persistent n-gram sets ------------------------------------------------------------
+def _sets(*ptrs):
+    arr = (ctypes.c_void_p * len(ptrs))()
+    for i, p in enumerate(ptrs):
+        arr[i] = p
+    return arr
+
+
+def test_ngram_set_size(L):
+    out = ctypes.c_size_t(0)
+    assert L.attt_ngram_set_size(1000, 4, ctypes.byref(out)) == attt.OK
+    # 2048 slots of an 8-byte key, a 4-byte count and four 4-byte tokens, after a 256-byte header
+    assert out.value == 256 + 2048 * (8 + 4 + 16)
+    assert L.attt_ngram_set_size(1024, 4, ctypes.byref(out)) == attt.OK
+    assert out.value == 256 + 2048 * 28                  # load factor exactly 1/2 still fits
+    assert L.attt_ngram_set_size(1025, 4, ctypes.byref(out)) == attt.OK
+    assert out.value == 256 + 4096 * 28
+    assert L.attt_ngram_set_size(0, 4, ctypes.byref(out)) == attt.EINVAL
+    assert L.attt_ngram_set_size(1 << 31, 4, ctypes.byref(out)) == attt.EINVAL
+    assert L.attt_ngram_set_size(10, 17, ctypes.byref(out)) == attt.EINVAL
+    assert L.attt_ngram_set_size(10, 3, None) == attt.EINVAL
+
+
+def test_ngram_set_validation(L):
+    s = _sets(FAKE_WS)
+    big = 1 << 30
+    assert L.attt_ngram_set_init(s, 0, 100, 3, big, None) == attt.EINVAL
+    assert L.attt_ngram_set_init(s, 1, 100, 0, big, None) == attt.EINVAL
+    assert L.attt_ngram_set_init(s, 1, 0, 3, big, None) == attt.EINVAL
+    assert L.attt_ngram_set_init(_sets(None), 1, 100, 3, big, None) == attt.EINVAL
+    assert L.attt_ngram_set_init(_sets(ctypes.c_void_p(0x7F0000001010)), 1, 100, 3, big, None) == attt.EINVAL
+    assert b"aligned" in L.attt_last_error()
+    need = ctypes.c_size_t(0)
+    assert L.attt_ngram_set_size(100, 3, ctypes.byref(need)) == attt.OK
+    assert L.attt_ngram_set_init(s, 1, 100, 3, need.value - 1, None) == attt.ENOSPACE
+    _, tp = _off([0, 5])
+    _, bad = _off([0, 5, 3])
+    assert L.attt_ngram_set_append(s, FAKE, bad, 2, 100, 3, None) == attt.EINVAL
+    assert L.attt_ngram_set_append(s, None, tp, 1, 100, 3, None) == attt.EINVAL
+    assert L.attt_ngram_set_weights(s, FAKE, tp, 1, 100, 3, 0.0, None, FAKE, None) == attt.EINVAL
+    assert L.attt_ngram_set_weights(s, FAKE, tp, 1, 100, 3, 0.05, None, None, None) == attt.EINVAL
+    assert b"weights is null" in L.attt_last_error()
