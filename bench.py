@@ -202,6 +202,46 @@ def cpu_baseline(wl, rows):
                        f"ngram {t_ng:.2f}s, ce {t_ce:.1f}s est, lora {t_lora:.2f}s")}
 
 
+def ngram_set_part(wl, attt, torch, reps):
+    """The persistent-set alternative for the n-gram rows (the history update of Algorithm 1),
+    outside the timed step: per update, one append of that update's text to every episode's
+    set (measured while the sets are built from the previous updates, one call per update)
+    and one weights query of the new update (over `reps` calls). Times are the kernels' own,
+    from the library's launch events, so host call overhead between small calls is excluded."""
+    from gpu_util import dev_i32
+    cfg, tok = wl.cfg, wl.tokens()
+    E = cfg.episodes
+    capacity = int(max(np.diff(tok["hist_off"]))) + cfg.update_len
+    nbytes = attt.ngram_set_size(capacity, cfg.n)
+    sets = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(E)]
+    attt.ngram_set_init(sets, capacity, cfg.n)
+    torch.cuda.synchronize()
+    texts_per_update = []
+    for i in range(cfg.prior_updates):
+        texts = [h[i * cfg.prior_len:(i + 1) * cfg.prior_len] for h in tok["history"]]
+        off = np.zeros(E + 1, np.int64)
+        off[1:] = np.cumsum([len(t) for t in texts])
+        texts_per_update.append((dev_i32(np.concatenate(texts)), off))
+    attt.timing_enable(True)
+    attt.timing_reset()
+    for flat, off in texts_per_update:
+        attt.ngram_set_append(sets, flat, off, capacity, cfg.n)
+    torch.cuda.synchronize()
+    app_ms, app_n = attt.timing_read("ngram_set")
+    toks = dev_i32(tok["tok_flat"])
+    f = torch.empty(len(tok["tok_flat"]), dtype=torch.int32, device="cuda")
+    w = torch.empty(len(tok["tok_flat"]), dtype=torch.float32, device="cuda")
+    for _ in range(reps):
+        attt.ngram_set_weights(sets, toks, tok["tok_off"], capacity, cfg.n, cfg.w_min, out=(f, w))
+    torch.cuda.synchronize()
+    q_ms, q_n = attt.timing_read("ngram_set_weight")
+    attt.timing_enable(False)
+    append = app_ms / max(1, app_n)
+    query = q_ms / max(1, q_n)
+    return {"query_ms": query, "append_ms": append, "ms": query + append,
+            "set_bytes_per_episode": nbytes, "capacity": capacity}
+
+
 def main():
     args = parse()
     if args.hbm_calibrate:
@@ -273,6 +313,10 @@ def main():
         "lora_pass": {"ms": lo_ms, "algorithmic_gbs": alg["lora_bytes"] / (lo_ms * 1e-3) / 1e9,
                       "frac_of_hbm_peak": alg["lora_bytes"] / (lo_ms * 1e-3) / PEAK_HBM},
     }
+    if cfg.prior_updates > 0:
+        ns = ngram_set_part(wl, attt, torch, max(args.steps, 10))
+        ns["streaming_ngram_pass_ms"] = ng_ms
+        parts["ngram_set_per_update"] = ns
     out = {
         "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
