@@ -205,8 +205,9 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int t = 0; t < kLoraMaxTiles; ++t)
-        la[ks][t] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rl[t], (uint32_t)(l16 * Jr.rows_pad + t0 + ks * 32 + g * 8) * 2u, 0, 0));
+        if (t < nt)  // uniform: a job's tile count; unused tiles issue no load
+          la[ks][t] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rl[t], (uint32_t)(l16 * Jr.rows_pad + t0 + ks * 32 + g * 8) * 2u, 0, 0));
   };
   u32x4 v0[2], v1[2], la0[2][kLoraMaxTiles], la1[2][kLoraMaxTiles];
   // One step: store its rows transposed (row pairs as 32-bit words) into buffer `buf`, one
