@@ -434,8 +434,11 @@ extern "C" attt_status attt_ngram_set_weights(void* const* sets, const int32_t* 
 // ------------------------------------------------------------------------------------------
 namespace {
 
-constexpr int64_t kCeRowBlock = 8192;     // rows per backward block
-constexpr int64_t kCeVocabChunk = 32768;  // vocab columns per backward chunk
+// Backward blocking: rows per block and vocab columns per chunk. A chunk's staged exponentials
+// take R x Vc x 2 bytes (2 GiB at 8192 x 131072): HBM has room, and one chunk over the whole
+// vocabulary (V <= 131072) saves the float32 dH partials between chunks and launches.
+constexpr int64_t kCeRowBlock = 8192;
+constexpr int64_t kCeVocabChunk = 131072;
 
 struct CePlan {
   CeGemmShape fwd{64, 64}, lexp{64, 64}, dz{64, 64}, dh{64, 64};
