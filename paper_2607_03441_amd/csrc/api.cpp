@@ -439,6 +439,7 @@ namespace {
 // vocabulary (V <= 131072) saves the float32 dH partials between chunks and launches.
 constexpr int64_t kCeRowBlock = 8192;
 constexpr int64_t kCeVocabChunk = 131072;
+constexpr int64_t kCeExpLaunch = 32768;  // columns per launch of the first GEMM (multiple of 256)
 
 struct CePlan {
   CeGemmShape fwd{64, 64}, lexp{64, 64}, dz{64, 64}, dh{64, 64};
@@ -651,10 +652,14 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
     for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
       const int64_t width = std::min(P.Vc, V - c0);
       const bool first = c0 == 0, last = c0 + P.Vc >= V;
-      HIP_TRY(launch_ce_logit_exp(P.lexp, hidden, lm_head, labels, label_logit, (int)r0, (int)R, (int)d,
-                                  (int)c0, (int)width, (int)V, sig_part, (int)P.n_vb_exp, dz, (int)P.Vc,
-                                  flag, s),
-              "ce_logit_exp");
+      // The first GEMM runs in launches of kCeExpLaunch columns: a launch boundary lines the
+      // workgroups up again, so each XCD's concurrent tiles keep sharing their operand panels
+      // in L2 instead of drifting apart over a whole-vocabulary launch (fewer L2 misses).
+      for (int64_t cc = 0; cc < width; cc += kCeExpLaunch)
+        HIP_TRY(launch_ce_logit_exp(P.lexp, hidden, lm_head, labels, label_logit, (int)r0, (int)R, (int)d,
+                                    (int)(c0 + cc), (int)std::min(kCeExpLaunch, width - cc), (int)V, sig_part,
+                                    (int)P.n_vb_exp, static_cast<uint8_t*>(dz) + cc * 2, (int)P.Vc, flag, s),
+                "ce_logit_exp");
       if (last)
         HIP_TRY(launch_ce_row_final((int)r0, (int)R, sig_part, (int)P.n_vb_exp, label_logit, weights, coef,
                                     lse_buf, rowloss, sa, sb, s),
