@@ -270,14 +270,19 @@ def main():
     attt.timing_enable(True)
     attt.timing_reset()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps - 1)]
     torch.cuda.synchronize()
     start.record()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         step.run()
+        if i + 1 < args.steps:
+            marks[i].record()
     stop.record()
     torch.cuda.synchronize()
     attt.timing_enable(False)
     ms_step = start.elapsed_time(stop) / args.steps
+    bounds = [start] + marks + [stop]
+    per_step = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)])
     kern = {}
     for name in attt.kernel_names():
         ms, n = attt.timing_read(name)
@@ -320,6 +325,7 @@ def main():
     out = {
         "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "step_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic (seeded; see workloads/gen.py)",
         "config": {"workload": cfg.name, "episodes": cfg.episodes, "update_tokens": cfg.rows,
