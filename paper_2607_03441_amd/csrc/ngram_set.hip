@@ -1,13 +1,14 @@
 // Persistent n-gram counts of an episode's history (the history update of Algorithm 1:
 // H^tok_{k+1} = H^tok_k followed by x_k) and exposure weights read from them (Eq. 8-9).
 //
-// A set is one caller-owned device buffer:
-//   header (256 B)  history length, distinct n-grams held, error flags, the last n-1 history
-//                   tokens (double-buffered), and the n and table size it was built for
-//   keys   u64 [S]  64-bit key of the n-gram in each slot, 0 = empty (keys are odd)
-//   counts u32 [S]  occurrences of that n-gram in the history
-//   toks   i32 [S][n] the n-gram's tokens, for exact confirmation
-// S is a power of two at least twice the capacity; slots are found by linear probing.
+// A set is one caller-owned device buffer: a 256-byte header (history length, distinct n-grams
+// held, error flags, the last n-1 history tokens (double-buffered), and the n and table size it
+// was built for) followed by S slot records of R = 12 + 4n bytes rounded up to 16:
+//   u64 key   64-bit key of the n-gram, 0 = empty slot (keys are odd)
+//   u32 count occurrences of the n-gram in the history
+//   i32 tok[n] the n-gram's tokens, for exact confirmation
+// so a lookup reads one record (one or two cache lines) instead of three arrays. S is a power
+// of two at least twice the capacity; slots are found by linear probing.
 //
 // Appending x to H adds the n-grams whose last token lies in x: those inside x and the n-1
 // that start in the history's last n-1 tokens (n-grams straddling two updates count). One
@@ -15,8 +16,8 @@
 // finds its key, and adds 1 to the count; counts are integers, so the final table does not
 // depend on the order of the adds. A second kernel confirms, after all claims have landed,
 // that every new n-gram's slot holds exactly its tokens (two different n-grams with the same
-// 64-bit key would otherwise share a count) and flags a collision if not; a third advances
-// the history length and switches to the new tail.
+// 64-bit key would otherwise share a count) and flags a collision if not; its last block to
+// finish advances the history length and switches to the new tail.
 //
 // The weights kernel looks up each n-gram start s of x (count 0 when absent or when the slot's
 // tokens differ), then f(j) = max over the starts that cover j and w = max(w_min, 1/(1+f)),
@@ -38,24 +39,31 @@ struct NgramSetHeader {
   int32_t par;      // which tail buffer is current
   int64_t slots;    // S
   int32_t tail[2][kMaxN];  // tail[par][i] = H[ntok - (n-1) + i] for the last min(ntok, n-1)
+  uint32_t ticket;  // blocks of the running confirm pass that have finished
 };
 static_assert(sizeof(NgramSetHeader) <= 256, "header fits its 256 bytes");
 
 constexpr uint32_t kSetOverflow = 1u, kSetCollision = 2u, kSetMismatch = 4u;
 
+__host__ __device__ __forceinline__ int64_t set_record_bytes(int n) { return (12 + 4 * n + 15) / 16 * 16; }
+
+// Slot records: key at +0, count at +8, tokens from +12.
 struct SetView {
   NgramSetHeader* hdr;
-  unsigned long long* keys;
-  uint32_t* counts;
-  int32_t* toks;
+  uint8_t* rec;
+  int64_t R;
+  __device__ __forceinline__ unsigned long long* key(int64_t s) const {
+    return reinterpret_cast<unsigned long long*>(rec + s * R);
+  }
+  __device__ __forceinline__ uint32_t* count(int64_t s) const { return reinterpret_cast<uint32_t*>(rec + s * R + 8); }
+  __device__ __forceinline__ int32_t* toks(int64_t s) const { return reinterpret_cast<int32_t*>(rec + s * R + 12); }
 };
 
-__device__ __forceinline__ SetView set_view(uint8_t* base, int64_t S) {
+__device__ __forceinline__ SetView set_view(uint8_t* base, int n) {
   SetView v;
   v.hdr = reinterpret_cast<NgramSetHeader*>(base);
-  v.keys = reinterpret_cast<unsigned long long*>(base + 256);
-  v.counts = reinterpret_cast<uint32_t*>(base + 256 + S * 8);
-  v.toks = reinterpret_cast<int32_t*>(base + 256 + S * 12);
+  v.rec = base + 256;
+  v.R = set_record_bytes(n);
   return v;
 }
 
@@ -95,10 +103,10 @@ __device__ __forceinline__ bool gather_new(const NgramSetHeader& h, const int32_
 __global__ __launch_bounds__(256) void ngram_set_init_kernel(NgramSetBatch b, int64_t S, int n) {
   const int ji = (int)blockIdx.y;
   if (ji >= b.count) return;
-  SetView v = set_view(static_cast<uint8_t*>(b.j[ji].set), S);
+  SetView v = set_view(static_cast<uint8_t*>(b.j[ji].set), n);
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < S; i += (int64_t)gridDim.x * 256) {
-    v.keys[i] = 0ull;
-    v.counts[i] = 0u;
+    *v.key(i) = 0ull;
+    *v.count(i) = 0u;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     v.hdr->ntok = 0;
@@ -107,6 +115,7 @@ __global__ __launch_bounds__(256) void ngram_set_init_kernel(NgramSetBatch b, in
     v.hdr->n = n;
     v.hdr->par = 0;
     v.hdr->slots = S;
+    v.hdr->ticket = 0;
   }
 }
 
@@ -116,7 +125,7 @@ __global__ __launch_bounds__(256) void ngram_set_append_kernel(NgramSetBatch b, 
   int ji = 0;
   while (ji + 1 < b.count && b.j[ji + 1].block_begin <= (int)blockIdx.x) ++ji;
   const NgramSetJob J = b.j[ji];
-  SetView v = set_view(static_cast<uint8_t*>(J.set), S);
+  SetView v = set_view(static_cast<uint8_t*>(J.set), n);
   const NgramSetHeader& h = *v.hdr;
   if (h.n != n || h.slots != S) {
     if (blockIdx.x == J.block_begin && threadIdx.x == 0) atomicOr(&v.hdr->flags, kSetMismatch);
@@ -140,59 +149,63 @@ __global__ __launch_bounds__(256) void ngram_set_append_kernel(NgramSetBatch b, 
   const unsigned long long key = set_key(t, n);
   int64_t slot = set_home(key, S);
   for (int64_t probe = 0; probe < S; ++probe, slot = (slot + 1) & (S - 1)) {
-    unsigned long long k = v.keys[slot];
+    unsigned long long k = *v.key(slot);
     if (k == 0ull) {
-      k = atomicCAS(v.keys + slot, 0ull, key);
+      k = atomicCAS(v.key(slot), 0ull, key);
       if (k == 0ull) {  // claimed: store the tokens, count one occurrence and one entry
-        for (int i = 0; i < n; ++i) v.toks[slot * n + i] = t[i];
-        atomicAdd(v.counts + slot, 1u);
+        int32_t* dst = v.toks(slot);
+        for (int i = 0; i < n; ++i) dst[i] = t[i];
+        atomicAdd(v.count(slot), 1u);
         if (atomicAdd(&v.hdr->nent, 1u) >= (uint64_t)capacity) atomicOr(&v.hdr->flags, kSetOverflow);
         return;
       }
     }
     if (k == key) {
-      atomicAdd(v.counts + slot, 1u);
+      atomicAdd(v.count(slot), 1u);
       return;
     }
   }
   atomicOr(&v.hdr->flags, kSetOverflow);  // every slot taken
 }
 
-// ---- confirm: each new n-gram's slot holds its own tokens ---------------------------------------
+// ---- confirm: each new n-gram's slot holds its own tokens; the last block commits ----------------
+// The block that finishes last (a ticket in the header, taken after a fence) advances the history
+// length and switches to the new tail, once every block has read the old ones.
 __global__ __launch_bounds__(256) void ngram_set_confirm_kernel(NgramSetBatch b, const int32_t* __restrict__ tokens,
                                                                 int64_t S, int n) {
   int ji = 0;
   while (ji + 1 < b.count && b.j[ji + 1].block_begin <= (int)blockIdx.x) ++ji;
   const NgramSetJob J = b.j[ji];
-  SetView v = set_view(static_cast<uint8_t*>(J.set), S);
-  const NgramSetHeader& h = *v.hdr;
-  if (h.n != n || h.slots != S) return;
+  SetView v = set_view(static_cast<uint8_t*>(J.set), n);
+  NgramSetHeader& h = *v.hdr;
+  if (h.n != n || h.slots != S) return;  // uniform per block: the set is flagged, nothing commits
   const int e = ((int)blockIdx.x - J.block_begin) * 256 + threadIdx.x;
-  if (e >= J.L) return;
   int32_t t[kMaxN];
-  if (!gather_new(h, h.tail[h.par], tokens + J.tok_base, e, n, t)) return;
-  const unsigned long long key = set_key(t, n);
-  int64_t slot = set_home(key, S);
-  for (int64_t probe = 0; probe < S; ++probe, slot = (slot + 1) & (S - 1)) {
-    const unsigned long long k = v.keys[slot];
-    if (k == 0ull) return;  // not inserted: the table overflowed (already flagged)
-    if (k == key) {
-      bool same = true;
-      for (int i = 0; i < n; ++i) same &= v.toks[slot * n + i] == t[i];
-      if (!same) atomicOr(&v.hdr->flags, kSetCollision);
-      return;
+  if (e < J.L && gather_new(h, h.tail[h.par], tokens + J.tok_base, e, n, t)) {
+    const unsigned long long key = set_key(t, n);
+    int64_t slot = set_home(key, S);
+    for (int64_t probe = 0; probe < S; ++probe, slot = (slot + 1) & (S - 1)) {
+      const unsigned long long k = *v.key(slot);
+      if (k == 0ull) break;  // not inserted: the table overflowed (already flagged)
+      if (k == key) {
+        bool same = true;
+        const int32_t* st = v.toks(slot);
+        for (int i = 0; i < n; ++i) same &= st[i] == t[i];
+        if (!same) atomicOr(&h.flags, kSetCollision);
+        break;
+      }
     }
   }
-}
-
-// ---- commit: history length and tail move on (one thread per set) --------------------------------
-__global__ __launch_bounds__(64) void ngram_set_commit_kernel(NgramSetBatch b, int64_t S, int n) {
-  const int ji = (int)(blockIdx.x * 64 + threadIdx.x);
-  if (ji >= b.count) return;
-  SetView v = set_view(static_cast<uint8_t*>(b.j[ji].set), S);
-  if (v.hdr->n != n || v.hdr->slots != S || b.j[ji].L == 0) return;  // an empty x keeps the tail
-  v.hdr->ntok += b.j[ji].L;
-  v.hdr->par ^= 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const uint32_t nb = (uint32_t)((J.L + 255) / 256);
+    if (atomicAdd(&h.ticket, 1u) == nb - 1) {
+      h.ntok += J.L;
+      h.par ^= 1;
+      h.ticket = 0;
+    }
+  }
 }
 
 // ---- weights: lookups of x's n-gram starts, window maximum, w -------------------------------------
@@ -205,7 +218,7 @@ __global__ __launch_bounds__(256) void ngram_set_weights_kernel(NgramSetBatch b,
   int ji = 0;
   while (ji + 1 < b.count && b.j[ji + 1].block_begin <= (int)blockIdx.x) ++ji;
   const NgramSetJob J = b.j[ji];
-  SetView v = set_view(static_cast<uint8_t*>(J.set), S);
+  SetView v = set_view(static_cast<uint8_t*>(J.set), n);
   const bool bad = v.hdr->flags != 0 || v.hdr->n != n || v.hdr->slots != S;
   const int j0 = ((int)blockIdx.x - J.block_begin) * 256;
   const int32_t* x = tokens + J.tok_base;
@@ -220,12 +233,13 @@ __global__ __launch_bounds__(256) void ngram_set_weights_kernel(NgramSetBatch b,
       const unsigned long long key = set_key(t, n);
       int64_t slot = set_home(key, S);
       for (int64_t probe = 0; probe < S; ++probe, slot = (slot + 1) & (S - 1)) {
-        const unsigned long long k = v.keys[slot];
+        const unsigned long long k = *v.key(slot);
         if (k == 0ull) break;
         if (k == key) {
           bool same = true;
-          for (int i = 0; i < n; ++i) same &= v.toks[slot * n + i] == t[i];
-          if (same) cnt = v.counts[slot];
+          const int32_t* st = v.toks(slot);
+          for (int i = 0; i < n; ++i) same &= st[i] == t[i];
+          if (same) cnt = *v.count(slot);
           break;
         }
       }
@@ -247,7 +261,7 @@ __global__ __launch_bounds__(256) void ngram_set_weights_kernel(NgramSetBatch b,
 }
 
 size_t ngram_set_bytes(int64_t S, int n) {
-  const size_t raw = 256 + (size_t)S * (8 + 4) + (size_t)S * n * 4;
+  const size_t raw = 256 + (size_t)S * (size_t)set_record_bytes(n);
   return (raw + 255) & ~(size_t)255;
 }
 
@@ -266,11 +280,9 @@ hipError_t launch_ngram_set_append(const NgramSetBatch& b, int blocks, const int
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(ngram_set_confirm_kernel, dim3(blocks), dim3(256), 0, s, b, tokens, S, n);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL(ngram_set_commit_kernel, dim3((b.count + 63) / 64), dim3(64), 0, s, b, S, n);
-  return hipGetLastError();
+  return hipSuccess;  // every text empty: nothing changes
 }
 
 hipError_t launch_ngram_set_weights(const NgramSetBatch& b, int blocks, const int32_t* tokens, int64_t S,

@@ -108,8 +108,12 @@ def test_ce_workspace_sizes():
     fwd = attt.ce_workspace_size(8192, 4096, 128256, attt.BF16, want_grad=False)
     bwd = attt.ce_workspace_size(8192, 4096, 128256, attt.BF16, want_grad=True)
     assert 0 < fwd < bwd
-    # the backward stages one bounded vocab chunk, never the full N x V gradient
-    assert bwd - fwd < 8192 * 128256 * 2
+    # the backward stages one bounded block of rows x vocab columns, never the full N x V
+    # gradient: past the row block, more rows add only a few bytes per row
+    fwd8 = attt.ce_workspace_size(8 * 8192, 4096, 128256, attt.BF16, want_grad=False)
+    bwd8 = attt.ce_workspace_size(8 * 8192, 4096, 128256, attt.BF16, want_grad=True)
+    assert bwd8 - fwd8 < 8 * 8192 * 128256 * 2 // 4
+    assert (bwd8 - fwd8) - (bwd - fwd) <= 16 * 7 * 8192
     assert attt.ce_workspace_size(4, 8, 3, attt.F32) >= 256
 
 
@@ -151,12 +155,15 @@ def _sets(*ptrs):
 def test_ngram_set_size(L):
     out = ctypes.c_size_t(0)
     assert L.attt_ngram_set_size(1000, 4, ctypes.byref(out)) == attt.OK
-    # 2048 slots of an 8-byte key, a 4-byte count and four 4-byte tokens, after a 256-byte header
-    assert out.value == 256 + 2048 * (8 + 4 + 16)
+    # 2048 slot records (8-byte key, 4-byte count, four 4-byte tokens: 28 -> 32 bytes) after a
+    # 256-byte header
+    assert out.value == 256 + 2048 * 32
     assert L.attt_ngram_set_size(1024, 4, ctypes.byref(out)) == attt.OK
-    assert out.value == 256 + 2048 * 28                  # load factor exactly 1/2 still fits
+    assert out.value == 256 + 2048 * 32                  # load factor exactly 1/2 still fits
     assert L.attt_ngram_set_size(1025, 4, ctypes.byref(out)) == attt.OK
-    assert out.value == 256 + 4096 * 28
+    assert out.value == 256 + 4096 * 32
+    assert L.attt_ngram_set_size(1000, 16, ctypes.byref(out)) == attt.OK
+    assert out.value == 256 + 2048 * 80                  # 12 + 64 bytes -> 80
     assert L.attt_ngram_set_size(0, 4, ctypes.byref(out)) == attt.EINVAL
     assert L.attt_ngram_set_size(1 << 31, 4, ctypes.byref(out)) == attt.EINVAL
     assert L.attt_ngram_set_size(10, 17, ctypes.byref(out)) == attt.EINVAL
