@@ -67,7 +67,8 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
   const int kdim = Jr.kdim, nt = Jr.nt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
-  // this workgroup's 32 rows; rows past the input read as zero through the descriptor range
+  constexpr int RG = kLoraP1Rows / 16;  // groups of 16 rows
+  // this workgroup's rows; rows past the input read as zero through the descriptor range
   const int row0 = rt * kLoraP1Rows;
   const int nrows = max(0, min(kLoraP1Rows, Jr.rows - row0));
   const bf16_t* src = static_cast<const bf16_t*>(Jr.src) + (int64_t)row0 * kdim;
@@ -80,22 +81,22 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
   const int kq = ((kdim + 4 * 2 * kLoraKBlock - 1) / (4 * 2 * kLoraKBlock)) * 2 * kLoraKBlock;
   const int kbeg = wave * kq, kend = min(kdim, kbeg + kq);
 
-  f32x4 acc[2][NT];
+  f32x4 acc[RG][NT];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < RG; ++a)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Step kb: for MFMA q, lane (l16, g) holds rows a*16 + l16 at k = kb + q*32 + g*8 .. +7 (the
   // MFMA's own k order; one load instruction covers 64 contiguous bytes of 16 rows), and for
   // every tile the adapter row l16 at the same k. k at or past kend reads as zero.
-  auto load = [&](int kb, u32x4 (&xa)[2][4], u32x4 (&oa)[NT][4]) {
+  auto load = [&](int kb, u32x4 (&xa)[RG][4], u32x4 (&oa)[NT][4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int k = kb + q * 32 + g * 8;
       const bool kin = k < kend;
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < RG; ++a)
         xa[a][q] = __builtin_bit_cast(
             u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, kin ? (uint32_t)((a * 16 + l16) * kdim + k) * 2u : kOOB, 0, 0));
 #pragma unroll
@@ -104,19 +105,19 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
             u32x4, __builtin_amdgcn_raw_buffer_load_b128(ro[t], kin ? (uint32_t)(l16 * kdim + k) * 2u : kOOB, 0, 0));
     }
   };
-  auto mma = [&](const u32x4 (&xa)[2][4], const u32x4 (&oa)[NT][4]) {
+  auto mma = [&](const u32x4 (&xa)[RG][4], const u32x4 (&oa)[NT][4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if (t >= nt) break;
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < RG; ++a)
           acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[a][q]),
                                                               __builtin_bit_cast(bf16x8, oa[t][q]), acc[a][t], 0, 0, 0);
       }
   };
-  u32x4 xa0[2][4], oa0[NT][4], xa1[2][4], oa1[NT][4];
+  u32x4 xa0[RG][4], oa0[NT][4], xa1[RG][4], oa1[NT][4];
   if (kbeg < kend) {
     load(kbeg, xa0, oa0);
     for (int kb = kbeg; kb < kend; kb += 2 * kLoraKBlock) {
@@ -127,10 +128,10 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
     }
   }
   // waves 1-3 hand their sums to wave 0 through LDS (fixed order: wave 0 + 1 + 2 + 3)
-  __shared__ f32x4 red[3][2 * NT][64];
+  __shared__ f32x4 red[3][RG * NT][64];
   if (wave > 0) {
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RG; ++a)
 #pragma unroll
       for (int t = 0; t < NT; ++t) red[wave - 1][a * NT + t][lane] = acc[a][t];
   }
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
 #pragma unroll
   for (int w = 0; w < 3; ++w)
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < RG; ++a)
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[a][t] += red[w][a * NT + t][lane];
   // D of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16.
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
     bf16_t* outT = reinterpret_cast<bf16_t*>(ws + Jr.t[t].out_off);
     const float s = Jr.t[t].scale;
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
+    for (int a = 0; a < RG; ++a) {
       const int r = row0 + a * 16 + g * 4;
       uint2 pk;
       pk.x = pack_bf16x2(s * acc[a][t][0], s * acc[a][t][1]);

@@ -191,6 +191,24 @@ def test_ce_bf16_overflow_guard(attt):
     _ce_case(attt, h, W, labels, weights, np.array([0, 100, N], np.int64), True)
 
 
+def test_ce_bf16_overflow_guard_many_tiles(attt):
+    """The exact path at a size where its GEMMs have more tiles than the guard's grid (one
+    workgroup per CU), so every guard workgroup walks several tiles: forward and dZ on
+    256x256 tiles (9 x 57), dH on 128x128 tiles (16 x 17)."""
+    N, d, V = 2176, 2048, 14592
+    h = random_dense((N, d), 15.0, True, 34)
+    W = random_dense((V, d), 0.05, True, 35)
+    rng = np.random.default_rng(36)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    z = h.f32.astype(np.float64) @ W.f32.astype(np.float64).T
+    gap = z.max(1) - z[np.arange(N), labels]
+    assert np.sum(gap > 90) >= 10
+    del z
+    weights = rng.uniform(0.05, 1, N).astype(np.float32)
+    note("ce bf16 overflow guard, many tiles")
+    _ce_case(attt, h, W, labels, weights, np.array([0, 1000, N], np.int64), True)
+
+
 def test_ce_bf16_confident_labels(attt):
     """p_y within about 1e-5 of 1: the gradient rows are small differences, computed without
     cancellation (the label term is kept out of the sums)."""
