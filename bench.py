@@ -242,6 +242,29 @@ def ngram_set_part(wl, attt, torch, reps):
             "set_bytes_per_episode": nbytes, "capacity": capacity}
 
 
+def lora_sgd_part(step, attt, torch, reps):
+    """The adapter step of Eq. 2 for the step's adapters, outside the timed step: float32
+    masters of every A and B updated by their gradients, bf16 operand copies written and the
+    gradients reset (one grouped call, the kernel's own time over `reps` calls). Algorithm 1
+    takes two such steps per update."""
+    params, nbytes = [], 0
+    for p in step.problems:
+        for k, g in (("A", "dA"), ("B", "dB")):
+            master = p[k].float().clone()
+            params.append(dict(param=master, grad=p[g], param_bf16=torch.empty_like(p[k])
+                               if p[k].dtype == torch.bfloat16 else None))
+            nbytes += master.numel() * (4 + 4 + 4 + 4 + (2 if p[k].dtype == torch.bfloat16 else 0))
+    attt.timing_enable(True)
+    attt.timing_reset()
+    for _ in range(reps):
+        attt.lora_sgd_step(params, 5e-4, zero_grad=True)
+    torch.cuda.synchronize()
+    ms, n = attt.timing_read("lora_sgd")
+    attt.timing_enable(False)
+    ms /= max(1, n)
+    return {"ms": ms, "bytes": nbytes, "gbs": nbytes / (ms * 1e-3) / 1e9, "lr": 5e-4}
+
+
 def main():
     args = parse()
     if args.hbm_calibrate:
@@ -318,6 +341,7 @@ def main():
         "lora_pass": {"ms": lo_ms, "algorithmic_gbs": alg["lora_bytes"] / (lo_ms * 1e-3) / 1e9,
                       "frac_of_hbm_peak": alg["lora_bytes"] / (lo_ms * 1e-3) / PEAK_HBM},
     }
+    parts["lora_sgd_per_step"] = lora_sgd_part(step, attt, torch, max(args.steps, 10))
     if cfg.prior_updates > 0:
         ns = ngram_set_part(wl, attt, torch, max(args.steps, 10))
         ns["streaming_ngram_pass_ms"] = ng_ms

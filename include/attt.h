@@ -13,6 +13,7 @@
  *                             grow with every update (the history update of Algorithm 1)
  *   attt_weighted_ce_fwd_bwd  weighted CE through the frozen LM head, loss and dL/dh (Eq. 10)
  *   attt_lora_grad            LoRA dA / dB of the adapted projections (Sec. 3.1, Appendix C)
+ *   attt_lora_sgd_step        the adapter step theta <- theta - lr grad (Eq. 2, Algorithm 1)
  *
  * Conventions shared by every call
  *   - Data pointers are device pointers unless a parameter says "host". The caller owns all
@@ -208,6 +209,37 @@ attt_status attt_lora_workspace_size(const attt_lora_problem* problems, int32_t 
                                      size_t* bytes);
 attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t count, int32_t dtype,
                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * attt_lora_sgd_step: the adapter update of Eq. 2 and Algorithm 1 (the parameter step that
+ * follows the gradient of the weighted loss), theta <- theta - lr * grad, for adapter
+ * parameters kept in float32. Per element, in float32: the product lr * grad is rounded to
+ * nearest, then the difference is (two roundings, no fused multiply-add), so any IEEE float32
+ * evaluation of  param - lr * grad  reproduces the result bit for bit.
+ *
+ * params  HOST array of `count` descriptors, processed as one grouped launch:
+ *   param       device float [n], updated in place
+ *   grad        device float [n]; read, then set to 0 when zero_grad != 0, ready for the next
+ *               accumulation by attt_lora_grad (whose dA / dB are +=)
+ *   param_bf16  device bf16 [n] or NULL: the updated param rounded to nearest even, the operand
+ *               copy that the next bf16 attt_lora_grad call reads as A or B
+ *   0 <= n < 2^31 (ATTT_EUNSUPPORTED beyond); descriptors with n == 0 are skipped
+ * lr      finite (the paper's setting is 5e-4, two steps per update)
+ * Arrays are caller-owned; param and grad 4-byte aligned, param_bf16 2-byte aligned; no array
+ * may overlap another of any descriptor. Nothing is allocated; launches are asynchronous on
+ * `stream`.
+ * Errors: ATTT_EINVAL (count < 0, null params with count > 0, non-finite lr, n < 0, null param
+ * or grad with n > 0, misalignment), ATTT_EUNSUPPORTED, ATTT_EHIP.
+ * ------------------------------------------------------------------------------------ */
+typedef struct attt_lora_param {
+  float* param;
+  float* grad;
+  void* param_bf16;
+  int64_t n;
+} attt_lora_param;
+
+attt_status attt_lora_sgd_step(const attt_lora_param* params, int32_t count, float lr, int32_t zero_grad,
+                               void* stream);
 
 /* --------------------------------------------------------------------------------------
  * Kernel timing (diagnostics). When enabled, every launch of a named kernel is bracketed

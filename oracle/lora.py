@@ -11,6 +11,11 @@ Given the upstream gradient dy = dLoss/dy, with U = x A^T:
     dA = (s dy B)^T x        [r, d_in]
 
 Computed in float64 from the exact input values.
+
+The adapter step of Eq. 2 (and of Algorithm 1), theta <- theta - eta grad, is taken on
+float32 parameters in float32 arithmetic: the product eta * grad rounded to nearest, then the
+difference rounded to nearest (the paper fixes no precision; this is the reading the library
+documents). Its bf16 operand copy rounds to nearest even.
 """
 import numpy as np
 
@@ -45,3 +50,21 @@ def lora_forward(x, W0, A, B, scale):
     if W0 is not None:
         y = y + x @ np.asarray(W0, np.float64).T
     return y
+
+
+def sgd_step(param, grad, lr):
+    """theta - lr * grad (Eq. 2) in float32: numpy rounds the product and the difference to
+    nearest, one IEEE operation each."""
+    p = np.asarray(param, np.float32)
+    g = np.asarray(grad, np.float32)
+    return p - np.float32(lr) * g
+
+
+def bf16_round_bits(values):
+    """bfloat16 bit patterns of float32 values, rounded to nearest, ties to even (the upper 16
+    bits after adding 0x7FFF plus the lowest kept bit); NaN stays a quiet NaN of the same sign."""
+    b = np.asarray(values, np.float32).view(np.uint32).astype(np.uint64)
+    nan = np.isnan(np.asarray(values, np.float32))
+    r = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16) & 0xFFFF
+    q = ((b >> 16) | 0x0040) & 0xFFFF
+    return np.where(nan, q, r).astype(np.uint16)

@@ -13,9 +13,9 @@ import numpy as np
 
 __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_workspace_size",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
-           "weighted_ce_fwd_bwd", "ce_workspace_size", "lora_grad", "lora_workspace_size",
+           "weighted_ce_fwd_bwd", "ce_workspace_size", "lora_grad", "lora_workspace_size", "lora_sgd_step",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
-           "F32", "BF16", "LoraProblem"]
+           "F32", "BF16", "LoraProblem", "LoraParam"]
 
 F32 = 0
 BF16 = 1
@@ -36,6 +36,11 @@ class LoraProblem(ctypes.Structure):
                 ("B", ctypes.c_void_p), ("dA", ctypes.c_void_p), ("dB", ctypes.c_void_p),
                 ("rows", ctypes.c_int64), ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64),
                 ("rank", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class LoraParam(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("param_bf16", ctypes.c_void_p),
+                ("n", ctypes.c_int64)]
 
 
 def lib_path():
@@ -82,6 +87,8 @@ def load():
     L.attt_lora_workspace_size.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, psz]
     L.attt_lora_grad.restype = i32
     L.attt_lora_grad.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, vp, sz, vp]
+    L.attt_lora_sgd_step.restype = i32
+    L.attt_lora_sgd_step.argtypes = [ctypes.POINTER(LoraParam), i32, f32, i32, vp]
     L.attt_timing_enable.restype = i32
     L.attt_timing_enable.argtypes = [i32]
     L.attt_timing_reset.restype = i32
@@ -318,6 +325,28 @@ def lora_grad(problems, workspace=None):
     _check(L.attt_lora_workspace_size(arr, len(problems), dt, ctypes.byref(need)))
     ws = _workspace(need.value, problems[0]["x"].device, workspace)
     _check(L.attt_lora_grad(arr, len(problems), dt, _dptr(ws), ws.numel(), _stream_ptr()))
+
+
+def lora_sgd_step(params, lr, zero_grad=False):
+    """The adapter step theta <- theta - lr * grad (Eq. 2) on float32 parameters, in place.
+    Each entry: dict(param, grad[, param_bf16]) of equal numel; param and grad float32,
+    param_bf16 (optional) bfloat16, which receives the updated param rounded to nearest even.
+    With zero_grad the gradients are reset to 0 after they are read."""
+    L = load()
+    torch = _torch()
+    arr = (LoraParam * max(len(params), 1))()
+    for i, p in enumerate(params):
+        P, G, Pb = p["param"], p["grad"], p.get("param_bf16")
+        _dev(P, "param")
+        _dev(G, "grad")
+        if P.dtype != torch.float32 or G.dtype != torch.float32 or G.numel() != P.numel():
+            raise ValueError("param and grad must be float32 tensors of equal size")
+        if Pb is not None:
+            _dev(Pb, "param_bf16")
+            if Pb.dtype != torch.bfloat16 or Pb.numel() != P.numel():
+                raise ValueError("param_bf16 must be a bfloat16 tensor of the param's size")
+        arr[i] = LoraParam(_dptr(P), _dptr(G), _dptr(Pb), P.numel())
+    _check(L.attt_lora_sgd_step(arr, len(params), float(lr), 1 if zero_grad else 0, _stream_ptr()))
 
 
 # ------------------------------------------------------------------------------------------

@@ -48,7 +48,7 @@ namespace attt {
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_logit_exp", "ce_overflow_guard", "lora_u_du", "lora_dadb",
-    "lora_reduce", "ngram_set", "ngram_set_weight"};
+    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -902,4 +902,32 @@ extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t
   return lora_launch_all(
       red, [](const LoraRedJob& J) { return (int)ceil_div((int64_t)J.rank * J.d_in + (int64_t)J.d_out * J.rank, 256); },
       [&](const LoraRedBatch& b, int n) { return launch_lora_reduce(b, n, ws, s); }, "lora_reduce");
+}
+
+extern "C" attt_status attt_lora_sgd_step(const attt_lora_param* params, int32_t count, float lr,
+                                          int32_t zero_grad, void* stream) {
+  if (count < 0) return fail(ATTT_EINVAL, "lora_sgd: count must be >= 0");
+  if (count > 0 && !params) return fail(ATTT_EINVAL, "lora_sgd: params is null");
+  if (!std::isfinite(lr)) return fail(ATTT_EINVAL, "lora_sgd: lr is not finite");
+  std::vector<LoraSgdJob> jobs;
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_param& q = params[i];
+    if (q.n < 0) return fail(ATTT_EINVAL, "lora_sgd[%d]: n must be >= 0", i);
+    if (q.n >= ((int64_t)1 << 31)) return fail(ATTT_EUNSUPPORTED, "lora_sgd[%d]: n beyond this build's limits", i);
+    if (q.n == 0) continue;
+    if (!q.param || !q.grad) return fail(ATTT_EINVAL, "lora_sgd[%d]: param / grad is null", i);
+    if (reinterpret_cast<uintptr_t>(q.param) % 4 || reinterpret_cast<uintptr_t>(q.grad) % 4 ||
+        reinterpret_cast<uintptr_t>(q.param_bf16) % 2)
+      return fail(ATTT_EINVAL, "lora_sgd[%d]: misaligned array", i);
+    LoraSgdJob J{};
+    J.param = q.param;
+    J.grad = q.grad;
+    J.param_bf16 = static_cast<uint16_t*>(q.param_bf16);
+    J.n = q.n;
+    jobs.push_back(J);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return lora_launch_all(
+      jobs, [](const LoraSgdJob& J) { return (int)ceil_div(J.n, (int64_t)kLoraSgdPerBlock); },
+      [&](const LoraSgdBatch& b, int n) { return launch_lora_sgd(b, n, lr, zero_grad, s); }, "lora_sgd");
 }

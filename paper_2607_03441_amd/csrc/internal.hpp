@@ -25,6 +25,7 @@ enum KernelId {
   K_LORA_REDUCE,
   K_NGRAM_SET,
   K_NGRAM_SET_WEIGHT,
+  K_LORA_SGD,
   K_NUM_KERNELS
 };
 
@@ -252,6 +253,19 @@ using LoraP1Batch = LoraBatchOf<LoraP1Job>;
 using LoraP2Batch = LoraBatchOf<LoraP2Job>;
 using LoraRedBatch = LoraBatchOf<LoraRedJob>;
 using LoraBTBatch = LoraBatchOf<LoraBTJob>;
+
+// Adapter step: param [n] -= lr * grad [n] (float32), optional bf16 copy, optional grad reset.
+struct LoraSgdJob {
+  float* param;
+  float* grad;
+  uint16_t* param_bf16;  // nullable
+  int64_t n;
+  int32_t b_begin;
+  int32_t pad;
+};
+using LoraSgdBatch = LoraBatchOf<LoraSgdJob>;
+constexpr int kLoraSgdPerBlock = 1024;  // elements per workgroup (256 threads x 4)
+hipError_t launch_lora_sgd(const LoraSgdBatch& b, int blocks, float lr, int zero_grad, hipStream_t s);
 
 hipError_t launch_lora_bt(int dtype, const LoraBTBatch& b, int blocks, uint8_t* ws, hipStream_t s);
 // nt: the largest rank-tile count of the batch's jobs (bf16 kernels are specialised on it)

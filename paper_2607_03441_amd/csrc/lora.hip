@@ -328,6 +328,36 @@ __global__ __launch_bounds__(256) void lora_reduce_kernel(LoraRedBatch b, const 
 }
 
 // ------------------------------------------------------------------------------------------
+// Adapter step of Eq. 2: p <- p - lr g in float32, the product and the difference each rounded
+// to nearest (explicit roundings, no contraction into a fused multiply-add), then the bf16
+// copy (round to nearest even) and the gradient reset when asked. 1024 elements per workgroup.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void lora_sgd_kernel(LoraSgdBatch b, float lr, int zero_grad) {
+  const int ji = find_job(b, (int)blockIdx.x);
+  const LoraSgdJob J = b.j[ji];
+  const int64_t base = (int64_t)((int)blockIdx.x - J.b_begin) * kLoraSgdPerBlock;
+#pragma unroll
+  for (int u = 0; u < kLoraSgdPerBlock / 256; ++u) {
+    const int64_t i = base + u * 256 + threadIdx.x;
+    if (i < J.n) {
+#pragma clang fp contract(off)  // the product keeps its own rounding: no fused multiply-add
+      const float t = lr * J.grad[i];
+      const float p = J.param[i] - t;
+      J.param[i] = p;
+      if (J.param_bf16) J.param_bf16[i] = (uint16_t)f32_to_bf16_bits(p);
+      if (zero_grad) J.grad[i] = 0.0f;
+    }
+  }
+}
+
+hipError_t launch_lora_sgd(const LoraSgdBatch& b, int blocks, float lr, int zero_grad, hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
+  KernelTimer t(K_LORA_SGD, s);
+  hipLaunchKernelGGL(lora_sgd_kernel, dim3(blocks), dim3(256), 0, s, b, lr, zero_grad);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------
 hipError_t launch_lora_bt(int dtype, const LoraBTBatch& b, int blocks, uint8_t* ws, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   KernelTimer t(K_LORA_U, s);

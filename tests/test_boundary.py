@@ -137,6 +137,29 @@ def test_lora_validation(L):
     assert L.attt_lora_grad(arr, 1, 5, FAKE_WS, 1 << 30, None) == attt.EINVAL
 
 
+def _sgd(L, count=1, lr=0.5, **kw):
+    p = dict(param=FAKE, grad=ctypes.c_void_p(0x7F0000001000), param_bf16=None, n=100)
+    p.update(kw)
+    arr = (attt.LoraParam * 1)(attt.LoraParam(**p))
+    return L.attt_lora_sgd_step(arr, count, lr, 1, None)
+
+
+def test_lora_sgd_validation(L):
+    assert _sgd(L, lr=float("inf")) == attt.EINVAL
+    assert _sgd(L, lr=float("nan")) == attt.EINVAL
+    assert _sgd(L, count=-1) == attt.EINVAL
+    assert _sgd(L, n=-1) == attt.EINVAL
+    assert _sgd(L, param=None) == attt.EINVAL
+    assert _sgd(L, grad=None) == attt.EINVAL
+    assert _sgd(L, param=ctypes.c_void_p(0x7F0000000002)) == attt.EINVAL
+    assert _sgd(L, param_bf16=ctypes.c_void_p(0x7F0000000003)) == attt.EINVAL
+    assert _sgd(L, n=1 << 31) == attt.EUNSUPPORTED
+    assert L.attt_lora_sgd_step(None, 1, 0.5, 0, None) == attt.EINVAL
+    # nothing to do: no launch, no device access
+    assert _sgd(L, param=None, grad=None, n=0) == attt.OK
+    assert L.attt_lora_sgd_step(None, 0, 0.5, 0, None) == attt.OK
+
+
 def test_timing_api_without_launches(L):
     attt.timing_reset()
     assert attt.timing_read("ce_fwd_lse") == (0.0, 0)
