@@ -94,3 +94,18 @@ def test_lora_full_sampled(attt, wl):
         assert cosine(dA, dA_o) >= 0.999, p["name"]
         assert cosine(dB, dB_o) >= 0.999, p["name"]
         assert rel_norm(dA, dA_o) <= 2e-2 and rel_norm(dB, dB_o) <= 2e-2
+
+
+def test_ce_full_deterministic(attt, wl):
+    """The launch configuration the bench times, run twice on the same inputs: loss, lse and
+    dL/dh are bitwise identical (ordered reductions, no float atomics, no scratch)."""
+    cfg = wl.cfg
+    tok, ce = wl.tokens(), wl.ce()
+    _, w = ongram.ngram_weights(tok["history"], tok["updates"], cfg.n, cfg.w_min)
+    note(f"ce determinism {cfg.key}")
+    args = (dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]), dev_f32(w))
+    runs = []
+    for _ in range(2):
+        loss, lse, dH = attt.weighted_ce_fwd_bwd(*args, row_offsets=ce["row_offsets"])
+        runs.append((host(loss).tobytes(), host(lse).tobytes(), host(dH).tobytes()))
+    assert runs[0] == runs[1]
