@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c3", help="workload key c1..c5 (default: Llama-8B shape)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=2560,
+    ap.add_argument("--cpu-rows", type=int, default=5120,
                     help="CE rows the oracle sample covers (about 10 s of float64 work at the Llama-8B shape)")
     ap.add_argument("--hbm-calibrate", action="store_true",
                     help="only run a plain 1 GiB device copy, 4 times: the reference for scaling "
