@@ -209,6 +209,23 @@ def test_ce_bf16_overflow_guard_many_tiles(attt):
     _ce_case(attt, h, W, labels, weights, np.array([0, 1000, N], np.int64), True)
 
 
+def test_ce_bf16_overflow_guard_two_chunks(attt):
+    """The exact path when the vocabulary spans two chunks (131072 + 700 columns): its dH
+    accumulates float32 partials between the chunk launches, as the main path does."""
+    N, d, V = 96, 64, 131072 + 700
+    h = random_dense((N, d), 60.0, True, 37)
+    W = random_dense((V, d), 0.05, True, 38)
+    rng = np.random.default_rng(39)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    z = h.f32.astype(np.float64) @ W.f32.astype(np.float64).T
+    gap = z.max(1) - z[np.arange(N), labels]
+    assert np.sum(gap > 90) >= 10
+    del z
+    weights = rng.uniform(0.05, 1, N).astype(np.float32)
+    note("ce bf16 overflow guard, two vocabulary chunks")
+    _ce_case(attt, h, W, labels, weights, np.array([0, 40, N], np.int64), True)
+
+
 def test_ce_bf16_confident_labels(attt):
     """p_y within about 1e-5 of 1: the gradient rows are small differences, computed without
     cancellation (the label term is kept out of the sums)."""
