@@ -189,7 +189,7 @@ hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, c
 
 // ---- LoRA ------------------------------------------------------------------------------
 constexpr int kLoraRowTile = 128;  // row padding of the transposed pass-1 results
-constexpr int kLoraP1Rows = 32;    // pass-1 rows per workgroup
+constexpr int kLoraP1Rows = 64;    // pass-1 rows per workgroup (16 per wave)
 constexpr int kLoraKBlock = 128;   // pass-1 contraction step
 constexpr int kLoraColTile = 64;   // pass-2 output columns per workgroup
 constexpr int kLoraTStep = 64;     // pass-2 rows per step

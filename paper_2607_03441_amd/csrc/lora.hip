@@ -7,12 +7,12 @@
 // pass for all of them; dy differs per projection.
 //   B^T (lora_bt_kernel): B [d_out, r] -> B^T [r_pad, d_out] (zero rows past r), so both
 //     adapter operands are row-major [rank, k].
-//   Pass 1 (lora_p1_*): per 32 rows of x (or dy), s U^T = s (x A^T)^T (or s (dy B)^T) for all
-//     tiles of the job, on MFMA 16x16x32; the workgroup's four waves take a quarter of the
-//     contraction each. Operands are 16-byte loads in the MFMA's own k order (each instruction
-//     covers 64 contiguous bytes of 16 rows); the adapter fragments come from L2 straight into
-//     registers. The next step's rows are in flight while the current step's MFMAs run.
-//     Results are stored transposed ([16, rows_pad] per tile).
+//   Pass 1 (lora_p1_*): per 64 rows of x (or dy), s U^T = s (x A^T)^T (or s (dy B)^T) for all
+//     tiles of the job, on MFMA 16x16x32; each of the workgroup's four waves owns 16 rows over
+//     the whole contraction. Rows are 16-byte loads in the MFMA's own k order (each instruction
+//     covers 64 contiguous bytes of 16 rows), two steps in flight; the adapter operand slice of
+//     each step is staged once per workgroup in LDS and shared by its waves. Results are
+//     stored transposed ([16, rows_pad] per tile).
 //   Pass 2 (lora_p2_*): out[c, k] = sum_t L[c, t] src[t, k] with (L, src) = (s dU^T, x) for dA
 //     and (s U^T, dy) for dB. The contraction runs over rows, the slow index of src, so 64-row
 //     x 64-column tiles of src are written transposed into LDS (two rows per 32-bit store,
@@ -56,107 +56,111 @@ __global__ __launch_bounds__(256) void lora_bt_kernel(LoraBTBatch b, uint8_t* __
 // ------------------------------------------------------------------------------------------
 constexpr uint32_t kOOB = 0x7FFFFFF0u;  // offset past every descriptor's range: loads return 0
 
-// A workgroup takes 32 rows; its four waves split the contraction into four ranges and their
-// partial sums meet in LDS, so each wave's chain of dependent loads is a quarter as long.
-// NT is the largest tile count of the batch; a job with fewer tiles skips the rest.
+// A workgroup takes kLoraP1Rows = 64 rows, each of its four waves 16 of them over the whole
+// contraction. The rank tiles' operand slices of every 128-wide step ([16, 128] per tile) are
+// loaded once per workgroup into LDS (double-buffered, rows padded to kP1Pitch elements so the
+// sixteen rows one fragment read touches fall in distinct banks) and shared by the four waves,
+// so the operand traffic from L2 is a quarter of what per-wave fragment loads would cost. The
+// rows of step s+2 are in flight while step s runs. NT is the largest tile count of the batch;
+// a job with fewer tiles skips the rest.
+constexpr int kP1Pitch = kLoraKBlock + 8;
+static_assert(kLoraP1Rows == 64, "four waves of 16 rows");
+
 template <int NT>
 __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_t* __restrict__ ws) {
   const int ji = find_job(b, (int)blockIdx.x);
   const LoraP1Job& Jr = b.j[ji];
   const int rt = (int)blockIdx.x - Jr.b_begin;
   const int kdim = Jr.kdim, nt = Jr.nt;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
-  constexpr int RG = kLoraP1Rows / 16;  // groups of 16 rows
-  // this workgroup's rows; rows past the input read as zero through the descriptor range
-  const int row0 = rt * kLoraP1Rows;
-  const int nrows = max(0, min(kLoraP1Rows, Jr.rows - row0));
-  const bf16_t* src = static_cast<const bf16_t*>(Jr.src) + (int64_t)row0 * kdim;
+  // this wave's 16 rows; rows past the input read as zero through the descriptor range
+  const int row0 = rt * kLoraP1Rows + wave * 16;
+  const int nrows = max(0, min(16, Jr.rows - row0));
+  const bf16_t* src = static_cast<const bf16_t*>(Jr.src) + (int64_t)min(row0, Jr.rows) * kdim;
   const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, nrows * kdim * 2);
   __amdgpu_buffer_rsrc_t ro[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
     ro[t] = buffer_rsrc(t < nt ? Jr.t[t].op : src, t < nt ? Jr.t[t].valid * kdim * 2 : 0);
-  // this wave's contraction range, in whole pairs of steps
-  const int kq = ((kdim + 4 * 2 * kLoraKBlock - 1) / (4 * 2 * kLoraKBlock)) * 2 * kLoraKBlock;
-  const int kbeg = wave * kq, kend = min(kdim, kbeg + kq);
+  __shared__ __align__(16) bf16_t opl[2][NT][16 * kP1Pitch];
+  const int ns = (kdim + kLoraKBlock - 1) / kLoraKBlock;
 
-  f32x4 acc[RG][NT];
+  // operand staging: thread -> operand row sr, 16-byte chunk sc of the step's 128 columns
+  const int sr = tid >> 4, sc = tid & 15;
+  u32x4 stg[NT];
+  auto stage_load = [&](int s) {
+    const int k = s * kLoraKBlock + sc * 8;
 #pragma unroll
-  for (int a = 0; a < RG; ++a)
+    for (int t = 0; t < NT; ++t)
+      if (t < nt)
+        stg[t] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(ro[t], k < kdim ? (uint32_t)(sr * kdim + k) * 2u : kOOB, 0, 0));
+  };
+  auto stage_store = [&](int buf) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc[a][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // Step kb: for MFMA q, lane (l16, g) holds rows a*16 + l16 at k = kb + q*32 + g*8 .. +7 (the
-  // MFMA's own k order; one load instruction covers 64 contiguous bytes of 16 rows), and for
-  // every tile the adapter row l16 at the same k. k at or past kend reads as zero.
-  auto load = [&](int kb, u32x4 (&xa)[RG][4], u32x4 (&oa)[NT][4]) {
+    for (int t = 0; t < NT; ++t)
+      if (t < nt) *reinterpret_cast<u32x4*>(&opl[buf][t][sr * kP1Pitch + sc * 8]) = stg[t];
+  };
+  // Step s of the rows: for MFMA q, lane (l16, g) holds row l16 at k = 128 s + 32 q + 8 g .. +7
+  // (the MFMA's own k order; one load instruction covers 64 contiguous bytes of 16 rows); k at
+  // or past kdim reads as zero.
+  auto xload = [&](int s, u32x4 (&xa)[4]) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int k = kb + q * 32 + g * 8;
-      const bool kin = k < kend;
-#pragma unroll
-      for (int a = 0; a < RG; ++a)
-        xa[a][q] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, kin ? (uint32_t)((a * 16 + l16) * kdim + k) * 2u : kOOB, 0, 0));
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        oa[t][q] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(ro[t], kin ? (uint32_t)(l16 * kdim + k) * 2u : kOOB, 0, 0));
+      const int k = s * kLoraKBlock + q * 32 + g * 8;
+      xa[q] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, k < kdim ? (uint32_t)(l16 * kdim + k) * 2u : kOOB, 0, 0));
     }
   };
-  auto mma = [&](const u32x4 (&xa)[RG][4], const u32x4 (&oa)[NT][4]) {
+  f32x4 acc[NT];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+  for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](int buf, const u32x4 (&xa)[4]) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        if (t >= nt) break;
+    for (int t = 0; t < NT; ++t) {
+      if (t >= nt) break;
 #pragma unroll
-        for (int a = 0; a < RG; ++a)
-          acc[a][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[a][q]),
-                                                              __builtin_bit_cast(bf16x8, oa[t][q]), acc[a][t], 0, 0, 0);
+      for (int q = 0; q < 4; ++q) {
+        const u32x4 o = *reinterpret_cast<const u32x4*>(&opl[buf][t][l16 * kP1Pitch + q * 32 + g * 8]);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, xa[q]),
+                                                         __builtin_bit_cast(bf16x8, o), acc[t], 0, 0, 0);
       }
-  };
-  u32x4 xa0[RG][4], oa0[NT][4], xa1[RG][4], oa1[NT][4];
-  if (kbeg < kend) {
-    load(kbeg, xa0, oa0);
-    for (int kb = kbeg; kb < kend; kb += 2 * kLoraKBlock) {
-      load(kb + kLoraKBlock, xa1, oa1);  // past kend: zeros
-      mma(xa0, oa0);
-      load(kb + 2 * kLoraKBlock, xa0, oa0);
-      mma(xa1, oa1);
     }
-  }
-  // waves 1-3 hand their sums to wave 0 through LDS (fixed order: wave 0 + 1 + 2 + 3)
-  __shared__ f32x4 red[3][RG * NT][64];
-  if (wave > 0) {
-#pragma unroll
-    for (int a = 0; a < RG; ++a)
-#pragma unroll
-      for (int t = 0; t < NT; ++t) red[wave - 1][a * NT + t][lane] = acc[a][t];
-  }
+  };
+  u32x4 x0[4], x1[4];
+  stage_load(0);
+  xload(0, x0);
+  if (ns > 1) xload(1, x1);
+  stage_store(0);
   __syncthreads();
-  if (wave != 0) return;
-#pragma unroll
-  for (int w = 0; w < 3; ++w)
-#pragma unroll
-    for (int a = 0; a < RG; ++a)
-#pragma unroll
-      for (int t = 0; t < NT; ++t) acc[a][t] += red[w][a * NT + t][lane];
+  // Step s: the operand stage of s+1 in flight, the MFMAs of step s (LDS buffer s&1, rows
+  // loaded two steps earlier), the rows of step s+2 into the registers just consumed, then
+  // the stage of s+1 into the other buffer and one barrier. That buffer was last read in step
+  // s-1, before the previous barrier.
+  auto step = [&](int s, u32x4 (&xa)[4]) {
+    if (s + 1 < ns) stage_load(s + 1);
+    mma(s & 1, xa);
+    if (s + 2 < ns) xload(s + 2, xa);
+    if (s + 1 < ns) stage_store((s + 1) & 1);
+    __syncthreads();
+  };
+  for (int s = 0; s < ns; s += 2) {
+    step(s, x0);
+    if (s + 1 < ns) step(s + 1, x1);
+  }
   // D of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16.
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t >= nt) break;
     bf16_t* outT = reinterpret_cast<bf16_t*>(ws + Jr.t[t].out_off);
-    const float s = Jr.t[t].scale;
-#pragma unroll
-    for (int a = 0; a < RG; ++a) {
-      const int r = row0 + a * 16 + g * 4;
-      uint2 pk;
-      pk.x = pack_bf16x2(s * acc[a][t][0], s * acc[a][t][1]);
-      pk.y = pack_bf16x2(s * acc[a][t][2], s * acc[a][t][3]);
-      *reinterpret_cast<uint2*>(outT + (int64_t)l16 * Jr.rows_pad + r) = pk;
-    }
+    const float scale = Jr.t[t].scale;
+    const int r = row0 + g * 4;
+    uint2 pk;
+    pk.x = pack_bf16x2(scale * acc[t][0], scale * acc[t][1]);
+    pk.y = pack_bf16x2(scale * acc[t][2], scale * acc[t][3]);
+    *reinterpret_cast<uint2*>(outT + (int64_t)l16 * Jr.rows_pad + r) = pk;
   }
 }
 
