@@ -952,29 +952,35 @@ __global__ __launch_bounds__(256) void ce_guard_row_reduce_kernel(
   ce_row_reduce_body(b, partials, n_vb, label_logit, weights, lse, coef, rowloss);
 }
 
+// One 1024-thread workgroup per episode: every thread sums its rows in order (loads issued
+// eight at a time), then the waves' sums meet in a fixed order.
+constexpr int kLossThreads = 1024;
 __device__ __forceinline__ void ce_loss_body(
     CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss) {
   const CeEp E = b.e[blockIdx.x];
   double acc = 0.0;
-  for (int i = threadIdx.x; i < E.L; i += blockDim.x) acc += (double)rowloss[E.row0 + i];
+#pragma unroll 8
+  for (int i = threadIdx.x; i < E.L; i += kLossThreads) acc += (double)rowloss[E.row0 + i];
   acc = wave_sum_f64(acc);
-  __shared__ double part[4];
+  constexpr int kWaves = kLossThreads / 64;
+  __shared__ double part[kWaves];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (lane == 0) part[wave] = acc;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const double t = (part[0] + part[1]) + (part[2] + part[3]);
+    double t = 0.0;
+    for (int w = 0; w < kWaves; ++w) t += part[w];
     loss[b.first + blockIdx.x] = E.L > 0 ? (float)(t / (double)E.L) : 0.0f;
   }
 }
 
-__global__ __launch_bounds__(256) void ce_loss_kernel(
+__global__ __launch_bounds__(kLossThreads) void ce_loss_kernel(
     CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss) {
   ce_loss_body(b, rowloss, loss);
 }
 
 // The same kernel launched by the overflow guard: returns at once unless *gate != 0.
-__global__ __launch_bounds__(256) void ce_guard_loss_kernel(
+__global__ __launch_bounds__(kLossThreads) void ce_guard_loss_kernel(
     CeEpBatch b, const float* __restrict__ rowloss, float* __restrict__ loss,
     const int* __restrict__ gate) {
   if (*gate == 0) return;
@@ -1096,9 +1102,9 @@ hipError_t launch_ce_loss(const CeEpBatch& b, const float* rowloss, float* loss,
   if (b.count <= 0) return hipSuccess;
   KernelTimer t(gate ? K_CE_GUARD : K_CE_LOSS, s);
   if (gate)
-    hipLaunchKernelGGL(ce_guard_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss, gate);
+    hipLaunchKernelGGL(ce_guard_loss_kernel, dim3(b.count), dim3(kLossThreads), 0, s, b, rowloss, loss, gate);
   else
-    hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(256), 0, s, b, rowloss, loss);
+    hipLaunchKernelGGL(ce_loss_kernel, dim3(b.count), dim3(kLossThreads), 0, s, b, rowloss, loss);
   return hipGetLastError();
 }
 
