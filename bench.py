@@ -250,7 +250,9 @@ def gpu_hold(torch, calls):
     """Keep the GPU busy (torch.cuda._sleep, ~1 ms per 2e6 cycles) while `calls` small calls are
     queued behind it, so the launch events around each kernel measure the kernel and not the
     host between calls."""
-    torch.cuda._sleep(int(max(2e7, 1e6 * calls)))
+    sleep = getattr(torch.cuda, "_sleep", None)
+    if sleep is not None:
+        sleep(int(max(2e7, 1e6 * calls)))
 
 
 def lora_sgd_part(step, attt, torch, reps):
