@@ -306,7 +306,8 @@ __global__ __launch_bounds__(256) void lora_p2_f32_kernel(LoraP2Batch b, uint8_t
 
 // ------------------------------------------------------------------------------------------
 // Ordered reduction of the split partials into dA, dB (+=). Partials of rank c of a problem
-// live in its tile c/16: [tile][split][16][cols].
+// live in its tile c/16: [tile][split][16][cols]. The split loop is unrolled so its loads are
+// in flight together; the additions keep their order.
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void lora_reduce_kernel(LoraRedBatch b, const uint8_t* __restrict__ ws) {
   const int ji = find_job(b, (int)blockIdx.x);
@@ -318,6 +319,7 @@ __global__ __launch_bounds__(256) void lora_reduce_kernel(LoraRedBatch b, const 
     const float* p = reinterpret_cast<const float*>(ws + J.pa_off) +
                      ((int64_t)(c >> 4) * J.sa * 16 + (c & 15)) * J.d_in + k;
     float s = 0.0f;
+#pragma unroll 8
     for (int sp = 0; sp < J.sa; ++sp) s += p[(int64_t)sp * 16 * J.d_in];
     J.dA[idx] += s;
   } else if (idx < na + nb) {
@@ -326,6 +328,7 @@ __global__ __launch_bounds__(256) void lora_reduce_kernel(LoraRedBatch b, const 
     const float* p = reinterpret_cast<const float*>(ws + J.pb_off) +
                      ((int64_t)(c >> 4) * J.sb * 16 + (c & 15)) * J.d_out + o;
     float s = 0.0f;
+#pragma unroll 8
     for (int sp = 0; sp < J.sb; ++sp) s += p[(int64_t)sp * 16 * J.d_out];
     J.dB[i2] += s;
   }
