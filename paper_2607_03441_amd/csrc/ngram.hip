@@ -238,6 +238,7 @@ __global__ __launch_bounds__(1024) void ngram_weight_kernel(NgramEpBatch batch, 
       const int p = s / kQMax;
       const uint16_t* col = partial + ((int64_t)E.chunk_base + (int64_t)p * E.chunks) * kQMax + (s - p * kQMax);
       int ch = grp;
+#pragma unroll 4
       for (; ch + 12 < E.chunks; ch += 16) {
         a0 += col[(int64_t)ch * kQMax];
         a1 += col[(int64_t)(ch + 4) * kQMax];
