@@ -140,34 +140,71 @@ attt_status attt_ngram_set_weights(void* const* sets, const int32_t* tokens, con
  * Row t of `hidden` is the hidden state that predicts token labels[t]; weights[t] is that
  * token's weight w. Rows are grouped into E episodes by row_offsets; episode e has
  * L_e = row_offsets[e+1] - row_offsets[e] rows and
- *     z_t    = W h_t                                   (logits, never written to memory)
+ *     z_t    = W h_t                                   (logits)
  *     lse_t  = log sum_v exp(z_tv)
  *     loss_e = (1 / L_e) sum_{t in e} w_t (lse_t - z_{t, labels[t]})
  *     dL/dh_t = (w_t / L_e) (softmax(z_t) - onehot(labels[t])) W
  * Natural log, full softmax over V, no bias, no label smoothing; the head gets no gradient.
+ * The logits z are never written to memory, and the bf16 backward holds no buffer of (rows x
+ * vocabulary) at all: one persistent kernel computes 256 x 256 tiles of the softmax numerators
+ * e_tv = exp(z_tv - z_{t,labels[t]}) and, on other CUs of the same XCD, contracts them with W as
+ * they arrive through a ring of a few MB in the workspace (dL/dh is a per-row scale of
+ * sum_v e_tv W_v minus the label term). It needs the MI355X layout of 256 CUs in 8 XCDs and
+ * cooperative launch (ATTT_EUNSUPPORTED otherwise). The float32 backward stages dL/dz for blocks
+ * of at most 8192 rows x 131072 columns in the workspace.
  *
  * hidden       device [N, d] of dtype
  * lm_head      device [V, d] of dtype (the nn.Linear weight layout)
  * labels       device int32 [N], each in [0, V); a label outside that range is not an error
- *              the host can see: the bf16 path makes that row's loss term NaN (and, with
- *              grad_hidden, its lse and its gradient row), and never reads W at that label
+ *              the host can see: that row's loss term becomes NaN (and, with grad_hidden, its
+ *              gradient row; on the bf16 path also its lse), and W is never read at that label
  * weights      device float [N]
  * row_offsets  HOST int64 [E+1], from 0 to N, non-decreasing; NULL means one episode of N rows
  * num_episodes E >= 1
- * N, d, V      N >= 0, 1 <= d with d % 8 == 0, 1 <= V < 2^31
+ * N, d, V      N >= 0, 1 <= d < 2^20 with d % 8 == 0, 1 <= V < 2^31; the bf16 backward needs
+ *              V <= 2^21 - 256 (ATTT_EUNSUPPORTED beyond)
  * dtype        ATTT_F32 or ATTT_BF16
  * loss         device float [E]
  * lse          device float [N] or NULL
  * grad_hidden  device [N, d] of dtype, or NULL for the forward only
- * The workspace query takes want_grad = (grad_hidden != NULL).
+ * The workspace query takes flags: ATTT_CE_WANT_GRAD when grad_hidden is passed, plus
+ * ATTT_CE_HEAD_T when the call is given a prepared transposed head (attt_weighted_ce_fwd_bwd_ex).
  * ------------------------------------------------------------------------------------ */
-attt_status attt_ce_workspace_size(int64_t N, int64_t d, int64_t V, int32_t dtype, int32_t want_grad,
+#define ATTT_CE_WANT_GRAD 1
+#define ATTT_CE_HEAD_T 2
+attt_status attt_ce_workspace_size(int64_t N, int64_t d, int64_t V, int32_t dtype, int32_t flags,
                                    size_t* bytes);
 attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* lm_head, const int32_t* labels,
                                      const float* weights, const int64_t* row_offsets,
                                      int32_t num_episodes, int64_t N, int64_t d, int64_t V,
                                      int32_t dtype, float* loss, float* lse, void* grad_hidden,
                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Diagnostics: bounds (microseconds) of every wait inside the persistent bf16 backward, for its
+ * label-referenced pass and for its exact pass (defaults 20000 each; both >= 0). A wait that runs
+ * out aborts that pass: the label-referenced pass then falls back to the exact pass; an aborted
+ * exact pass makes loss, lse and dL/dh NaN. Tests set tiny bounds to drive these paths. Applies
+ * to later calls in the process; not synchronised against concurrent calls. */
+attt_status attt_ce_set_wait_limit(int64_t label_us, int64_t exact_us);
+
+/* The frozen head, transposed once (Sec. 3.1: only the episode's adapter is trained, so the
+ * LM head of Eq. 10 is the same matrix in every update of every episode). The bf16 backward
+ * contracts dL/dz with W over the vocabulary and reads W as W^T [d, Vp] (Vp = V rounded up to
+ * 256, columns V .. Vp-1 zero) so that both GEMM operands are contiguous along the contraction.
+ * attt_weighted_ce_fwd_bwd builds that copy in its workspace on every call;
+ * attt_ce_head_transpose builds it once into a caller-owned buffer of attt_ce_head_t_size
+ * bytes (16-byte aligned), and attt_weighted_ce_fwd_bwd_ex reads it from there (lm_head_t,
+ * bf16 with grad_hidden only; NULL = build it in the workspace as the plain call does). The
+ * buffer stays valid while lm_head is unchanged. */
+attt_status attt_ce_head_t_size(int64_t d, int64_t V, size_t* bytes);
+attt_status attt_ce_head_transpose(const void* lm_head, int64_t d, int64_t V, void* lm_head_t,
+                                   size_t lm_head_t_bytes, void* stream);
+attt_status attt_weighted_ce_fwd_bwd_ex(const void* hidden, const void* lm_head, const void* lm_head_t,
+                                        const int32_t* labels, const float* weights,
+                                        const int64_t* row_offsets, int32_t num_episodes, int64_t N,
+                                        int64_t d, int64_t V, int32_t dtype, float* loss, float* lse,
+                                        void* grad_hidden, void* workspace, size_t workspace_bytes,
+                                        void* stream);
 
 /* --------------------------------------------------------------------------------------
  * LoRA adapter gradients (episode-specific adapter, Sec. 3.1; rank and alpha, Appendix C).
@@ -186,7 +223,7 @@ attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* lm_head, co
  *   dA     device float [rank, d_in]   (+=)
  *   dB     device float [d_out, rank]  (+=)
  *   rows >= 0, d_in and d_out >= 1 and multiples of 8, 1 <= rank <= ATTT_LORA_MAX_RANK;
- *   rows < 2^30 and d_in, d_out < 2^20 (ATTT_EUNSUPPORTED beyond)
+ *   rows < 2^24 and d_in, d_out < 2^20 (ATTT_EUNSUPPORTED beyond)
  *   Outputs of different problems must not overlap. Problems with the same x pointer, d_in
  *   and rows (the q, k and v projections of one layer) are computed together, x being read
  *   once per pass for up to 64 of their combined (16-padded) ranks.

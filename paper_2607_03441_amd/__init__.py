@@ -13,12 +13,14 @@ import numpy as np
 
 __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_workspace_size",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
-           "weighted_ce_fwd_bwd", "ce_workspace_size", "lora_grad", "lora_workspace_size", "lora_sgd_step",
+           "weighted_ce_fwd_bwd", "ce_workspace_size", "ce_head_t_size", "ce_head_transpose", "lora_grad", "lora_workspace_size", "lora_sgd_step",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
            "F32", "BF16", "LoraProblem", "LoraParam"]
 
 F32 = 0
 BF16 = 1
+CE_WANT_GRAD = 1
+CE_HEAD_T = 2
 OK, EINVAL, ENOSPACE, EUNSUPPORTED, EHIP = range(5)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -83,6 +85,15 @@ def load():
     L.attt_weighted_ce_fwd_bwd.restype = i32
     L.attt_weighted_ce_fwd_bwd.argtypes = [vp, vp, vp, vp, p64, i32, i64, i64, i64, i32, vp, vp, vp,
                                            vp, sz, vp]
+    L.attt_weighted_ce_fwd_bwd_ex.restype = i32
+    L.attt_weighted_ce_fwd_bwd_ex.argtypes = [vp, vp, vp, vp, vp, p64, i32, i64, i64, i64, i32, vp, vp, vp,
+                                              vp, sz, vp]
+    L.attt_ce_set_wait_limit.restype = i32
+    L.attt_ce_set_wait_limit.argtypes = [i64, i64]
+    L.attt_ce_head_t_size.restype = i32
+    L.attt_ce_head_t_size.argtypes = [i64, i64, psz]
+    L.attt_ce_head_transpose.restype = i32
+    L.attt_ce_head_transpose.argtypes = [vp, i64, i64, vp, sz, vp]
     L.attt_lora_workspace_size.restype = i32
     L.attt_lora_workspace_size.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, psz]
     L.attt_lora_grad.restype = i32
@@ -246,17 +257,49 @@ def ngram_set_weights(sets, tokens, token_offsets, capacity, n, w_min=0.05, want
 
 
 # ------------------------------------------------------------------------------------------
-def ce_workspace_size(N, d, V, dtype, want_grad=True):
+def ce_workspace_size(N, d, V, dtype, want_grad=True, head_t=False):
     L = load()
     out = ctypes.c_size_t(0)
-    _check(L.attt_ce_workspace_size(N, d, V, dtype, 1 if want_grad else 0, ctypes.byref(out)))
+    flags = (CE_WANT_GRAD if want_grad else 0) | (CE_HEAD_T if head_t else 0)
+    _check(L.attt_ce_workspace_size(N, d, V, dtype, flags, ctypes.byref(out)))
     return out.value
 
 
+def ce_set_wait_limit(label_us=20000, exact_us=20000):
+    """Bounds of the waits inside the persistent bf16 backward (diagnostics; defaults restore)."""
+    _check(load().attt_ce_set_wait_limit(int(label_us), int(exact_us)))
+
+
+def ce_head_t_size(d, V):
+    L = load()
+    out = ctypes.c_size_t(0)
+    _check(L.attt_ce_head_t_size(int(d), int(V), ctypes.byref(out)))
+    return out.value
+
+
+def ce_head_transpose(lm_head, out=None):
+    """The frozen bf16 LM head [V, d] transposed once into the layout the bf16 backward reads
+    (uint8 device tensor of ce_head_t_size bytes); pass it as lm_head_t= to weighted_ce_fwd_bwd."""
+    torch = _torch()
+    L = load()
+    _dev(lm_head, "lm_head")
+    if lm_head.dtype != torch.bfloat16:
+        raise TypeError("the transposed head is for the bf16 backward")
+    V, d = lm_head.shape
+    nbytes = ce_head_t_size(d, V)
+    if out is None:
+        out = torch.empty(nbytes, dtype=torch.uint8, device=lm_head.device)
+    _dev(out, "out")
+    _check(L.attt_ce_head_transpose(_dptr(lm_head), d, V, _dptr(out), out.numel() * out.element_size(),
+                                    _stream_ptr()))
+    return out
+
+
 def weighted_ce_fwd_bwd(hidden, lm_head, labels, weights, row_offsets=None, want_grad=True,
-                        want_lse=True, workspace=None, out=None):
+                        want_lse=True, workspace=None, out=None, lm_head_t=None):
     """Eq. 10 forward and backward. hidden [N, d], lm_head [V, d] (float32 or bfloat16),
     labels int32 [N], weights float32 [N]; row_offsets: host int64 [E+1] or None (one episode).
+    lm_head_t: the head prepared by ce_head_transpose (bf16 backward only) or None.
     Returns (loss [E], lse [N] or None, grad_hidden [N, d] or None)."""
     torch = _torch()
     L = load()
@@ -283,12 +326,15 @@ def weighted_ce_fwd_bwd(hidden, lm_head, labels, weights, row_offsets=None, want
         loss = torch.empty(E, dtype=torch.float32, device=dev)
         lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
         grad = torch.empty_like(hidden) if want_grad else None
+    if lm_head_t is not None:
+        _dev(lm_head_t, "lm_head_t")
     need = ctypes.c_size_t(0)
-    _check(L.attt_ce_workspace_size(N, d, V, dt, 1 if grad is not None else 0, ctypes.byref(need)))
+    flags = (CE_WANT_GRAD if grad is not None else 0) | (CE_HEAD_T if lm_head_t is not None else 0)
+    _check(L.attt_ce_workspace_size(N, d, V, dt, flags, ctypes.byref(need)))
     ws = _workspace(need.value, dev, workspace)
-    _check(L.attt_weighted_ce_fwd_bwd(_dptr(hidden), _dptr(lm_head), _dptr(labels), _dptr(weights),
-                                      rp, E, N, d, V, dt, _dptr(loss), _dptr(lse), _dptr(grad),
-                                      _dptr(ws), ws.numel(), _stream_ptr()))
+    _check(L.attt_weighted_ce_fwd_bwd_ex(_dptr(hidden), _dptr(lm_head), _dptr(lm_head_t), _dptr(labels),
+                                         _dptr(weights), rp, E, N, d, V, dt, _dptr(loss), _dptr(lse),
+                                         _dptr(grad), _dptr(ws), ws.numel(), _stream_ptr()))
     return loss, lse, grad
 
 

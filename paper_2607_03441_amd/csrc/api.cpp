@@ -47,8 +47,8 @@ namespace attt {
 
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
-    "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_logit_exp", "ce_overflow_guard", "lora_u_du", "lora_dadb",
-    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd"};
+    "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard", "lora_u_du", "lora_dadb",
+    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -235,28 +235,49 @@ extern "C" attt_status attt_ngram_workspace_size(const int64_t* history_offsets,
   return ATTT_OK;
 }
 
+namespace {
+attt_status ngram_check_args(const int32_t* history, const int64_t* history_offsets, const int32_t* tokens,
+                             const int64_t* token_offsets, int32_t num_episodes, int32_t n, float w_min,
+                             float* weights) {
+  attt_status st = ngram_validate(history_offsets, token_offsets, num_episodes, n);
+  if (st) return st;
+  if (!(w_min >= 0x1p-20f && w_min <= 1.0f))
+    return fail(ATTT_EINVAL, "ngram: w_min must be in [2^-20, 1] (got %g)", (double)w_min);
+  const int64_t T = token_offsets[num_episodes];
+  if (T > 0 && !tokens) return fail(ATTT_EINVAL, "ngram: tokens is null");
+  if (T > 0 && !weights) return fail(ATTT_EINVAL, "ngram: weights is null");
+  if (history_offsets[num_episodes] > 0 && !history) return fail(ATTT_EINVAL, "ngram: history is null");
+  return ATTT_OK;
+}
+
+attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t* tokens, int32_t E,
+                      int32_t n, float w_min, uint32_t* exposure, float* weights, void* workspace,
+                      hipStream_t s);
+}  // namespace
+
 extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_offsets,
                                           const int32_t* tokens, const int64_t* token_offsets,
                                           int32_t num_episodes, int32_t n, float w_min,
                                           uint32_t* exposure, float* weights, void* workspace,
                                           size_t workspace_bytes, void* stream) {
-  attt_status st = ngram_validate(history_offsets, token_offsets, num_episodes, n);
+  attt_status st = ngram_check_args(history, history_offsets, tokens, token_offsets, num_episodes, n, w_min,
+                                    weights);
   if (st) return st;
-  if (!(w_min >= 0x1p-20f && w_min <= 1.0f))
-    return fail(ATTT_EINVAL, "ngram: w_min must be in [2^-20, 1] (got %g)", (double)w_min);
-  const int32_t E = num_episodes;
-  const int64_t T = token_offsets[E];
-  if (T > 0 && !tokens) return fail(ATTT_EINVAL, "ngram: tokens is null");
-  if (T > 0 && !weights) return fail(ATTT_EINVAL, "ngram: weights is null");
-  if (history_offsets[E] > 0 && !history) return fail(ATTT_EINVAL, "ngram: history is null");
-  NgramPlan P = ngram_plan(history_offsets, token_offsets, E, n);
+  NgramPlan P = ngram_plan(history_offsets, token_offsets, num_episodes, n);
   if (workspace_bytes < P.total)
     return fail(ATTT_ENOSPACE, "ngram: workspace %zu bytes, need %zu", workspace_bytes, P.total);
   if (!workspace) return fail(ATTT_EINVAL, "ngram: workspace is null");
   if (!aligned256(workspace)) return fail(ATTT_EINVAL, "ngram: workspace must be 256-byte aligned");
-  if (T == 0) return ATTT_OK;
+  if (token_offsets[num_episodes] == 0) return ATTT_OK;
+  return ngram_run(P, history, tokens, num_episodes, n, w_min, exposure, weights, workspace,
+                   static_cast<hipStream_t>(stream));
+}
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t* tokens, int32_t E,
+                      int32_t n, float w_min, uint32_t* exposure, float* weights, void* workspace,
+                      hipStream_t s) {
+
   uint16_t* partial = static_cast<uint16_t*>(workspace);
 
   // count kernel: batches of partitions; a partition's chunks are consecutive blocks
@@ -312,6 +333,7 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
   }
   return ATTT_OK;
 }
+}  // namespace
 
 // ------------------------------------------------------------------------------------------
 // Persistent n-gram sets
@@ -434,19 +456,18 @@ extern "C" attt_status attt_ngram_set_weights(void* const* sets, const int32_t* 
 // ------------------------------------------------------------------------------------------
 namespace {
 
-// Backward blocking: rows per block and vocab columns per chunk. A chunk's staged exponentials
-// take R x Vc x 2 bytes (2 GiB at 8192 x 131072): HBM has room, and one chunk over the whole
-// vocabulary (V <= 131072) saves the float32 dH partials between chunks and launches.
+// float32 backward (three VALU GEMMs) blocking: rows per block and vocab columns per staged dZ
+// chunk. The bf16 backward stages nothing of that shape (ce_fused.hip).
 constexpr int64_t kCeRowBlock = 8192;
 constexpr int64_t kCeVocabChunk = 131072;
-constexpr int64_t kCeExpLaunch = 32768;  // columns per launch of the first GEMM (multiple of 256)
 
 struct CePlan {
-  CeGemmShape fwd{64, 64}, lexp{64, 64}, dz{64, 64}, dh{64, 64};
-  int64_t n_vb = 0, n_vb_exp = 0, R = 0, Vc = 0, Vp = 0;
+  CeGemmShape fwd{64, 64};
+  int64_t n_vb = 0, nv = 0, R = 0, Vc = 0, Vp = 0;
+  int slices = 0, consumers = 0, passes = 0, slots = 0, items_max = 0, sync_ints = 0;
   size_t off_part = 0, off_label = 0, off_lse = 0, off_coef = 0, off_rowloss = 0;
-  size_t off_sa = 0, off_sb = 0, off_flag = 0;
-  size_t off_wt = 0, off_dz = 0, off_acc = 0, total = 0;
+  size_t off_flag = 0, off_sync = 0, off_sync2 = 0, off_ring = 0;
+  size_t off_wt = 0, off_dz = 0, total = 0;
 };
 
 CeGemmShape mfma_shape(int64_t rows, int64_t cols) {
@@ -454,26 +475,27 @@ CeGemmShape mfma_shape(int64_t rows, int64_t cols) {
   return big >= 512 ? CeGemmShape{256, 256} : CeGemmShape{128, 128};
 }
 
-attt_status ce_validate(int64_t N, int64_t d, int64_t V, int32_t dtype) {
+// Largest V of the bf16 backward: the dH GEMM reads 256 rows of the transposed head [d, Vp]
+// through one buffer descriptor of 1 GiB, so 256 * Vp * 2 bytes must stay below 2^30.
+constexpr int64_t kCeMaxVBf16Grad = ((int64_t)1 << 21) - 256;
+
+attt_status ce_validate(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
   if (dtype != ATTT_F32 && dtype != ATTT_BF16) return fail(ATTT_EINVAL, "ce: unknown dtype %d", dtype);
   if (N < 0) return fail(ATTT_EINVAL, "ce: N must be >= 0 (got %lld)", (long long)N);
   if (d < 1 || d % 8 != 0) return fail(ATTT_EINVAL, "ce: d must be a positive multiple of 8 (got %lld)", (long long)d);
   if (V < 1) return fail(ATTT_EINVAL, "ce: V must be >= 1 (got %lld)", (long long)V);
   if (N >= ((int64_t)1 << 31) || V >= ((int64_t)1 << 31) || d >= ((int64_t)1 << 20))
     return fail(ATTT_EUNSUPPORTED, "ce: dimensions beyond this build's limits");
+  if (dtype == ATTT_BF16 && grad && V > kCeMaxVBf16Grad)
+    return fail(ATTT_EUNSUPPORTED, "ce: the bf16 backward supports V <= %lld (got %lld)",
+                (long long)kCeMaxVBf16Grad, (long long)V);
   return ATTT_OK;
 }
 
-CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
+CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad, bool have_head_t) {
   CePlan P;
-  const size_t esz = dtype == ATTT_BF16 ? 2 : 4;
   if (dtype == ATTT_BF16) {
     P.fwd = mfma_shape(N, V);
-    P.Vc = std::min<int64_t>(round_up(V, 256), kCeVocabChunk);
-    P.R = std::min<int64_t>(std::max<int64_t>(N, 1), kCeRowBlock);
-    P.lexp = mfma_shape(P.Vc, P.R);
-    P.dz = mfma_shape(P.R, P.Vc);
-    P.dh = mfma_shape(d, P.R);
     P.Vp = round_up(V, 256);
   } else {
     P.Vc = std::min<int64_t>(round_up(V, 64), kCeVocabChunk);
@@ -481,10 +503,10 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
     P.Vp = V;
   }
   P.n_vb = ceil_div(V, P.fwd.bn);
-  P.n_vb_exp = ceil_div(V, P.lexp.bm);
-  // The (max, sum) partials of the three-GEMM path and the sigma partials of the
-  // label-referenced path share one region: the second is consumed before the first is written.
-  const size_t part = std::max((size_t)N * P.n_vb * 8, (size_t)N * P.n_vb_exp * 4);
+  P.nv = ceil_div(V, 256);
+  // The (max, sum) partials of the forward and the per-(row, vocab tile) sums of the fused
+  // backward share one region: the sums are consumed before the exact path writes partials.
+  const size_t part = std::max((size_t)N * P.n_vb * 8, dtype == ATTT_BF16 ? (size_t)N * P.nv * 4 : 0);
   size_t o = 0;
   P.off_part = o;    o += align256(part);
   P.off_label = o;   o += align256((size_t)N * 4);
@@ -493,33 +515,92 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad) {
   P.off_rowloss = o; o += align256((size_t)N * 4);
   if (grad && N > 0) {
     if (dtype == ATTT_BF16) {
-      P.off_sa = o;   o += align256((size_t)N * 4);
-      P.off_sb = o;   o += align256((size_t)N * 4);
-      P.off_flag = o; o += 256;
-      P.off_wt = o;
-      o += align256((size_t)d * P.Vp * 2);
-    }
-    P.off_dz = o;
-    o += align256((size_t)P.R * P.Vc * esz);
-    const bool chunks = V > P.Vc;
-    if (dtype == ATTT_BF16 && chunks) {
-      // float32 partial dH in the dH kernel's tile layout: whole bm x bn tiles
-      P.off_acc = o;
-      o += align256((size_t)ceil_div(d, P.dh.bm) * ceil_div(P.R, P.dh.bn) * P.dh.bm * P.dh.bn * 4);
+      // fused backward: one consumer per 256-column slice of d (at most 24 of a team of
+      // kCeTeam; more slices take several passes), the rest produce; the ring gives every
+      // producer two slots plus slack
+      P.slices = (int)ceil_div(d, 256);
+      P.consumers = std::min(P.slices, 24);
+      P.passes = (int)ceil_div(P.slices, P.consumers);
+      P.slots = 2 * (kCeTeam - P.consumers) + 4;
+      // items of the busiest team: its row tiles (one in 8) x passes x vocabulary tiles
+      P.items_max = (int)round_up(ceil_div(ceil_div(N, 256), 8) * P.passes * P.nv, 4);
+      P.sync_ints = ce_fused_sync_ints(P.slots, P.items_max);
+      P.off_flag = o;  o += 256;
+      P.off_sync = o;  o += align256((size_t)P.sync_ints * 4);
+      P.off_sync2 = o; o += align256((size_t)P.sync_ints * 4);
+      P.off_ring = o;  o += align256(ce_fused_ring_bytes(P.slots));
+      if (!have_head_t) {
+        P.off_wt = o;
+        o += align256((size_t)d * P.Vp * 2);
+      }
+    } else {
+      P.off_dz = o;
+      o += align256((size_t)P.R * P.Vc * 4);
     }
   }
   P.total = std::max<size_t>(o, 256);
   return P;
 }
 
+// The fused backward runs one workgroup per CU in teams of kCeTeam per XCD: the 256-CU, 8-XCD
+// layout of the MI355X, with cooperative launch. Cached per device.
+attt_status ce_fused_device_ok() {
+  static std::mutex mu;
+  static int state[64] = {};  // 0 unknown, 1 ok, 2 not
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(ATTT_EUNSUPPORTED, "ce: device index %d", dev);
+  std::lock_guard<std::mutex> lk(mu);
+  if (state[dev] == 0) {
+    int cus = 0, coop = 0;
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "hipDeviceGetAttribute");
+    HIP_TRY(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev), "hipDeviceGetAttribute");
+    state[dev] = (cus == 8 * kCeTeam && coop) ? 1 : 2;
+    if (state[dev] == 2)
+      return fail(ATTT_EUNSUPPORTED, "ce: the bf16 backward needs %d CUs and cooperative launch (device has %d CUs%s)",
+                  8 * kCeTeam, cus, coop ? "" : ", no cooperative launch");
+  }
+  if (state[dev] == 2) return fail(ATTT_EUNSUPPORTED, "ce: the bf16 backward needs %d CUs and cooperative launch",
+                                   8 * kCeTeam);
+  return ATTT_OK;
+}
+
+// bounds of the fused backward's waits (microseconds): label-referenced pass, exact pass
+int64_t g_ce_wait_us[2] = {20000, 20000};
+
 }  // namespace
 
 extern "C" attt_status attt_ce_workspace_size(int64_t N, int64_t d, int64_t V, int32_t dtype,
-                                              int32_t want_grad, size_t* bytes) {
+                                              int32_t flags, size_t* bytes) {
   if (!bytes) return fail(ATTT_EINVAL, "ce: bytes is null");
-  attt_status st = ce_validate(N, d, V, dtype);
+  if (flags & ~(ATTT_CE_WANT_GRAD | ATTT_CE_HEAD_T)) return fail(ATTT_EINVAL, "ce: unknown flags 0x%x", flags);
+  const bool grad = (flags & ATTT_CE_WANT_GRAD) != 0;
+  attt_status st = ce_validate(N, d, V, dtype, grad);
   if (st) return st;
-  *bytes = ce_plan(N, d, V, dtype, want_grad != 0).total;
+  *bytes = ce_plan(N, d, V, dtype, grad, (flags & ATTT_CE_HEAD_T) != 0).total;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ce_head_t_size(int64_t d, int64_t V, size_t* bytes) {
+  if (!bytes) return fail(ATTT_EINVAL, "ce_head_t: bytes is null");
+  attt_status st = ce_validate(0, d, V, ATTT_BF16, true);
+  if (st) return st;
+  *bytes = (size_t)d * round_up(V, 256) * 2;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ce_head_transpose(const void* lm_head, int64_t d, int64_t V, void* lm_head_t,
+                                              size_t lm_head_t_bytes, void* stream) {
+  attt_status st = ce_validate(0, d, V, ATTT_BF16, true);
+  if (st) return st;
+  if (!lm_head || !lm_head_t) return fail(ATTT_EINVAL, "ce_head_t: null pointer");
+  if (!aligned16(lm_head) || !aligned16(lm_head_t))
+    return fail(ATTT_EINVAL, "ce_head_t: lm_head and lm_head_t must be 16-byte aligned");
+  const int64_t Vp = round_up(V, 256);
+  if (lm_head_t_bytes < (size_t)d * Vp * 2)
+    return fail(ATTT_ENOSPACE, "ce_head_t: %zu bytes, need %zu", lm_head_t_bytes, (size_t)d * Vp * 2);
+  HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)Vp, lm_head_t, static_cast<hipStream_t>(stream)),
+          "ce_head_transpose");
   return ATTT_OK;
 }
 
@@ -530,8 +611,21 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
                                                 float* loss, float* lse, void* grad_hidden,
                                                 void* workspace, size_t workspace_bytes,
                                                 void* stream) {
-  attt_status st = ce_validate(N, d, V, dtype);
+  return attt_weighted_ce_fwd_bwd_ex(hidden, lm_head, nullptr, labels, weights, row_offsets, num_episodes, N,
+                                     d, V, dtype, loss, lse, grad_hidden, workspace, workspace_bytes, stream);
+}
+
+extern "C" attt_status attt_weighted_ce_fwd_bwd_ex(const void* hidden, const void* lm_head,
+                                                   const void* lm_head_t, const int32_t* labels,
+                                                   const float* weights, const int64_t* row_offsets,
+                                                   int32_t num_episodes, int64_t N, int64_t d, int64_t V,
+                                                   int32_t dtype, float* loss, float* lse, void* grad_hidden,
+                                                   void* workspace, size_t workspace_bytes, void* stream) {
+  attt_status st = ce_validate(N, d, V, dtype, grad_hidden != nullptr);
   if (st) return st;
+  if (lm_head_t && (dtype != ATTT_BF16 || !grad_hidden))
+    return fail(ATTT_EINVAL, "ce: lm_head_t applies to the bf16 backward only");
+  if (lm_head_t && !aligned16(lm_head_t)) return fail(ATTT_EINVAL, "ce: lm_head_t must be 16-byte aligned");
   if (num_episodes < 1) return fail(ATTT_EINVAL, "ce: num_episodes must be >= 1 (got %d)", num_episodes);
   int64_t single[2] = {0, N};
   const int64_t* off = row_offsets;
@@ -550,7 +644,7 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
       return fail(ATTT_EINVAL, "ce: hidden, lm_head and grad_hidden must be 16-byte aligned");
   }
   const bool grad = grad_hidden != nullptr;
-  CePlan P = ce_plan(N, d, V, dtype, grad);
+  CePlan P = ce_plan(N, d, V, dtype, grad, lm_head_t != nullptr);
   if (workspace_bytes < P.total)
     return fail(ATTT_ENOSPACE, "ce: workspace %zu bytes, need %zu", workspace_bytes, P.total);
   if (!workspace) return fail(ATTT_EINVAL, "ce: workspace is null");
@@ -592,90 +686,117 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd(const void* hidden, const void* 
     }
     return ATTT_OK;
   };
-  // The three-GEMM algorithm: forward (max, sum exp) partials -> lse, w CE, loss; then per
-  // (row block, vocab chunk) dZ = coef (softmax - onehot) and dH (+)= dZ W. With `gate` set it
-  // runs only when the flag is raised.
-  void* dz = ws + P.off_dz;
-  void* wt = (grad && dtype == ATTT_BF16) ? ws + P.off_wt : nullptr;
-  float* acc = P.off_acc ? reinterpret_cast<float*>(ws + P.off_acc) : nullptr;
-  auto three_gemm = [&](const int* gate) -> attt_status {
+  const void* wt = !(grad && dtype == ATTT_BF16) ? nullptr : lm_head_t ? lm_head_t : ws + P.off_wt;
+  // The forward (both dtypes; also the exact path of the bf16 backward, gated on `gate`):
+  // (max, sum exp) partials -> lse, coef, w CE -> loss.
+  auto forward = [&](const int* gate) -> attt_status {
     HIP_TRY(launch_ce_fwd(dtype, P.fwd, hidden, lm_head, labels, (int)N, (int)d, (int)V, part,
                           (int)P.n_vb, label_logit, gate, s),
             "ce_fwd_lse");
-    attt_status st2 = batches(4, [&](const CeEpBatch& b, int blocks) -> attt_status {
+    return batches(4, [&](const CeEpBatch& b, int blocks) -> attt_status {
       HIP_TRY(launch_ce_row_reduce(b, blocks, part, (int)P.n_vb, label_logit, weights, lse_buf, coef,
                                    rowloss, gate, s),
               "ce_row_reduce");
       HIP_TRY(launch_ce_loss(b, rowloss, loss, gate, s), "ce_loss");
       return ATTT_OK;
     });
-    if (st2 || !grad) return st2;
+  };
+
+  if (dtype == ATTT_F32) {
+    // float32: three VALU GEMMs, dZ = coef (softmax - onehot) staged per (row block, vocab chunk)
+    st = forward(nullptr);
+    if (st || !grad) return st;
+    float* dz = reinterpret_cast<float*>(ws + P.off_dz);
     for (int64_t r0 = 0; r0 < N; r0 += P.R) {
       const int64_t R = std::min(P.R, N - r0);
       for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
         const int64_t width = std::min(P.Vc, V - c0);
-        const bool first = c0 == 0, last = c0 + P.Vc >= V;
-        HIP_TRY(launch_ce_bwd_dz(dtype, P.dz, hidden, lm_head, labels, lse_buf, coef, (int)r0, (int)R,
-                                 (int)d, (int)c0, (int)width, (int)V, dz, (int)P.Vc, gate, s),
+        HIP_TRY(launch_ce_bwd_dz(static_cast<const float*>(hidden), static_cast<const float*>(lm_head), labels,
+                                 lse_buf, coef, (int)r0, (int)R, (int)d, (int)c0, (int)width, (int)V, dz, (int)P.Vc,
+                                 s),
                 "ce_bwd_dz");
-        const int64_t K = dtype == ATTT_BF16 ? round_up(width, 64) : round_up(width, 16);
-        HIP_TRY(launch_ce_bwd_dh(dtype, P.dh, dz, (int)P.Vc, lm_head, wt, (int)P.Vp, (int)r0, (int)R,
-                                 (int)d, (int)c0, (int)K, (int)V, acc, grad_hidden, first, last,
-                                 CeRowScale{}, gate, s),
+        HIP_TRY(launch_ce_bwd_dh(dz, (int)P.Vc, static_cast<const float*>(lm_head), (int)r0, (int)R, (int)d, (int)c0,
+                                 (int)round_up(width, 16), (int)V, static_cast<float*>(grad_hidden), c0 == 0, s),
                 "ce_bwd_dh");
       }
     }
     return ATTT_OK;
-  };
-
-  if (dtype == ATTT_BF16) {
-    int* flag = grad ? reinterpret_cast<int*>(ws + P.off_flag) : nullptr;
-    HIP_TRY(launch_ce_label(hidden, lm_head, labels, (int)N, (int)d, (int)V, label_logit, flag, s),
-            "ce_label_logit");
   }
-  if (!grad || dtype != ATTT_BF16) return three_gemm(nullptr);
 
-  // bf16 forward + backward: the label-referenced two-GEMM pass, then the guard.
+  HIP_TRY(launch_ce_label(hidden, lm_head, labels, (int)N, (int)d, (int)V, label_logit,
+                          grad ? reinterpret_cast<int*>(ws + P.off_flag) : nullptr, s),
+          "ce_label_logit");
+  if (!grad) return forward(nullptr);
+
+  // bf16 forward + backward: the fused label-referenced pass (ce_fused.hip), lse and the loss
+  // from its per-tile sums, then the exact pass, which runs only if the guard flag was raised
+  // (a label-referenced sum could overflow, or the fused pass aborted).
+  st = ce_fused_device_ok();
+  if (st) return st;
   int* flag = reinterpret_cast<int*>(ws + P.off_flag);
+  int* sync = reinterpret_cast<int*>(ws + P.off_sync);
+  int* sync2 = reinterpret_cast<int*>(ws + P.off_sync2);
   float* sig_part = reinterpret_cast<float*>(ws + P.off_part);
-  float* sa = reinterpret_cast<float*>(ws + P.off_sa);
-  float* sb = reinterpret_cast<float*>(ws + P.off_sb);
   st = batches(256, [&](const CeEpBatch& b, int blocks) -> attt_status {
     HIP_TRY(launch_ce_coef(b, blocks, weights, coef, s), "ce_coef");
     return ATTT_OK;
   });
   if (st) return st;
-  HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)P.Vp, wt, s), "ce_head_transpose");
-  const CeRowScale rs{sa, sb, labels};
-  for (int64_t r0 = 0; r0 < N; r0 += P.R) {
-    const int64_t R = std::min(P.R, N - r0);
-    for (int64_t c0 = 0; c0 < V; c0 += P.Vc) {
-      const int64_t width = std::min(P.Vc, V - c0);
-      const bool first = c0 == 0, last = c0 + P.Vc >= V;
-      // The first GEMM runs in launches of kCeExpLaunch columns: a launch boundary lines the
-      // workgroups up again, so each XCD's concurrent tiles keep sharing their operand panels
-      // in L2 instead of drifting apart over a whole-vocabulary launch (fewer L2 misses).
-      for (int64_t cc = 0; cc < width; cc += kCeExpLaunch)
-        HIP_TRY(launch_ce_logit_exp(P.lexp, hidden, lm_head, labels, label_logit, (int)r0, (int)R, (int)d,
-                                    (int)(c0 + cc), (int)std::min(kCeExpLaunch, width - cc), (int)V, sig_part,
-                                    (int)P.n_vb_exp, static_cast<uint8_t*>(dz) + cc * 2, (int)P.Vc, flag, s),
-                "ce_logit_exp");
-      if (last)
-        HIP_TRY(launch_ce_row_final((int)r0, (int)R, sig_part, (int)P.n_vb_exp, label_logit, weights, coef,
-                                    lse_buf, rowloss, sa, sb, s),
-                "ce_row_final");
-      HIP_TRY(launch_ce_bwd_dh(dtype, P.dh, dz, (int)P.Vc, lm_head, wt, (int)P.Vp, (int)r0, (int)R,
-                               (int)d, (int)c0, (int)round_up(width, 64), (int)V, acc, grad_hidden, first,
-                               last, rs, nullptr, s),
-              "ce_bwd_dh");
-    }
-  }
+  if (!lm_head_t)
+    HIP_TRY(launch_ce_head_transpose(lm_head, (int)V, (int)d, (int)P.Vp, ws + P.off_wt, s), "ce_head_transpose");
+  // both sync areas are adjacent: one clear
+  HIP_TRY(launch_ce_sync_clear(sync, (int)((P.off_sync2 - P.off_sync) / 4 + P.sync_ints), s), "ce_sync_clear");
+  CeFusedArgs fa{};
+  fa.h = static_cast<const bf16_t*>(hidden);
+  fa.W = static_cast<const bf16_t*>(lm_head);
+  fa.WT = static_cast<const bf16_t*>(wt);
+  fa.labels = labels;
+  fa.label_logit = label_logit;
+  fa.lse = lse_buf;
+  fa.coef = coef;
+  fa.sig_part = sig_part;
+  fa.grad = static_cast<bf16_t*>(grad_hidden);
+  fa.ring = ws + P.off_ring;
+  fa.sync = sync;
+  fa.gate = flag;
+  fa.limit = (uint64_t)g_ce_wait_us[0] * 100;
+  fa.N = (int)N;
+  fa.d = (int)d;
+  fa.V = (int)V;
+  fa.Vp = (int)P.Vp;
+  fa.nv = (int)P.nv;
+  fa.row_tiles = (int)ceil_div(N, 256);
+  fa.slices = P.slices;
+  fa.consumers = P.consumers;
+  fa.passes = P.passes;
+  fa.slots = P.slots;
+  fa.items_max = P.items_max;
+  HIP_TRY(launch_ce_fused(true, fa, s), "ce_fused_bwd");
+  HIP_TRY(launch_ce_row_final(0, (int)N, sig_part, (int)P.nv, label_logit, weights, coef, lse_buf, rowloss, nullptr,
+                              nullptr, s),
+          "ce_row_final");
   st = batches(4, [&](const CeEpBatch& b, int) -> attt_status {
     HIP_TRY(launch_ce_loss(b, rowloss, loss, nullptr, s), "ce_loss");
     return ATTT_OK;
   });
   if (st) return st;
-  return three_gemm(flag);
+  HIP_TRY(launch_ce_fused_status(sync, flag, s), "ce_fused_status");
+  // exact path: forward lse, then the fused pass on coef (exp(z - lse) - onehot)
+  st = forward(flag);
+  if (st) return st;
+  fa.sync = sync2;
+  fa.limit = (uint64_t)g_ce_wait_us[1] * 100;
+  HIP_TRY(launch_ce_fused(false, fa, s), "ce_fused_bwd (exact)");
+  HIP_TRY(launch_ce_fused_nan(sync2, loss, E, lse_buf, (int)N, grad_hidden, N * d, s), "ce_fused_nan");
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_ce_set_wait_limit(int64_t label_us, int64_t exact_us) {
+  if (label_us < 0 || exact_us < 0 || label_us > ((int64_t)1 << 40) || exact_us > ((int64_t)1 << 40))
+    return fail(ATTT_EINVAL, "ce_set_wait_limit: limits must be in [0, 2^40] microseconds");
+  g_ce_wait_us[0] = label_us;
+  g_ce_wait_us[1] = exact_us;
+  return ATTT_OK;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -704,8 +825,10 @@ attt_status lora_validate(const attt_lora_problem* p, int32_t count, int32_t dty
       return fail(ATTT_EINVAL, "lora[%d]: rank must be in [1, %d] (got %d)", i, ATTT_LORA_MAX_RANK, q.rank);
     if (q.rows < 0 || q.d_in < 1 || q.d_out < 1 || q.d_in % 8 || q.d_out % 8)
       return fail(ATTT_EINVAL, "lora[%d]: need rows >= 0 and d_in, d_out positive multiples of 8", i);
-    if (q.rows >= ((int64_t)1 << 30) || q.d_in >= ((int64_t)1 << 20) || q.d_out >= ((int64_t)1 << 20))
-      return fail(ATTT_EUNSUPPORTED, "lora[%d]: dimensions beyond this build's limits", i);
+    // pass 2 addresses a rank tile's [2][16, rows_pad] bf16 operand through one 32-bit range
+    if (q.rows >= ((int64_t)1 << 24) || q.d_in >= ((int64_t)1 << 20) || q.d_out >= ((int64_t)1 << 20))
+      return fail(ATTT_EUNSUPPORTED, "lora[%d]: dimensions beyond this build's limits (rows < 2^24, "
+                  "d_in and d_out < 2^20)", i);
     if (!std::isfinite(q.scale)) return fail(ATTT_EINVAL, "lora[%d]: scale is not finite", i);
     if (!q.dA || !q.dB) return fail(ATTT_EINVAL, "lora[%d]: dA / dB is null", i);
     if (q.rows > 0 && (!q.x || !q.dy || !q.A || !q.B)) return fail(ATTT_EINVAL, "lora[%d]: null input", i);
@@ -718,6 +841,7 @@ attt_status lora_validate(const attt_lora_problem* p, int32_t count, int32_t dty
 LoraPlan lora_plan(const attt_lora_problem* p, int32_t count, int32_t dtype) {
   LoraPlan P;
   const size_t esz = dtype == ATTT_BF16 ? 2 : 4;
+  const size_t lt_planes = dtype == ATTT_BF16 ? 2 : 1;
   P.prob.resize(count);
   // Problems reading the same x (same pointer, d_in and rows) share pass-1 and dA jobs.
   std::vector<int> tiles(count, 0);
@@ -748,8 +872,9 @@ LoraPlan lora_plan(const attt_lora_problem* p, int32_t count, int32_t dtype) {
     Q.rows_pad = (int32_t)round_up(q.rows, kLoraRowTile);
     Q.splits = std::max(1, std::min(16, Q.rows_pad / 512));
     Q.bt_off = (int64_t)o;  o += align256((size_t)Q.rp * q.d_out * esz);
-    Q.ut_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.rows_pad * esz);
-    Q.dut_off = (int64_t)o; o += align256((size_t)Q.rp * Q.rows_pad * esz);
+    // pass-1 results U^T and dU^T: float32, or for bf16 two planes (hi, lo) per rank tile
+    Q.ut_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.rows_pad * esz * lt_planes);
+    Q.dut_off = (int64_t)o; o += align256((size_t)Q.rp * Q.rows_pad * esz * lt_planes);
     Q.pa_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.splits * q.d_in * 4);
     Q.pb_off = (int64_t)o;  o += align256((size_t)Q.rp * Q.splits * q.d_out * 4);
   }
@@ -797,6 +922,7 @@ extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   const int64_t esz = dtype == ATTT_BF16 ? 2 : 4;
+  const int64_t lt_tile = 16 * (dtype == ATTT_BF16 ? 2 : 1) * esz;  // bytes per row of rows_pad per tile
 
   std::vector<LoraBTJob> bt;
   std::vector<LoraP1Job> p1;
@@ -834,8 +960,8 @@ extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t
       const LoraProb& Q = P.prob[i];
       for (int t = 0; t < Q.rp / 16; ++t) {
         add_tile1(J1, static_cast<const uint8_t*>(q.A) + (int64_t)16 * t * q.d_in * esz,
-                  std::min(16, q.rank - 16 * t), q.scale, Q.ut_off + (int64_t)16 * t * Q.rows_pad * esz);
-        add_tile2(J2, Q.dut_off + (int64_t)16 * t * Q.rows_pad * esz,
+                  std::min(16, q.rank - 16 * t), q.scale, Q.ut_off + (int64_t)t * Q.rows_pad * lt_tile);
+        add_tile2(J2, Q.dut_off + (int64_t)t * Q.rows_pad * lt_tile,
                   Q.pa_off + (int64_t)t * Q.splits * 16 * q.d_in * 4);
       }
     }
@@ -867,8 +993,8 @@ extern "C" attt_status attt_lora_grad(const attt_lora_problem* problems, int32_t
     J2.splits = Q.splits;
     for (int t = 0; t < Q.rp / 16; ++t) {
       add_tile1(J1, ws + Q.bt_off + (int64_t)16 * t * q.d_out * esz, 16, q.scale,
-                Q.dut_off + (int64_t)16 * t * Q.rows_pad * esz);
-      add_tile2(J2, Q.ut_off + (int64_t)16 * t * Q.rows_pad * esz,
+                Q.dut_off + (int64_t)t * Q.rows_pad * lt_tile);
+      add_tile2(J2, Q.ut_off + (int64_t)t * Q.rows_pad * lt_tile,
                 Q.pb_off + (int64_t)t * Q.splits * 16 * q.d_out * 4);
     }
     p1.push_back(J1);

@@ -1,337 +1,36 @@
-// Token-weighted cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10), forward and
-// backward with respect to the hidden states, on gfx950.
+// Token-weighted cross-entropy through a frozen LM head (Sec. 3.3, Eq. 10) on gfx950: the
+// forward of both dtypes, the float32 backward, and the row and episode kernels around the bf16
+// backward, whose two contractions run fused in one persistent kernel (ce_fused.hip).
 //
-// Forward only (logits never leave the chip): one GEMM z = h W^T over (vocab tile, row tile)
-// whose epilogue reduces every row of the tile to (max, sum exp(z - max)). A row kernel merges
-// the partials into lse and w * CE; an episode kernel sums those in a fixed order into
+// Forward (logits never leave the chip): one GEMM z = h W^T over (vocab tile, row tile) whose
+// epilogue reduces every row of the tile to (max, sum exp(z - max)). A row kernel merges the
+// partials into lse and w * CE; an episode kernel sums those in a fixed order into
 // loss_e = (1/L_e) sum w_t CE_t.
 //
-// Forward + backward (bf16): two GEMMs over the vocabulary, the algorithmic 4 N V d flops.
-// Every row takes its own label logit r_t = z_{t,y_t} as the exponent reference, so the first
-// GEMM can form e_tv = exp(z_tv - r_t) without knowing lse:
+// bf16 forward + backward: every row takes its own label logit r_t = z_{t,y_t} (ce_label_logit,
+// one dot product per row) as the exponent reference, so the fused kernel forms
+// e_tv = exp(z_tv - r_t) without knowing lse:
 //     sigma_t = sum_{v != y_t} e_tv,   lse_t = r_t + log1p(sigma_t),   CE_t = log1p(sigma_t)
 //     dL/dh_t = (w_t / L_e) (U_t - sigma_t W_{y_t}) / (1 + sigma_t),  U_t = sum_{v != y_t} e_tv W_v
 // which is (w_t / L_e)(softmax(z_t) - onehot(y_t)) W rewritten; the label term is kept out of
-// the sums, so nothing cancels when p_y is close to 1. Per vocab chunk, the first GEMM
-// (ce_logit_exp) stores e (bf16) into a bounded staging buffer and the per-row sums of its
-// tile; the second (ce_bwd_dh) accumulates U += e_chunk W_chunk in float32. After the last
-// chunk's first GEMM a row kernel forms sigma, lse and CE, and the last dh epilogue applies
-// the row scale and the label term. r_t is one of the row's logits, so sigma never
-// underflows; a logit more than 64 above r_t (a label with probability below e^-64)
-// could overflow e, and sets a flag on which the exact three-GEMM path (forward lse, then
-// dZ = (w/L)(exp(z - lse) - onehot) and dH = dZ W) reruns in full, overwriting the outputs.
-// Its kernels read the flag first and return at once when it is clear.
+// the sums, so nothing cancels when p_y is close to 1. ce_row_final turns the fused kernel's
+// per-(row, vocab tile) sums into sigma, lse and the row losses. r_t is one of the row's logits,
+// so sigma never underflows; a logit more than 64 above r_t (a label with probability below
+// e^-64) could overflow e and raises a flag, on which the exact path (forward lse, then the fused
+// kernel on coef exp(z - lse)) reruns in full, overwriting the outputs. Its kernels read the flag
+// first and return at once when it is clear.
 //
-// bf16 path: MFMA v_mfma_f32_32x32x16_bf16. A 256x256 tile runs on 8 waves (2x4, 128x64
-// each, two waves per SIMD); small problems use 128x128 on 4 waves. K advances 64 per stage,
-// double-buffered in LDS, with an XOR swizzle of the 16-byte chunks (chunk ^ (row/2)%8): the
-// LDS serves 16 lanes of a 16-byte read per clock over 64 banks, and the 16 consecutive rows
-// those lanes read fall in distinct banks. Global reads are buffer loads whose masked lanes
-// point past the descriptor's range (the hardware returns zero, no branches). Tile order is
-// XCD-aware: workgroup i runs on XCD i%8, each XCD takes a contiguous range of the order, and
-// the order walks groups of 8 row tiles column by column, so the workgroups resident on one
-// XCD share a few hidden and LM-head panels in its L2.
-// f32 path: plain VALU tiles (64x64, 4x4 per thread) running the three-GEMM algorithm; it
-// serves the float32 configuration.
+// bf16 GEMMs: MFMA v_mfma_f32_32x32x16_bf16 through the core in gemm_core.hpp (256x256 tiles on 8
+// waves, 128x128 on 4 for small problems; XCD-aware tile order).
+// f32 path: plain VALU tiles (64x64, 4x4 per thread) running the three-GEMM algorithm (forward,
+// dZ = coef (softmax - onehot) staged per block of rows and vocabulary, dH = dZ W); it serves the
+// float32 configuration.
 #include "common.hpp"
+#include "gemm_core.hpp"
 #include "internal.hpp"
 
 namespace attt {
 
-// ------------------------------------------------------------------------------------------
-// Shared helpers
-// ------------------------------------------------------------------------------------------
-__device__ __forceinline__ int xcd_remap(int bid, int total) {
-  const int xcd = bid & 7, j = bid >> 3;
-  const int q = total >> 3, r = total & 7;
-  return xcd * q + min(xcd, r) + j;
-}
-
-// Tile of workgroup `bid`: each XCD takes a contiguous range of the tile order, and that
-// order walks groups of 8 row tiles column by column, so the ~32 workgroups resident on one
-// XCD cover about 8 row panels x 4 column panels and share them in that XCD's L2.
-__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int t = xcd_remap(bid, tiles_m * tiles_n);
-  constexpr int GM = 8;
-  const int per_group = GM * tiles_n;
-  const int g = t / per_group;
-  const int first = g * GM;
-  const int gm = min(GM, tiles_m - first);
-  const int local = t - g * per_group;
-  tm = first + local % gm;
-  tn = local / gm;
-}
-
-// Workgroup tile BM x BN computed by WGM x WGN waves; each wave owns a (BM/WGM) x (BN/WGN)
-// block of 32x32 MFMA tiles. K advances 64 per stage, two stages in LDS.
-template <int BM_, int BN_, int WGM_, int WGN_>
-struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
-  static constexpr int NT = 64 * WGM * WGN;
-  static constexpr int BK = 64;
-  static constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  static constexpr int TM = WTM / 32, TN = WTN / 32;
-  static constexpr int RPL = NT / 8;  // rows one load round covers (8 x 16-byte chunks per row)
-  static constexpr int AL = BM / RPL, BL = BN / RPL;
-  static constexpr int SA = BM * BK, SB = BN * BK;
-  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);  // two stages
-};
-using CfgBig = Cfg<256, 256, 2, 4>;    // 8 waves, 128x64 per wave
-using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
-
-// Buffer loads return zero for offsets past the descriptor's range: masked lanes use kOOB
-// instead of branching. Valid offsets stay far below kRsrcBytes (a tile spans < 256 rows).
-constexpr uint32_t kOOB = 0x7FFFFFF0u;
-constexpr int kRsrcBytes = 0x40000000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p) { return buffer_rsrc(p, kRsrcBytes); }
-__device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
-
-// acc += A[0:BM, 0:K] * B[0:BN, 0:K]^T, A and B K-contiguous bf16. Rows at or past mval
-// (nval) and K-chunks at or past K read as zero. K % 8 == 0.
-template <class C>
-__device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, int64_t lda, int mval,
-                                              const bf16_t* __restrict__ B, int64_t ldb, int nval,
-                                              int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  // Global -> LDS without registers: buffer_load_dwordx4 ... lds writes lane i's 16 bytes at
-  // LDS base + 16 i, so one instruction fills a 1 KiB block of 8 rows x 128 bytes. Lane i of a
-  // block takes row 8*block + i/8 and physical chunk i%8, and fetches the logical chunk that
-  // the swizzle stores there (physical ^ (row/2)%8). The stage's blocks are dealt round-robin
-  // to the waves.
-  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
-  constexpr int NW = C::NT / 64;
-  constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
-  constexpr int BPW = (ABLK + BBLK) / NW;  // blocks per wave per stage
-  static_assert((ABLK + BBLK) % NW == 0 && ABLK % NW == 0, "stage blocks must split evenly");
-  uint32_t goff[BPW];
-  int gch[BPW];
-#pragma unroll
-  for (int j = 0; j < BPW; ++j) {
-    const int blk = wave + j * NW;
-    const bool isA = blk < ABLK;
-    const int row = (isA ? blk : blk - ABLK) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ ((row >> 1) & 7);
-    gch[j] = c;
-    const int val = isA ? mval : nval;
-    const int64_t ld = isA ? lda : ldb;
-    goff[j] = row < val ? (uint32_t)((int64_t)row * ld * 2) + c * 16 : kOOB;
-  }
-  auto dma = [&](int st, int k0) {
-    bf16_t* base = lds + st * (C::SA + C::SB);
-    const uint32_t kb = (uint32_t)k0 * 2;
-#pragma unroll
-    for (int j = 0; j < BPW; ++j) {
-      const int blk = wave + j * NW;
-      const bool isA = blk < ABLK;
-      const bool kin = k0 + gch[j] * 8 < K;
-      const uint32_t off = (kin && goff[j] != kOOB) ? goff[j] + kb : kOOB;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rA : rB,
-                                               (__attribute__((address_space(3))) void*)(base + blk * 512),
-                                               16, off, 0, 0, 0);
-    }
-  };
-
-  const int nk = (K + 63) / 64;
-  dma(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  const int l32 = lane & 31, hi = lane >> 5;
-  const int swz = (l32 >> 1) & 7;
-  const int arow = (wm * C::WTM + l32) * 64, brow = (wn * C::WTN + l32) * 64;
-  // operand fragments of sub-step kk live in fa/fb[kk & 1]; the reads for kk+1 are issued
-  // before the MFMAs of kk so their LDS latency hides behind those MFMAs
-  bf16x8 fa[2][C::TM], fb[2][C::TN];
-  auto fragload = [&](const bf16_t* As, const bf16_t* Bs, int kk, int slot) {
-    const int sw = ((kk * 2 + hi) ^ swz) << 3;
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-      fa[slot][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 32 * 64 + sw));
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-      fb[slot][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
-  };
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) dma((kt + 1) & 1, (kt + 1) * 64);
-    const bf16_t* As = lds + (kt & 1) * (C::SA + C::SB);
-    const bf16_t* Bs = As + C::SA;
-    fragload(As, Bs, 0, 0);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      if (kk + 1 < 4) fragload(As, Bs, kk + 1, (kk + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk & 1][i], fb[kk & 1][j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of the next stage have landed in LDS
-    __syncthreads();
-  }
-}
-
-// 8-wave ping-pong schedule. Waves 0-3 and 4-7 form two groups with one wave of each on every
-// SIMD. Phases are separated by workgroup barriers and group 1 runs one phase behind group 0, so
-// in every phase one wave per SIMD reads a whole K-step of operand fragments from LDS (memory
-// phase) while the other runs its 32 MFMAs (compute phase).
-__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// Tile loads are issued only in memory phases: a wave stalls at a load instruction until the
-// load path accepts it (about 1 KiB per 25 cycles per CU here), and a stall in a compute phase
-// idles the SIMD's matrix core. A stage is 64 instructions of 1 KiB; both groups share them:
-//  * group 0 issues blocks [0, kG0) of stage k+1 at the start of its memory phase of stage k
-//    (slot (k+1)&1 was last read by group 1 in the phase before) and waits for them at the end
-//    of its compute phase of stage k;
-//  * group 1 issues blocks [kG0, 16) of stage k+2 at the end of its memory phase of stage k,
-//    after its own fragment reads of slot k&1 have completed (group 0 finished reading that
-//    slot before the barrier that opened the phase), and waits for them one memory phase later.
-// Group 1's share thus has three phases to land instead of one, and neither group's memory
-// phase carries a whole stage of load issue.
-template <class C>
-__device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
-                                                 const bf16_t* __restrict__ B, int64_t ldb, int nval,
-                                                 int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
-  static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4, "ping-pong needs 8 waves in 2 groups of 4");
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const int grp = wave >> 2;
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  // A stage's 64 blocks of 8 rows x 128 bytes: block (wave & 3) + 4 j for j in [0, 16). Blocks
-  // j < 8 are A rows, the rest B rows; both groups use the same numbering.
-  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
-  constexpr int LW = 4;                               // waves per group
-  constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
-  constexpr int BPW = (ABLK + BBLK) / LW;             // blocks per wave of a group per stage
-  constexpr int kG0 = 6;                              // group 0's share per wave
-  static_assert(ABLK % LW == 0 && BBLK % LW == 0 && kG0 < BPW, "stage blocks must split evenly");
-  // Offsets are formed per load: the block's first row is wave-uniform, and the swizzled chunk
-  // of a lane depends only on the lane and on the parity of the block (rows 8b .. 8b+7).
-  const int lr = lane >> 3;
-  const int c_even = (lane & 7) ^ ((lr >> 1) & 7);
-  const int c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
-  const uint32_t la = (uint32_t)(lr * lda * 2), lb = (uint32_t)(lr * ldb * 2);
-  auto dma = [&](int st, int k0, int j0, int j1) {
-    bf16_t* base = lds + st * (C::SA + C::SB);
-#pragma unroll
-    for (int j = j0; j < j1; ++j) {
-      const int blk = (wave & 3) + j * LW;
-      const bool isA = blk < ABLK;
-      const int rb = (isA ? blk : blk - ABLK) * 8;
-      const int c = (rb & 8) ? c_odd : c_even;
-      const bool ok = rb + lr < (isA ? mval : nval) && k0 + c * 8 < K;
-      const uint32_t off = (uint32_t)((int64_t)rb * (isA ? lda : ldb) * 2) + (isA ? la : lb) +
-                           (uint32_t)(k0 + c * 8) * 2;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(isA ? rA : rB,
-                                               (__attribute__((address_space(3))) void*)(base + blk * 512),
-                                               16, ok ? off : kOOB, 0, 0, 0);
-    }
-  };
-
-  const int l32 = lane & 31, hi = lane >> 5;
-  const int swz = (l32 >> 1) & 7;
-  const int arow = (wm * C::WTM + l32) * 64, brow = (wn * C::WTN + l32) * 64;
-  bf16x8 fa[4][C::TM], fb[4][C::TN];
-  auto mem = [&](int k) {
-    const bf16_t* As = lds + (k & 1) * (C::SA + C::SB);
-    const bf16_t* Bs = As + C::SA;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int sw = ((kk * 2 + hi) ^ swz) << 3;
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-        fa[kk][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 32 * 64 + sw));
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j)
-        fb[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
-    }
-  };
-  auto compute = [&]() {
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][i], fb[kk][j], acc[i][j], 0, 0, 0);
-  };
-  // MFMAs are pure register operations and could be moved across the barriers; tying the
-  // accumulators to empty asm statements keeps each compute phase between its two barriers.
-  auto pin = [&]() {
-    static_assert(C::TM == 4 && C::TN == 2, "pin lists the 8 accumulators of a 128x64 wave tile");
-    asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[1][0]), "+v"(acc[1][1]),
-                 "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[3][0]), "+v"(acc[3][1]));
-  };
-  // Group 0, iteration k:  loads [0, kG0) of stage k+1; fragments(k); wait for own reads |
-  //                        MFMA(k); wait for own loads |
-  // group 1, one phase later: fragments(k); wait for own reads and loads; loads [kG0, 16) of
-  //                        stage k+2 | MFMA(k) |
-  // Group 1 takes one extra barrier before its loop, group 0 one after it, so every wave
-  // executes 2 nk + 2 barriers. Group 1's share of stage 1 is issued before the loop.
-  const int nk = (K + 63) / 64;
-  if (grp == 0) dma(0, 0, 0, BPW);
-  __builtin_amdgcn_s_waitcnt(0);
-  if (grp == 1 && nk > 1) dma(1, 64, kG0, BPW);
-  wg_barrier();
-  if (grp == 0) {
-    for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) dma((k + 1) & 1, (k + 1) * 64, 0, kG0);
-      mem(k);
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      wg_barrier();
-      pin();
-      compute();
-      pin();
-      __builtin_amdgcn_s_waitcnt(0);
-      wg_barrier();
-    }
-    wg_barrier();
-  } else {
-    wg_barrier();
-    for (int k = 0; k < nk; ++k) {
-      mem(k);
-      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-      if (k + 2 < nk) dma(k & 1, (k + 2) * 64, kG0, BPW);
-      wg_barrier();
-      pin();
-      compute();
-      pin();
-      wg_barrier();
-    }
-  }
-}
-
-template <class C>
-__device__ __forceinline__ void mfma_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
-                                              const bf16_t* __restrict__ B, int64_t ldb, int nval,
-                                              int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN]) {
-  if constexpr (C::NT == 512)
-    mfma_mainloop_pp<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
-  else
-    mfma_mainloop_db<C>(A, lda, mval, B, ldb, nval, K, lds, acc);
-}
-
-// Output layout of a 32x32 MFMA accumulator: register r of lane l holds
-// row 8*(r/4) + 4*(l/32) + r%4, column l%32.
-__device__ __forceinline__ int mfma_row(int r, int lane) { return ((r >> 2) << 3) + ((lane >> 5) << 2) + (r & 3); }
 
 // ------------------------------------------------------------------------------------------
 // bf16 forward. The GEMM runs transposed, z^T = W h^T, so a workgroup tile is 256 vocab rows x
@@ -439,302 +138,9 @@ __global__ __launch_bounds__(256) void ce_label_logit_bf16_kernel(const bf16_t* 
   if (lane == 0) label_logit[row] = s;
 }
 
-// bf16 backward part 1: dZ for rows [r0, r0+R) x vocab [c0, c0 + tiles_n*BN) into staging.
-template <class C>
-__device__ __forceinline__ void ce_dz_bf16_body(
-    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
-    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
-    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
-  extern __shared__ __align__(16) uint8_t smem[];
-  int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * C::BM, n0 = tn * C::BN;
-  f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(h + (int64_t)(r0 + m0) * d, d, R - m0, W + (int64_t)(c0 + n0) * d, d,
-                   cend - (c0 + n0), d, reinterpret_cast<bf16_t*>(smem), acc);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = m0 + wm * C::WTM + i * 32 + mfma_row(r, lane);
-      if (rl >= R) continue;
-      const int row = r0 + rl;
-      const float l = lse[row], c = coef[row];
-      const int y = labels[row];
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j) {
-        const int cl = n0 + wn * C::WTN + j * 32 + (lane & 31);
-        const int col = c0 + cl;
-        float g = 0.0f;
-        if (col < V) g = c * (__expf(acc[i][j][r] - l) - (col == y ? 1.0f : 0.0f));
-        dz[(int64_t)rl * ldz + cl] = (bf16_t)f32_to_bf16_bits(g);
-      }
-    }
-  }
-}
-
-template <class C>
-__global__ __launch_bounds__(C::NT) void ce_dz_bf16_kernel(
-    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
-    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
-    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz) {
-  ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
-}
-
-// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
-template <class C>
-__global__ __launch_bounds__(C::NT) void ce_guard_dz_bf16_kernel(
-    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
-    const float* __restrict__ lse, const float* __restrict__ coef, int r0, int R, int d, int c0,
-    int cend, int V, int tiles_m, int tiles_n, bf16_t* __restrict__ dz, int ldz,
-    const int* __restrict__ gate) {
-  if (*gate == 0) return;
-  ce_dz_bf16_body<C>(h, W, labels, lse, coef, r0, R, d, c0, cend, V, tiles_m, tiles_n, dz, ldz);
-}
-
-// bf16 backward part 2, transposed like the forward: acc[n, t] (+)= sum_k WT[n, c0 + k] S[t, k]
-// over the staged chunk S (n a column of dH, t a row of the block), so every lane holds one
-// row t and runs of four consecutive columns. The last chunk writes dH: acc itself (S = dZ),
-// or, with row scales (S = e), dH_t = sa_t acc_t - sb_t W_{y_t} (sa = coef / (1 + sigma),
-// sb = coef sigma / (1 + sigma)), as 32-byte stores.
-template <class C>
-__device__ __forceinline__ void ce_dh_bf16_body(
-    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
-    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
-    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
-    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
-    int V) {
-  extern __shared__ __align__(16) uint8_t smem[];
-  int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * C::BM, n0 = tn * C::BN;  // m0: first column of dH, n0: first row of the block
-  f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(WT + (int64_t)m0 * Vp + c0, Vp, d - m0, dz + (int64_t)n0 * ldz, ldz, R - n0, K,
-                         reinterpret_cast<bf16_t*>(smem), acc);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-  // The float32 partial sums between chunks keep the accumulators' register layout: per tile,
-  // per (MFMA tile i, j, quarter q of the 16 registers), the workgroup's threads hold 16
-  // contiguous bytes each, so every read and write is a coalesced 16-byte access. Every launch
-  // of one call uses the same tiling, so a tile reads back exactly what it wrote.
-  // Buffer accesses: the per-slot offset is a scalar, the lane's offset the only vector operand.
-  // The first chunk reads through an empty range (zeros), so the add needs no branch.
-  float* tbase = accbuf + (size_t)(tm * tiles_n + tn) * (C::BM * C::BN);
-  const __amdgpu_buffer_rsrc_t racc = buffer_rsrc(tbase, C::BM * C::BN * 4);
-  const __amdgpu_buffer_rsrc_t rprev = buffer_rsrc(tbase, first ? 0 : C::BM * C::BN * 4);
-  const uint32_t voff = threadIdx.x * 16u;
-  auto soff = [](int i, int j, int q) { return (uint32_t)(((i * C::TN + j) * 4 + q) * C::NT * 16); };
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f32x4 p = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rprev, voff, soff(i, j, q), 0));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += p[e];
-      }
-      __builtin_amdgcn_sched_barrier(0);  // one MFMA tile's partials in flight at a time: no spills
-    }
-  if (!last) {
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), racc, voff, soff(i, j, q), 0);
-        }
-    return;
-  }
-  const int hi = lane >> 5;
-#pragma unroll
-  for (int j = 0; j < C::TN; ++j) {
-    const int tl = n0 + wn * C::WTN + j * 32 + (lane & 31);  // row of the block
-    const bool tok = tl < R;
-    float a = 1.0f, b = 0.0f;
-    const bf16_t* wy = nullptr;
-    if (tok && sa) {
-      const int row = r0 + tl;
-      a = sa[row];
-      b = sb[row];
-      const int y = labels[row];
-      if (y >= 0 && y < V) wy = W + (int64_t)y * d;
-      else a = __int_as_float(0x7FC00000);  // outside the contract: NaN row, no read
-    }
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i) {
-      const int cb = m0 + wm * C::WTM + i * 32;  // column of the MFMA tile's first row
-      // register r holds column cb + 8 (r/4) + 4 (lane/32) + r%4: four runs of four columns
-      uint32_t pk[8];
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = cb + 8 * g + 4 * hi;
-        float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (wy && c + 4 <= d) {
-          const uint2 u = *reinterpret_cast<const uint2*>(wy + c);
-          wv[0] = bf16_bits_to_f32(u.x & 0xFFFFu);
-          wv[1] = bf16_bits_to_f32(u.x >> 16);
-          wv[2] = bf16_bits_to_f32(u.y & 0xFFFFu);
-          wv[3] = bf16_bits_to_f32(u.y >> 16);
-        }
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = a * acc[i][j][4 * g + e] - b * wv[e];
-        pk[2 * g] = pack_bf16x2(v[0], v[1]);
-        pk[2 * g + 1] = pack_bf16x2(v[2], v[3]);
-      }
-      // same half-wave exchange as the first GEMM: low lanes get columns 0-15, high 16-31
-      uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const auto sw = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
-        P[k] = sw[0];
-        Q[k] = sw[1];
-      }
-      const int c0w = cb + 16 * hi;  // d % 8 == 0: a run of 16 is whole, half, or absent
-      if (tok && c0w + 8 <= d) {
-        u32x4* dst = reinterpret_cast<u32x4*>(grad + (int64_t)(r0 + tl) * d + c0w);
-        dst[0] = u32x4{P[0], P[1], Q[0], Q[1]};
-        if (c0w + 16 <= d) dst[1] = u32x4{P[2], P[3], Q[2], Q[3]};
-      }
-    }
-  }
-}
-
-template <class C>
-__global__ __launch_bounds__(C::NT) void ce_dh_bf16_kernel(
-    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
-    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
-    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
-    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
-    int V) {
-  ce_dh_bf16_body<C>(dz, ldz, WT, Vp, r0, R, d, c0, K, tiles_m, tiles_n, accbuf, grad, first, last,
-                     sa, sb, labels, W, V);
-}
-
-// The same kernel launched by the overflow guard: returns at once unless *gate != 0.
-template <class C>
-__global__ __launch_bounds__(C::NT) void ce_guard_dh_bf16_kernel(
-    const bf16_t* __restrict__ dz, int ldz, const bf16_t* __restrict__ WT, int Vp, int r0, int R,
-    int d, int c0, int K, int tiles_m, int tiles_n, float* __restrict__ accbuf,
-    bf16_t* __restrict__ grad, int first, int last, const float* __restrict__ sa,
-    const float* __restrict__ sb, const int32_t* __restrict__ labels, const bf16_t* __restrict__ W,
-    int V, const int* __restrict__ gate) {
-  if (*gate == 0) return;
-  ce_dh_bf16_body<C>(dz, ldz, WT, Vp, r0, R, d, c0, K, tiles_m, tiles_n, accbuf, grad, first, last,
-                     sa, sb, labels, W, V);
-}
-
-// bf16 backward part 1, label-referenced: the chunk's logits transposed (vocab rows x token
-// columns, as in the forward), then for token t (local row of the block), with r_t its label
-// logit, e_tv = exp(z_tv - r_t) for v != y_t and v < V, zero otherwise. e goes in bf16 into
-// staging [R, ldz] (vocab contiguous), each lane storing 32 bytes per MFMA tile after one
-// half-wave exchange; the tile's per-token sum of e (float32) goes to sig_part[t][vocab tile].
-// A lane whose sum of e exceeds e^64 sets *flag.
-
-template <class C>
-__global__ __launch_bounds__(C::NT) void ce_logit_exp_bf16_kernel(
-    const bf16_t* __restrict__ h, const bf16_t* __restrict__ W, const int32_t* __restrict__ labels,
-    const float* __restrict__ label_logit, int r0, int R, int d, int c0, int cend, int tiles_v,
-    int tiles_t, float* __restrict__ sig_part, int n_vb, bf16_t* __restrict__ ez, int ldz,
-    int* __restrict__ flag) {
-  extern __shared__ __align__(16) uint8_t smem[];
-  int tv, tt;
-  tile_of(blockIdx.x, tiles_v, tiles_t, tv, tt);
-  const int v0 = c0 + tv * C::BM, t0 = tt * C::BN;
-  f32x16 acc[C::TM][C::TN];
-  mfma_mainloop<C>(W + (int64_t)v0 * d, d, cend - v0, h + (int64_t)(r0 + t0) * d, d, R - t0, d,
-                   reinterpret_cast<bf16_t*>(smem), acc);
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-  float* red = reinterpret_cast<float*>(smem);  // [WGM][BN]
-  const int vb = v0 + wm * C::WTM;              // vocab id of this wave's first tile row
-  const bool full = v0 + C::BM <= cend;         // no tile row past the chunk
-  constexpr float kLog2e = 1.4426950408889634f;
-  constexpr float kOverSum = 6.2351491e27f;  // e^64
-  bool over = false;
-#pragma unroll
-  for (int j = 0; j < C::TN; ++j) {
-    const int tl = wn * C::WTN + j * 32 + (lane & 31);
-    const int t = t0 + tl;
-    const bool tok = t < R;
-    float ref = 0.0f;
-    int y = -1;
-    if (tok) {
-      ref = label_logit[r0 + t];
-      y = labels[r0 + t];
-    }
-    const float nref = -ref * kLog2e;
-    const int ylane = y - vb - 4 * (lane >> 5);
-    float sum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < C::TM; ++i) {
-      // Register r holds vocab row 8 (r/4) + 4 (lane/32) + r%4 of the 32-row MFMA tile. The
-      // per-element label and range tests run only when some lane's label lies in this MFMA
-      // tile or the tile crosses the chunk's end.
-      const int yl = ylane - i * 32;
-      const bool mine = yl >= 0 && yl < 32 && (yl & 4) == 0;
-      float e[16];
-      if (!full || __ballot(mine) != 0) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int v = vb + i * 32 + mfma_row(r, lane);
-          e[r] = (v < cend && v != y) ? __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, nref)) : 0.0f;
-        }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, nref));
-      }
-      uint32_t pk[8];
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        sum += e[r];
-        sum += e[r + 1];
-        pk[r >> 1] = pack_bf16x2(e[r], e[r + 1]);
-      }
-      // Lanes 0-31 hold rows {0-3, 8-11, 16-19, 24-27}, lanes 32-63 the other four groups.
-      // Swapping groups {16-19, 24-27} of the low half with {4-7, 12-15} of the high half
-      // leaves rows 0-15 in the low lanes and rows 16-31 in the high lanes, in the same
-      // register order for both.
-      uint32_t P[4] = {pk[0], pk[1], pk[2], pk[3]}, Q[4] = {pk[4], pk[5], pk[6], pk[7]};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const auto sw = __builtin_amdgcn_permlane32_swap(P[k], Q[k], false, false);
-        P[k] = sw[0];
-        Q[k] = sw[1];
-      }
-      if (tok) {
-        u32x4* dst = reinterpret_cast<u32x4*>(ez + (int64_t)t * ldz + (vb - c0) + i * 32 + (lane >> 5) * 16);
-        dst[0] = u32x4{P[0], P[1], Q[0], Q[1]};
-        dst[1] = u32x4{P[2], P[3], Q[2], Q[3]};
-      }
-    }
-    // A single e above e^64 makes the lane's sum exceed it; a sum above it from several
-    // smaller terms only runs the exact path needlessly.
-    over |= sum > kOverSum;
-    sum += __shfl_xor(sum, 32, 64);
-    if (lane < 32) red[wm * C::BN + tl] = sum;
-  }
-  if (over) *flag = 1;
-  __syncthreads();
-  for (int tl = threadIdx.x; tl < C::BN; tl += C::NT) {
-    const int t = t0 + tl;
-    if (t >= R) continue;
-    float sum = red[tl];
-#pragma unroll
-    for (int w = 1; w < C::WGM; ++w) sum += red[w * C::BN + tl];
-    sig_part[(int64_t)(r0 + t) * n_vb + v0 / C::BM] = sum;
-  }
-}
-
-// Rows [r0, r0 + R) after the last chunk's first GEMM: sigma_t = sum of the vocab-tile
-// partials (fixed order), lse_t = r_t + log1p(sigma_t), row loss w_t log1p(sigma_t), and the
-// row scales of the dH epilogue. One wave per row.
+// Rows [r0, r0 + R) after the fused backward: sigma_t = sum of the vocab-tile partials (fixed
+// order), lse_t = r_t + log1p(sigma_t), row loss w_t log1p(sigma_t), and (when sa, sb are given)
+// the row scales coef / (1 + sigma), coef sigma / (1 + sigma). One wave per row.
 __global__ __launch_bounds__(256) void ce_row_final_kernel(int r0, int R, const float* __restrict__ sig_part,
                                                            int n_vb, const float* __restrict__ label_logit,
                                                            const float* __restrict__ weights,
@@ -755,8 +161,8 @@ __global__ __launch_bounds__(256) void ce_row_final_kernel(int r0, int R, const 
     const float c = coef[row];
     lse[row] = label_logit[row] + ce;
     rowloss[row] = weights[row] * ce;
-    sa[row] = c * inv;
-    sb[row] = c * (sum * inv);
+    if (sa) sa[row] = c * inv;
+    if (sb) sb[row] = c * (sum * inv);
   }
 }
 
@@ -846,6 +252,8 @@ __global__ __launch_bounds__(256) void ce_fwd_f32_kernel(const float* __restrict
       const int y = labels[row];
       for (int j = 0; j < 4; ++j)
         if (n0 + tx * 4 + j == y) label_logit[row] = acc[i][j];
+      // outside the contract: the row's loss term becomes NaN instead of reading stale memory
+      if ((y < 0 || y >= V) && tn == 0 && tx == 0) label_logit[row] = __int_as_float(0x7FC00000);
     }
   }
 }
@@ -870,10 +278,11 @@ __global__ __launch_bounds__(256) void ce_dz_f32_kernel(const float* __restrict_
     const int row = r0 + rl;
     const float l = lse[row], c = coef[row];
     const int y = labels[row];
+    const bool bad = y < 0 || y >= V;  // outside the contract: NaN gradient row
     for (int j = 0; j < 4; ++j) {
       const int cl = n0 + tx * 4 + j, col = c0 + cl;
       float g = 0.0f;
-      if (col < V) g = c * (expf(acc[i][j] - l) - (col == y ? 1.0f : 0.0f));
+      if (col < V) g = bad ? __int_as_float(0x7FC00000) : c * (expf(acc[i][j] - l) - (col == y ? 1.0f : 0.0f));
       dz[(int64_t)rl * ldz + cl] = g;
     }
   }
@@ -1123,39 +532,6 @@ hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* W
   return hipGetLastError();
 }
 
-template <class C>
-static hipError_t logit_exp_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels,
-                                 const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
-                                 float* sig_part, int n_vb, bf16_t* ez, int ldz, int* flag,
-                                 hipStream_t s) {
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = allow_big_lds(ce_logit_exp_bf16_kernel<C>);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  const int tv = (Vc + C::BM - 1) / C::BM, tt = (R + C::BN - 1) / C::BN;
-  const int cend = min(c0 + Vc, V);
-  KernelTimer t(K_CE_LOGIT_EXP, s);
-  hipLaunchKernelGGL(ce_logit_exp_bf16_kernel<C>, dim3(tv * tt), dim3(C::NT), C::LDS, s, h, W, labels,
-                     label_logit, r0, R, d, c0, cend, tv, tt, sig_part, n_vb, ez, ldz, flag);
-  return hipGetLastError();
-}
-
-hipError_t launch_ce_logit_exp(CeGemmShape t, const void* h, const void* W, const int32_t* labels,
-                               const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
-                               float* sig_part, int n_vb, void* ez, int ldz, int* flag, hipStream_t s) {
-  if (R == 0) return hipSuccess;
-  const bf16_t* hb = static_cast<const bf16_t*>(h);
-  const bf16_t* Wb = static_cast<const bf16_t*>(W);
-  bf16_t* z = static_cast<bf16_t*>(ez);
-  if (t.bm == 256)
-    return logit_exp_bf16<CfgBig>(hb, Wb, labels, label_logit, r0, R, d, c0, Vc, V, sig_part, n_vb, z, ldz,
-                                  flag, s);
-  return logit_exp_bf16<CfgSmall>(hb, Wb, labels, label_logit, r0, R, d, c0, Vc, V, sig_part, n_vb, z, ldz,
-                                  flag, s);
-}
-
 hipError_t launch_ce_row_final(int r0, int R, const float* sig_part, int n_vb, const float* label_logit,
                                const float* weights, const float* coef, float* lse, float* rowloss,
                                float* sa, float* sb, hipStream_t s) {
@@ -1166,92 +542,25 @@ hipError_t launch_ce_row_final(int r0, int R, const float* sig_part, int n_vb, c
   return hipGetLastError();
 }
 
-template <class C>
-static hipError_t dz_bf16(const bf16_t* h, const bf16_t* W, const int32_t* labels, const float* lse,
-                          const float* coef, int r0, int R, int d, int c0, int Vc, int V, bf16_t* dz,
-                          int ldz, const int* gate, hipStream_t s) {
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = allow_big_lds(ce_dz_bf16_kernel<C>);
-    if (e == hipSuccess) e = allow_big_lds(ce_guard_dz_bf16_kernel<C>);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  const int tm = (R + C::BM - 1) / C::BM, tn = (Vc + C::BN - 1) / C::BN;
-  const int cend = min(c0 + Vc, V);
-  KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DZ, s);
-  if (gate)
-    hipLaunchKernelGGL(ce_guard_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
-                       coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz, gate);
-  else
-    hipLaunchKernelGGL(ce_dz_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, h, W, labels, lse,
-                       coef, r0, R, d, c0, cend, V, tm, tn, dz, ldz);
-  return hipGetLastError();
-}
-
-hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
-                            const int32_t* labels, const float* lse, const float* coef, int r0,
-                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, const int* gate,
+hipError_t launch_ce_bwd_dz(const float* h, const float* W, const int32_t* labels, const float* lse,
+                            const float* coef, int r0, int R, int d, int c0, int Vc, int V, float* dz, int ldz,
                             hipStream_t s) {
   if (R == 0) return hipSuccess;
-  if (dtype == 1) {
-    const bf16_t* hb = static_cast<const bf16_t*>(h);
-    const bf16_t* Wb = static_cast<const bf16_t*>(W);
-    bf16_t* z = static_cast<bf16_t*>(dz);
-    if (t.bm == 256) return dz_bf16<CfgBig>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, gate, s);
-    return dz_bf16<CfgSmall>(hb, Wb, labels, lse, coef, r0, R, d, c0, Vc, V, z, ldz, gate, s);
-  }
   const int tm = (R + kVT - 1) / kVT, tn = (Vc + kVT - 1) / kVT;
   const int cend = min(c0 + Vc, V);
   KernelTimer tt(K_CE_BWD_DZ, s);
-  hipLaunchKernelGGL(ce_dz_f32_kernel, dim3(tm * tn), dim3(256), 0, s, static_cast<const float*>(h),
-                     static_cast<const float*>(W), labels, lse, coef, r0, R, d, c0, cend, V, tm,
-                     static_cast<float*>(dz), ldz);
+  hipLaunchKernelGGL(ce_dz_f32_kernel, dim3(tm * tn), dim3(256), 0, s, h, W, labels, lse, coef, r0, R, d, c0, cend,
+                     V, tm, dz, ldz);
   return hipGetLastError();
 }
 
-template <class C>
-static hipError_t dh_bf16(const bf16_t* dz, int ldz, const bf16_t* WT, int Vp, int r0, int R, int d,
-                          int c0, int K, float* acc, bf16_t* grad, bool first, bool last,
-                          const CeRowScale& rs, const bf16_t* W, int V, const int* gate, hipStream_t s) {
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = allow_big_lds(ce_dh_bf16_kernel<C>);
-    if (e == hipSuccess) e = allow_big_lds(ce_guard_dh_bf16_kernel<C>);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  const int tm = (d + C::BM - 1) / C::BM, tn = (R + C::BN - 1) / C::BN;  // transposed tiles
-  KernelTimer t(gate ? K_CE_GUARD : K_CE_BWD_DH, s);
-  if (gate)
-    hipLaunchKernelGGL(ce_guard_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp,
-                       r0, R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
-                       rs.labels, W, V, gate);
-  else
-    hipLaunchKernelGGL(ce_dh_bf16_kernel<C>, dim3(tm * tn), dim3(C::NT), C::LDS, s, dz, ldz, WT, Vp, r0,
-                       R, d, c0, K, tm, tn, acc, grad, first ? 1 : 0, last ? 1 : 0, rs.sa, rs.sb,
-                       rs.labels, W, V);
-  return hipGetLastError();
-}
-
-hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
-                            const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
-                            float* acc, void* grad, bool first, bool last, const CeRowScale& rs,
-                            const int* gate, hipStream_t s) {
+hipError_t launch_ce_bwd_dh(const float* dz, int ldz, const float* W, int r0, int R, int d, int c0, int K, int V,
+                            float* grad, bool first, hipStream_t s) {
   if (R == 0) return hipSuccess;
-  if (dtype == 1) {
-    const bf16_t* z = static_cast<const bf16_t*>(dz);
-    const bf16_t* wt = static_cast<const bf16_t*>(WT);
-    const bf16_t* w = static_cast<const bf16_t*>(W);
-    bf16_t* g = static_cast<bf16_t*>(grad);
-    if (t.bm == 256) return dh_bf16<CfgBig>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, rs, w, V, gate, s);
-    return dh_bf16<CfgSmall>(z, ldz, wt, Vp, r0, R, d, c0, K, acc, g, first, last, rs, w, V, gate, s);
-  }
   const int tm = (R + kVT - 1) / kVT, tn = (d + kVT - 1) / kVT;
   KernelTimer tt(K_CE_BWD_DH, s);
-  hipLaunchKernelGGL(ce_dh_f32_kernel, dim3(tm * tn), dim3(256), 0, s, static_cast<const float*>(dz),
-                     ldz, static_cast<const float*>(W), r0, R, d, c0, K, V - c0, tm,
-                     static_cast<float*>(grad), first ? 1 : 0);
+  hipLaunchKernelGGL(ce_dh_f32_kernel, dim3(tm * tn), dim3(256), 0, s, dz, ldz, W, r0, R, d, c0, K, V - c0, tm, grad,
+                     first ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -7,6 +7,8 @@
 
 namespace attt {
 
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
 // ---- kernel timing ---------------------------------------------------------------------
 enum KernelId {
   K_NGRAM_COUNT = 0,
@@ -18,7 +20,6 @@ enum KernelId {
   K_CE_HEAD_T,
   K_CE_BWD_DZ,
   K_CE_BWD_DH,
-  K_CE_LOGIT_EXP,
   K_CE_GUARD,
   K_LORA_U,
   K_LORA_DADB,
@@ -26,6 +27,7 @@ enum KernelId {
   K_NGRAM_SET,
   K_NGRAM_SET_WEIGHT,
   K_LORA_SGD,
+  K_CE_FUSED,
   K_NUM_KERNELS
 };
 
@@ -157,35 +159,52 @@ hipError_t launch_ce_coef(const CeEpBatch& b, int total_blocks, const float* wei
                           hipStream_t s);
 // W [V, d] -> WT [d, Vp] (bf16 only), zero columns V .. Vp-1.
 hipError_t launch_ce_head_transpose(const void* W, int V, int d, int Vp, void* WT, hipStream_t s);
-// bf16, label-referenced: e = exp(z - z_y) (0 at the label and past V) for rows [r0, r0+R) x
-// vocab [c0, c0+Vc) into staging [R, ldz]; per (row, vocab tile of t.bm) sums into
-// sig_part [N, n_vb]; sets *flag when a logit exceeds its reference by more than 64.
-hipError_t launch_ce_logit_exp(CeGemmShape t, const void* h, const void* W, const int32_t* labels,
-                               const float* label_logit, int r0, int R, int d, int c0, int Vc, int V,
-                               float* sig_part, int n_vb, void* ez, int ldz, int* flag, hipStream_t s);
 // Rows [r0, r0+R): sigma, lse, row loss and the dH row scales (sa, sb).
 hipError_t launch_ce_row_final(int r0, int R, const float* sig_part, int n_vb, const float* label_logit,
                                const float* weights, const float* coef, float* lse, float* rowloss,
                                float* sa, float* sb, hipStream_t s);
-// dZ chunk: rows [r0, r0+R) x vocab [c0, c0+Vc) of coef * (softmax - onehot), into
-// staging [R, ldz] (dtype), zero past V.
-hipError_t launch_ce_bwd_dz(int dtype, CeGemmShape t, const void* h, const void* W,
-                            const int32_t* labels, const float* lse, const float* coef, int r0,
-                            int R, int d, int c0, int Vc, int V, void* dz, int ldz, const int* gate,
+// float32 backward: dZ chunk, rows [r0, r0+R) x vocab [c0, c0+Vc) of coef * (softmax - onehot)
+// into staging [R, ldz], zero past V; then dH rows [r0, r0+R) (+)= dZ chunk . W[c0 : c0+K]
+// (first: overwrite).
+hipError_t launch_ce_bwd_dz(const float* h, const float* W, const int32_t* labels, const float* lse,
+                            const float* coef, int r0, int R, int d, int c0, int Vc, int V, float* dz, int ldz,
                             hipStream_t s);
-// Row scales of the label-referenced dH epilogue; all null for the plain dZ chunks.
-struct CeRowScale {
-  const float* sa = nullptr;
-  const float* sb = nullptr;
-  const int32_t* labels = nullptr;
+hipError_t launch_ce_bwd_dh(const float* dz, int ldz, const float* W, int r0, int R, int d, int c0, int K, int V,
+                            float* grad, bool first, hipStream_t s);
+
+// Fused bf16 backward (ce_fused.hip): one persistent cooperative grid of 8 x kCeTeam workgroups,
+// one per CU, in XCD teams of kCeTeam producers and consumers sharing a ring of bf16 tiles.
+constexpr int kCeTeam = 32;
+struct CeFusedArgs {
+  const bf16_t* h;            // [N, d]
+  const bf16_t* W;            // [V, d]
+  const bf16_t* WT;           // [d, Vp], columns V .. Vp-1 zero
+  const int32_t* labels;      // [N]
+  const float* label_logit;   // [N]  label mode
+  const float* lse;           // [N]  exact mode
+  const float* coef;          // [N]  w / L_e
+  float* sig_part;            // [N, nv] per-(row, vocab tile) sums of e, label mode
+  bf16_t* grad;               // [N, d]
+  uint8_t* ring;              // 8 x slots tiles of 256 x 256 bf16
+  int* sync;                  // zeroed sync area of ce_fused_sync_ints(slots) ints
+  int* gate;                  // guard flag: set on overflow (label mode); exact mode runs only if set
+  uint64_t limit;             // bound of every wait, ticks of the 100 MHz wall clock
+  int N, d, V, Vp;
+  int nv;                     // vocabulary tiles of 256
+  int row_tiles;              // row tiles of 256
+  int slices;                 // d-slices of 256
+  int consumers;              // consumers per team (<= slices); producers = kCeTeam - consumers
+  int passes;                 // ceil(slices / consumers): the row tile's tiles are made once per pass
+  int slots;                  // ring slots per XCD
+  int items_max;              // items of the busiest team, rounded up to a multiple of 4
 };
-// dH rows [r0, r0+R) (+)= staged chunk . W[c0 : c0+K]: f32 path reads W [V, d]; bf16 path reads
-// WT [d, Vp]. first: no accumulator read; last: write grad (dtype) instead of acc (f32), with
-// the row scales when rs.sa is set (bf16 only).
-hipError_t launch_ce_bwd_dh(int dtype, CeGemmShape t, const void* dz, int ldz, const void* W,
-                            const void* WT, int Vp, int r0, int R, int d, int c0, int K, int V,
-                            float* acc, void* grad, bool first, bool last, const CeRowScale& rs,
-                            const int* gate, hipStream_t s);
+size_t ce_fused_ring_bytes(int slots);
+int ce_fused_sync_ints(int slots, int items_max);
+hipError_t launch_ce_sync_clear(int* sync, int n, hipStream_t s);
+hipError_t launch_ce_fused(bool label, const CeFusedArgs& a, hipStream_t s);
+hipError_t launch_ce_fused_status(const int* sync, int* gate, hipStream_t s);
+hipError_t launch_ce_fused_nan(const int* sync, float* loss, int E, float* lse, int N, void* grad, int64_t nd,
+                               hipStream_t s);
 
 // ---- LoRA ------------------------------------------------------------------------------
 constexpr int kLoraRowTile = 128;  // row padding of the transposed pass-1 results
@@ -197,8 +216,8 @@ constexpr int kLoraMaxTiles = 4;   // rank tiles of 16 per job (64 ranks)
 constexpr int kLoraJobBatch = 16;  // jobs per launch (kernel-argument descriptors)
 
 // Pass 1: rows of `src` [rows, kdim] times up to four rank tiles of row-major adapter
-// operands [rank, kdim] (A, or B^T in the workspace); tile t writes scale * (src op^T)^T as
-// [16, rows_pad] (operand dtype) at workspace offset out_off.
+// operands [rank, kdim] (A, or B^T in the workspace); tile t writes scale * (src op^T)^T at
+// workspace offset out_off: float32 [16, rows_pad], or bf16 planes hi, lo [2][16, rows_pad].
 struct LoraP1Tile {
   const void* op;   // first row of the tile in its operand
   int64_t out_off;
@@ -212,8 +231,9 @@ struct LoraP1Job {
   LoraP1Tile t[kLoraMaxTiles];
 };
 
-// Pass 2: out[c, k] = sum_t L[c, t] src[t, k] per rank tile; L is a pass-1 result [16, rows_pad]
-// at lt_off; float32 partials [splits, 16, cols] at part_off.
+// Pass 2: out[c, k] = sum_t L[c, t] src[t, k] per rank tile; L is a pass-1 result at lt_off
+// (bf16: planes hi and lo, [2][16, rows_pad]; float32: [16, rows_pad]); float32 partials
+// [splits, 16, cols] at part_off.
 struct LoraP2Tile {
   int64_t lt_off;
   int64_t part_off;

@@ -12,11 +12,13 @@
 //     the whole contraction. Rows are 16-byte loads in the MFMA's own k order (each instruction
 //     covers 64 contiguous bytes of 16 rows), two steps in flight; the adapter operand slice of
 //     each step is staged once per workgroup in LDS and shared by its waves. Results are
-//     stored transposed ([16, rows_pad] per tile).
+//     stored transposed, per tile as two bf16 planes hi = RN(v), lo = RN(v - hi) of the float32
+//     value v ([2][16, rows_pad]), so pass 2 contracts with ~16 significant bits.
 //   Pass 2 (lora_p2_*): out[c, k] = sum_t L[c, t] src[t, k] with (L, src) = (s dU^T, x) for dA
 //     and (s U^T, dy) for dB. The contraction runs over rows, the slow index of src, so 64-row
 //     x 64-column tiles of src are written transposed into LDS (two rows per 32-bit store,
-//     double-buffered, one barrier per step) and read back as K-contiguous MFMA operands.
+//     double-buffered, one barrier per step) and read back as K-contiguous MFMA operands; the
+//     step's slice of L (both planes) is staged in LDS once per workgroup beside them.
 //     Rows are split into `splits` ranges whose float32 partials go to the workspace.
 //   Reduce (lora_reduce_kernel): sums the split partials in a fixed order and adds them to
 //     dA [r, d_in] and dB [d_out, r]. No float atomics: results are bit-reproducible.
@@ -150,17 +152,25 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
     step(s, x0);
     if (s + 1 < ns) step(s + 1, x1);
   }
-  // D of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16.
+  // D of a 16x16 tile: lane l, register v -> row 4*(l/16) + v, column l%16. The float32 result
+  // v goes out as two bf16 planes, hi = RN(v) and lo = RN(v - hi) (v - hi is exact in float32),
+  // so pass 2 contracts with hi + lo, about 16 significant bits instead of bf16's 8.
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t >= nt) break;
     bf16_t* outT = reinterpret_cast<bf16_t*>(ws + Jr.t[t].out_off);
     const float scale = Jr.t[t].scale;
     const int r = row0 + g * 4;
-    uint2 pk;
-    pk.x = pack_bf16x2(scale * acc[t][0], scale * acc[t][1]);
-    pk.y = pack_bf16x2(scale * acc[t][2], scale * acc[t][3]);
-    *reinterpret_cast<uint2*>(outT + (int64_t)l16 * Jr.rows_pad + r) = pk;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = scale * acc[t][e];
+    uint2 hi, lo;
+    hi.x = pack_bf16x2(v[0], v[1]);
+    hi.y = pack_bf16x2(v[2], v[3]);
+    lo.x = pack_bf16x2(v[0] - bf16_bits_to_f32(hi.x & 0xFFFFu), v[1] - bf16_bits_to_f32(hi.x >> 16));
+    lo.y = pack_bf16x2(v[2] - bf16_bits_to_f32(hi.y & 0xFFFFu), v[3] - bf16_bits_to_f32(hi.y >> 16));
+    *reinterpret_cast<uint2*>(outT + (int64_t)l16 * Jr.rows_pad + r) = hi;
+    *reinterpret_cast<uint2*>(outT + (int64_t)(16 + l16) * Jr.rows_pad + r) = lo;
   }
 }
 
@@ -169,7 +179,9 @@ __global__ __launch_bounds__(256) void lora_p1_bf16_kernel(LoraP1Batch b, uint8_
 // ------------------------------------------------------------------------------------------
 constexpr int kP2Pitch = kLoraTStep + 8;  // LDS row pitch (bf16) of the transposed tile
 
-__global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_t* __restrict__ ws) {
+size_t lora_p2_lds(int max_nt) { return (size_t)(2 * kLoraColTile + 2 * max_nt * 32) * kP2Pitch * 2; }
+
+__global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, int max_nt, uint8_t* __restrict__ ws) {
   const int ji = find_job(b, (int)blockIdx.x);
   const LoraP2Job& Jr = b.j[ji];
   const int cols = Jr.cols, nt = Jr.nt;
@@ -181,17 +193,26 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
   const int t_begin = sp * tper;
   const int t_end = min(Jr.rows_pad, t_begin + tper);
 
-  __shared__ __align__(16) bf16_t xs[2][kLoraColTile * kP2Pitch];
+  // Dynamic LDS: xs[2][kLoraColTile * kP2Pitch], then lt[2][max_nt][32 * kP2Pitch], the step's
+  // slice of every tile's L (planes hi, lo: 32 rows of kLoraTStep), shared by the workgroup's
+  // four waves, which all contract with the same fragments. max_nt: the batch's largest nt.
+  extern __shared__ __align__(16) uint8_t p2_smem[];
+  bf16_t (*xs)[kLoraColTile * kP2Pitch] = reinterpret_cast<bf16_t (*)[kLoraColTile * kP2Pitch]>(p2_smem);
+  bf16_t* lt_base = reinterpret_cast<bf16_t*>(p2_smem) + 2 * kLoraColTile * kP2Pitch;
+  auto lt = [&](int buf, int t) { return lt_base + (buf * max_nt + t) * (32 * kP2Pitch); };
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
   // staging: rows 2*pr, 2*pr+1 of the step, columns 8*cg .. 8*cg+7 of the tile
   const int pr = tid >> 3, cg = tid & 7;
   const bool cin = col0 + cg * 8 < cols;  // cols % 8 == 0: a column chunk is whole or absent
+  // L staging: plane row lr (hi rows 0-15, lo rows 16-31), 8 consecutive t from 8*lk
+  const int lr = tid >> 3, lk = tid & 7;
   const bf16_t* src = static_cast<const bf16_t*>(Jr.src);
+  // a tile's pass-1 result: planes hi and lo, [2][16][rows_pad] bf16
   __amdgpu_buffer_rsrc_t rl[kLoraMaxTiles];
 #pragma unroll
   for (int t = 0; t < kLoraMaxTiles; ++t)
-    rl[t] = buffer_rsrc(ws + (t < nt ? Jr.t[t].lt_off : 0), t < nt ? 16 * Jr.rows_pad * 2 : 0);
+    rl[t] = buffer_rsrc(ws + (t < nt ? Jr.t[t].lt_off : 0), t < nt ? 2 * 16 * Jr.rows_pad * 2 : 0);
 
   f32x4 acc[kLoraMaxTiles];
 #pragma unroll
@@ -199,7 +220,7 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
 
   // Rows of step t0 go through a descriptor based at row t0 (offsets stay small) whose range
   // ends at the input's last row.
-  auto load = [&](int t0, u32x4 (&v)[2], u32x4 (&la)[2][kLoraMaxTiles]) {
+  auto load = [&](int t0, u32x4 (&v)[2], u32x4 (&la)[kLoraMaxTiles]) {
     const int nr = max(0, min(kLoraTStep, Jr.rows - t0));
     const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src + (int64_t)t0 * cols, nr * cols * 2);
 #pragma unroll
@@ -207,18 +228,17 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
       v[e] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, cin ? (uint32_t)((2 * pr + e) * cols + col0 + cg * 8) * 2u : kOOB, 0, 0));
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-      for (int t = 0; t < kLoraMaxTiles; ++t)
-        if (t < nt)  // uniform: a job's tile count; unused tiles issue no load
-          la[ks][t] = __builtin_bit_cast(
-              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rl[t], (uint32_t)(l16 * Jr.rows_pad + t0 + ks * 32 + g * 8) * 2u, 0, 0));
+    for (int t = 0; t < kLoraMaxTiles; ++t)
+      if (t < nt)  // uniform: a job's tile count; unused tiles issue no load
+        la[t] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rl[t], (uint32_t)(lr * Jr.rows_pad + t0 + lk * 8) * 2u, 0, 0));
   };
-  u32x4 v0[2], v1[2], la0[2][kLoraMaxTiles], la1[2][kLoraMaxTiles];
-  // One step: store its rows transposed (row pairs as 32-bit words) into buffer `buf`, one
-  // barrier, two MFMA k-steps of 32 rows. Buffer `buf` was last read two steps earlier,
-  // before the previous step's barrier.
-  auto step = [&](int buf, const u32x4 (&v)[2], const u32x4 (&la)[2][kLoraMaxTiles]) {
+  u32x4 v0[2], v1[2], la0[kLoraMaxTiles], la1[kLoraMaxTiles];
+  // One step: store its rows transposed (row pairs as 32-bit words) into buffer `buf` and the L
+  // slices into lt[buf], one barrier, two MFMA k-steps of 32 rows, each as the hi and then the
+  // lo plane of L. Both buffers `buf` were last read two steps earlier, before the previous
+  // step's barrier.
+  auto step = [&](int buf, const u32x4 (&v)[2], const u32x4 (&la)[kLoraMaxTiles]) {
     uint32_t* dst = reinterpret_cast<uint32_t*>(xs[buf]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -227,6 +247,9 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
       dst[((cg * 8 + 2 * e) * kP2Pitch + 2 * pr) >> 1] = lo0 | (lo1 << 16);
       dst[((cg * 8 + 2 * e + 1) * kP2Pitch + 2 * pr) >> 1] = hi0 | (hi1 << 16);
     }
+#pragma unroll
+    for (int t = 0; t < kLoraMaxTiles; ++t)
+      if (t < nt) *reinterpret_cast<u32x4*>(lt(buf, t) + lr * kP2Pitch + lk * 8) = la[t];
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -235,7 +258,11 @@ __global__ __launch_bounds__(256) void lora_p2_bf16_kernel(LoraP2Batch b, uint8_
 #pragma unroll
       for (int t = 0; t < kLoraMaxTiles; ++t) {
         if (t >= nt) break;
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, la[ks][t]), bv, acc[t], 0, 0, 0);
+#pragma unroll
+        for (int hl = 0; hl < 2; ++hl) {
+          const u32x4 a = *reinterpret_cast<const u32x4*>(lt(buf, t) + (hl * 16 + l16) * kP2Pitch + ks * 32 + g * 8);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), bv, acc[t], 0, 0, 0);
+        }
       }
     }
   };
@@ -395,8 +422,10 @@ hipError_t launch_lora_pass1(int dtype, int nt, const LoraP1Batch& b, int blocks
 hipError_t launch_lora_pass2(int dtype, const LoraP2Batch& b, int blocks, uint8_t* ws, hipStream_t s) {
   if (blocks <= 0) return hipSuccess;
   KernelTimer t(K_LORA_DADB, s);
+  int max_nt = 1;
+  for (int i = 0; i < b.count; ++i) max_nt = max(max_nt, b.j[i].nt);
   if (dtype == 1)
-    hipLaunchKernelGGL(lora_p2_bf16_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
+    hipLaunchKernelGGL(lora_p2_bf16_kernel, dim3(blocks), dim3(256), lora_p2_lds(max_nt), s, b, max_nt, ws);
   else
     hipLaunchKernelGGL(lora_p2_f32_kernel, dim3(blocks), dim3(256), 0, s, b, ws);
   return hipGetLastError();

@@ -212,3 +212,47 @@ def test_ngram_set_validation(L):
     assert L.attt_ngram_set_weights(s, FAKE, tp, 1, 100, 3, 0.0, None, FAKE, None) == attt.EINVAL
     assert L.attt_ngram_set_weights(s, FAKE, tp, 1, 100, 3, 0.05, None, None, None) == attt.EINVAL
     assert b"weights is null" in L.attt_last_error()
+
+
+def test_ce_limits_and_flags(L):
+    # the bf16 backward's transposed head is read through a 1 GiB descriptor: V <= 2^21 - 256
+    assert _ce(L, V=(1 << 21) - 255) == attt.EUNSUPPORTED
+    assert b"V <=" in L.attt_last_error()
+    out = ctypes.c_size_t(0)
+    assert L.attt_ce_workspace_size(16, 64, (1 << 21) - 255, attt.BF16, 1, ctypes.byref(out)) == attt.EUNSUPPORTED
+    assert L.attt_ce_workspace_size(16, 64, (1 << 21) - 255, attt.BF16, 0, ctypes.byref(out)) == attt.OK
+    assert L.attt_ce_workspace_size(16, 64, 100, attt.BF16, 4, ctypes.byref(out)) == attt.EINVAL
+
+
+def test_ce_prepared_head(L):
+    d, V = 4096, 128256
+    assert attt.ce_head_t_size(d, V) == d * 128256 * 2            # V is already a multiple of 256
+    assert attt.ce_head_t_size(64, 1000) == 64 * 1024 * 2
+    with_t = attt.ce_workspace_size(8192, d, V, attt.BF16, want_grad=True, head_t=True)
+    plain = attt.ce_workspace_size(8192, d, V, attt.BF16, want_grad=True)
+    assert plain - with_t == d * 128256 * 2                       # the per-call copy is gone
+    FAKE_T = ctypes.c_void_p(0x7F0000002000)
+    assert L.attt_ce_head_transpose(None, 64, 100, FAKE_T, 1 << 20, None) == attt.EINVAL
+    assert L.attt_ce_head_transpose(FAKE, 64, 100, ctypes.c_void_p(0x7F0000002008), 1 << 20, None) == attt.EINVAL
+    assert L.attt_ce_head_transpose(FAKE, 64, 100, FAKE_T, 64 * 256 * 2 - 1, None) == attt.ENOSPACE
+    assert L.attt_ce_head_transpose(FAKE, 60, 100, FAKE_T, 1 << 20, None) == attt.EINVAL
+    _, op = _off((0, 16))
+    # a prepared head only applies to the bf16 backward
+    assert L.attt_weighted_ce_fwd_bwd_ex(FAKE, FAKE, FAKE_T, FAKE, FAKE, op, 1, 16, 64, 100, attt.F32, FAKE,
+                                         None, FAKE, FAKE_WS, 1 << 40, None) == attt.EINVAL
+    assert L.attt_weighted_ce_fwd_bwd_ex(FAKE, FAKE, FAKE_T, FAKE, FAKE, op, 1, 16, 64, 100, attt.BF16, FAKE,
+                                         None, None, FAKE_WS, 1 << 40, None) == attt.EINVAL
+    assert L.attt_weighted_ce_fwd_bwd_ex(FAKE, FAKE, ctypes.c_void_p(0x7F0000002004), FAKE, FAKE, op, 1, 16, 64,
+                                         100, attt.BF16, FAKE, None, FAKE, FAKE_WS, 1 << 40, None) == attt.EINVAL
+
+
+def test_lora_row_limit(L):
+    # pass 2 addresses a rank tile's [16, rows_pad] operand through one 32-bit descriptor
+    assert _lora(L, rows=1 << 24) == attt.EUNSUPPORTED
+    assert b"rows < 2^24" in L.attt_last_error()
+
+
+def test_ce_wait_limit_validation(L):
+    assert L.attt_ce_set_wait_limit(-1, 10) == attt.EINVAL
+    assert L.attt_ce_set_wait_limit(10, -1) == attt.EINVAL
+    assert L.attt_ce_set_wait_limit(20000, 20000) == attt.OK

@@ -1,15 +1,16 @@
 """GPU parity at the full workload sizes (Llama-8B shape, long-trajectory Qwen-14B shape,
 16-episode stuck-agent batch), in the launch configuration the bench times.
 
-n-gram exposure and weights are compared in full (bit-exact). The LM-head CE is compared on
-sampled rows computed one by one by the oracle (lse and dL/dh rows), and the loss through a
-property that holds at any size: loss_e = (1/L_e) sum_t w_t (lse_t - z_{t,y_t}) with the
-label logits from the oracle and the GPU's lse (itself checked on the sampled rows). LoRA
-gradients are compared on sampled columns of dA and rows of dB."""
+n-gram exposure and weights are compared in full (bit-exact). The LM-head CE is compared
+against the float64 oracle on every row for lse and the per-episode loss; dL/dh is compared
+on every row at the Llama-8B shape, and at the two larger shapes on one row in every 64 plus
+the first and last row of every episode (the oracle's dL/dh over all rows would take minutes
+there). LoRA gradients are compared in full: whole-matrix and per-row cosine, and every
+element against the bound of the oracle-sized tests."""
 import numpy as np
 import pytest
 
-from gpu_util import cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
+from gpu_util import check_rows, cosine, dev_dense, dev_f32, dev_i32, host, note
 from oracle import ce as oce
 from oracle import lora as olora
 from oracle import ngram as ongram
@@ -18,6 +19,10 @@ from workloads import Workload
 pytestmark = pytest.mark.gpu
 
 CONFIGS = ["c3", "c4", "c5"]
+BF16_COS = 0.999
+BF16_ELEM = 2.0 ** -7
+LSE_RTOL = 1e-4
+LOSS_RTOL = 1e-4      # stricter than the bf16 loss bar of 2e-2: lse is float32-accurate
 
 
 @pytest.fixture(scope="module", params=CONFIGS)
@@ -36,7 +41,14 @@ def test_ngram_full(attt, wl):
     assert np.array_equal(host(w).view(np.uint32), wo.view(np.uint32))
 
 
-def test_ce_full_sampled(attt, wl):
+def _sampled_rows(off, N, every):
+    starts = np.asarray(off[:-1], np.int64)
+    ends = np.asarray(off[1:], np.int64)
+    keep = ends > starts
+    return np.unique(np.concatenate([np.arange(every // 2, N, every), starts[keep], ends[keep] - 1]))
+
+
+def test_ce_full(attt, wl):
     cfg = wl.cfg
     tok, ce = wl.tokens(), wl.ce()
     _, w = ongram.ngram_weights(tok["history"], tok["updates"], cfg.n, cfg.w_min)
@@ -44,31 +56,31 @@ def test_ce_full_sampled(attt, wl):
     loss, lse, dH = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
                                              dev_f32(w), row_offsets=ce["row_offsets"])
     loss, lse, dH = host(loss), host(lse), host(dH)
-    N = cfg.rows
-    rng = np.random.default_rng(17)
-    rows = np.unique(np.concatenate([[0, N - 1], rng.integers(0, N, 14),
-                                     np.asarray(ce["row_offsets"][1:-1], np.int64)]))
-    note(f"oracle rows {cfg.key}: {len(rows)}")
+    N, off = cfg.rows, ce["row_offsets"]
+    full_grad = cfg.key == "c3"
+    note(f"oracle over all {N} rows ({'with' if full_grad else 'without'} dL/dh)")
+    loss_o, lse_o, dH_o = oce.weighted_ce(ce["h"].f32, ce["W"].f32, ce["labels"], w, off, want_grad=full_grad)
+    rel = np.abs(lse - lse_o) / np.abs(lse_o)
+    note(f"lse: max rel err {rel.max():.3e} over {N} rows")
+    assert rel.max() <= LSE_RTOL, int(np.argmax(rel))
+    lrel = np.abs(loss - loss_o) / np.abs(loss_o)
+    note(f"loss: max rel err {lrel.max():.3e} over {cfg.episodes} episodes")
+    assert lrel.max() <= LOSS_RTOL, (loss, loss_o)
+    if full_grad:
+        assert cosine(dH, dH_o) >= BF16_COS
+        check_rows(dH, dH_o, BF16_COS, BF16_ELEM, f"dH {cfg.key} all rows")
+        return
+    rows = _sampled_rows(off, N, 64)
+    note(f"oracle dL/dh on {len(rows)} sampled rows")
     W64 = np.asarray(ce["W"].f32, np.float64)
-    lse_o, _, dH_o = oce.ce_rows(ce["h"].f32, W64, ce["labels"], w, ce["row_offsets"], rows)
-    assert np.max(np.abs(lse[rows] - lse_o) / np.abs(lse_o)) <= 1e-4
-    assert cosine(dH[rows], dH_o) >= 0.999
-    for i in range(len(rows)):
-        assert cosine(dH[rows[i]], dH_o[i]) >= 0.999
-    # label logits by the oracle's definition (z_{t,y_t} = h_t . W_{y_t}), in row chunks
-    h = ce["h"].f32
-    zy = np.empty(N, np.float64)
-    for s in range(0, N, 4096):
-        e = min(N, s + 4096)
-        zy[s:e] = np.einsum("ij,ij->i", h[s:e].astype(np.float64), W64[ce["labels"][s:e]])
-    off = ce["row_offsets"]
-    for e in range(cfg.episodes):
-        a, b = int(off[e]), int(off[e + 1])
-        want = np.sum(w[a:b].astype(np.float64) * (lse[a:b].astype(np.float64) - zy[a:b])) / (b - a)
-        assert abs(loss[e] - want) <= 1e-4 * abs(want), (e, loss[e], want)
+    parts = [oce.ce_rows(ce["h"].f32, W64, ce["labels"], w, off, rows[s:s + 256])[2]
+             for s in range(0, len(rows), 256)]
+    dH_o = np.concatenate(parts)
+    assert cosine(dH[rows], dH_o) >= BF16_COS
+    check_rows(dH[rows], dH_o, BF16_COS, BF16_ELEM, f"dH {cfg.key} sampled rows")
 
 
-def test_lora_full_sampled(attt, wl):
+def test_lora_full(attt, wl):
     import torch
     cfg = wl.cfg
     probs = wl.lora()
@@ -82,30 +94,31 @@ def test_lora_full_sampled(attt, wl):
                         scale=p["scale"], dA=torch.zeros(r, p["d_in"], dtype=torch.float32, device="cuda"),
                         dB=torch.zeros(p["d_out"], r, dtype=torch.float32, device="cuda")))
     attt.lora_grad(dev)
-    rng = np.random.default_rng(5)
-    step = max(1, len(probs) // 8)
-    for p, q in list(zip(probs, dev))[::step]:
-        cols = np.sort(rng.choice(p["d_in"], 64, replace=False))
-        outs = np.sort(rng.choice(p["d_out"], 64, replace=False))
-        dA_o, dB_o = olora.lora_grad_sampled(p["x"].f32, p["dy"].f32, p["A"].f32, p["B"].f32, p["scale"],
-                                             cols, outs)
-        dA = host(q["dA"])[:, cols]
-        dB = host(q["dB"])[outs]
-        assert cosine(dA, dA_o) >= 0.999, p["name"]
-        assert cosine(dB, dB_o) >= 0.999, p["name"]
-        assert rel_norm(dA, dA_o) <= 2e-2 and rel_norm(dB, dB_o) <= 2e-2
+    for p, q in zip(probs, dev):
+        dA_o, dB_o = olora.lora_grad(p["x"].f32, p["dy"].f32, p["A"].f32, p["B"].f32, p["scale"])
+        dA, dB = host(q["dA"]), host(q["dB"])
+        assert cosine(dA, dA_o) >= BF16_COS and cosine(dB, dB_o) >= BF16_COS, p["name"]
+        check_rows(dA, dA_o, BF16_COS, BF16_ELEM, f"dA {p['name']}")
+        check_rows(dB, dB_o, BF16_COS, BF16_ELEM, f"dB {p['name']}")
 
 
 def test_ce_full_deterministic(attt, wl):
-    """The launch configuration the bench times, run twice on the same inputs: loss, lse and
-    dL/dh are bitwise identical (ordered reductions, no float atomics, no scratch)."""
+    """The launch configuration the bench times (prepared head), run four times on the same
+    inputs, plus once with the head transposed inside the call: loss, lse and dL/dh are bitwise
+    identical every time (fixed accumulation orders, no float atomics)."""
+    import torch
     cfg = wl.cfg
     tok, ce = wl.tokens(), wl.ce()
     _, w = ongram.ngram_weights(tok["history"], tok["updates"], cfg.n, cfg.w_min)
     note(f"ce determinism {cfg.key}")
     args = (dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]), dev_f32(w))
-    runs = []
-    for _ in range(2):
-        loss, lse, dH = attt.weighted_ce_fwd_bwd(*args, row_offsets=ce["row_offsets"])
-        runs.append((host(loss).tobytes(), host(lse).tobytes(), host(dH).tobytes()))
-    assert runs[0] == runs[1]
+    head_t = attt.ce_head_transpose(args[1])
+    first = None
+    for rep in range(5):
+        kw = dict(lm_head_t=head_t) if rep < 4 else {}
+        loss, lse, dH = attt.weighted_ce_fwd_bwd(*args, row_offsets=ce["row_offsets"], **kw)
+        out = (host(loss).tobytes(), host(lse).tobytes(), dH.contiguous().view(torch.int16).cpu().numpy().tobytes())
+        if first is None:
+            first = out
+        for what, a, b in zip(("loss", "lse", "dL/dh"), out, first):
+            assert a == b, (cfg.key, rep, what)

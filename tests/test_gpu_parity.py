@@ -3,11 +3,14 @@ sizes the oracle finishes in seconds: the tiny float32 step, the small bf16 mode
 ragged tiles and tails, several episodes, and the degenerate cases of the method.
 
 Bars: f and w bit-exact; float32 loss / lse / gradients within 1e-5 relative (normwise
-for gradients); bf16 loss within 2e-2 relative and gradient cosine >= 0.999."""
+for gradients); bf16 loss within 2e-2 relative, gradient cosine >= 0.999 for the whole
+gradient and for every row of it, and every gradient element within
+2^-7 (|ref| + rms of its row) of the oracle (bf16 output rounding is at most 2^-8 relative,
+and the bf16 operands the kernels stage add an error of the same order)."""
 import numpy as np
 import pytest
 
-from gpu_util import cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
+from gpu_util import check_rows, cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
 from oracle import ce as oce
 from oracle import lora as olora
 from oracle import ngram as ongram
@@ -18,6 +21,7 @@ pytestmark = pytest.mark.gpu
 F32_TOL = 1e-5
 BF16_LOSS_TOL = 2e-2
 BF16_COS = 0.999
+BF16_ELEM = 2.0 ** -7
 
 
 # ------------------------------------------------------------------------------------------
@@ -108,8 +112,7 @@ def _ce_case(attt, h, W, labels, weights, off, bf16):
     if bf16:
         assert np.all(np.abs(loss - lo) <= BF16_LOSS_TOL * np.abs(lo)), (loss, lo)
         assert cosine(dH, dHo) >= BF16_COS
-        for r in range(0, len(dHo), max(1, len(dHo) // 64)):
-            assert cosine(dH[r], dHo[r]) >= 0.99
+        check_rows(dH, dHo, BF16_COS, BF16_ELEM, f"dH {dH.shape}")
     else:
         assert np.all(np.abs(loss - lo) <= F32_TOL * np.abs(lo)), (loss, lo)
         assert rel_norm(dH, dHo) <= F32_TOL
@@ -292,7 +295,9 @@ def _lora_case(attt, problems, bf16, zero_dA=False):
         if bf16:
             if np.any(dAo != 0):
                 assert cosine(dA, dAo) >= BF16_COS
+                check_rows(dA, dAo, BF16_COS, BF16_ELEM, f"dA {dA.shape}")
             assert cosine(dB, dBo) >= BF16_COS
+            check_rows(dB, dBo, BF16_COS, BF16_ELEM, f"dB {dB.shape}")
         else:
             if np.any(dAo != 0):
                 assert rel_norm(dA, dAo) <= F32_TOL
@@ -385,3 +390,96 @@ def test_chained_step_tiny_f32(attt):
     dAo, dBo = out["lora"][0]
     assert rel_norm(host(q["dA"]), dAo) <= F32_TOL
     assert rel_norm(host(q["dB"]), dBo) <= F32_TOL
+
+
+def test_chained_step_small_bf16(attt):
+    """The small bf16 model shape end to end: weights -> weighted CE (loss, dL/dh) -> LoRA of
+    q, k, v, o, the o projection taking the GPU's dL/dh as its upstream gradient, against the
+    oracle's chained step (whose o projection takes the oracle's dL/dh)."""
+    import torch
+    from oracle import step as ostep
+    wl = Workload("c2")
+    cfg = wl.cfg
+    tok, ce, probs = wl.tokens(), wl.ce(), wl.lora()
+    note("chained c2 bf16")
+    _, w = attt.ngram_weights(dev_i32(tok["hist_flat"]), tok["hist_off"], dev_i32(tok["tok_flat"]),
+                              tok["tok_off"], n=cfg.n, w_min=cfg.w_min)
+    loss, lse, dH = attt.weighted_ce_fwd_bwd(dev_dense(ce["h"]), dev_dense(ce["W"]), dev_i32(ce["labels"]),
+                                             w, row_offsets=ce["row_offsets"])
+    xs, dev = {}, []
+    for p in probs:
+        if id(p["x"]) not in xs:
+            xs[id(p["x"])] = dev_dense(p["x"])
+        dy = dH if p["name"].endswith(".o") else dev_dense(p["dy"])
+        r = p["rank"]
+        dev.append(dict(x=xs[id(p["x"])], dy=dy, A=dev_dense(p["A"]), B=dev_dense(p["B"]), scale=p["scale"],
+                        dA=torch.zeros(r, p["d_in"], dtype=torch.float32, device="cuda"),
+                        dB=torch.zeros(p["d_out"], r, dtype=torch.float32, device="cuda")))
+    attt.lora_grad(dev)
+    out = ostep.update_step(tok, ce, probs, cfg.n, cfg.w_min)
+    assert host(w).view(np.uint32).tolist() == out["w"].view(np.uint32).tolist()
+    lo = out["loss"]
+    assert np.all(np.abs(host(loss) - lo) <= BF16_LOSS_TOL * np.abs(lo)), (host(loss), lo)
+    assert np.max(np.abs(host(lse) - out["lse"]) / np.abs(out["lse"])) <= 1e-4
+    check_rows(host(dH), out["dH"], BF16_COS, BF16_ELEM, "chained dH")
+    for p, q, (dAo, dBo) in zip(probs, dev, out["lora"]):
+        dA, dB = host(q["dA"]), host(q["dB"])
+        assert cosine(dA, dAo) >= BF16_COS and cosine(dB, dBo) >= BF16_COS, p["name"]
+        check_rows(dA, dAo, BF16_COS, BF16_ELEM, f"chained dA {p['name']}")
+        check_rows(dB, dBo, BF16_COS, BF16_ELEM, f"chained dB {p['name']}")
+
+
+@pytest.mark.parametrize("shape", [(2048, 2048, 32000), (513, 96, 8200), (96, 64, 131072 + 700)])
+def test_ce_prepared_head_matches(attt, shape):
+    """The head transposed once by attt_ce_head_transpose and passed to the _ex call gives
+    bitwise the outputs of the plain call, which transposes into its workspace."""
+    N, d, V = shape
+    note(f"ce prepared head {shape}")
+    h = random_dense((N, d), 1.0, True, 71)
+    W = random_dense((V, d), 0.05, True, 72)
+    labels = np.random.default_rng(73).integers(0, V, N).astype(np.int32)
+    weights = np.random.default_rng(74).uniform(0.05, 1, N).astype(np.float32)
+    th, tW, tl, tw = dev_dense(h), dev_dense(W), dev_i32(labels), dev_f32(weights)
+    off = np.array([0, N // 2, N], np.int64)
+    plain = [host(t) for t in attt.weighted_ce_fwd_bwd(th, tW, tl, tw, row_offsets=off)]
+    head_t = attt.ce_head_transpose(tW)
+    prep = [host(t) for t in attt.weighted_ce_fwd_bwd(th, tW, tl, tw, row_offsets=off, lm_head_t=head_t)]
+    for a, b in zip(plain, prep):
+        assert a.tobytes() == b.tobytes()
+
+
+def _ce_bf16_small_case(seed, N=700, d=512, V=5000):
+    h = random_dense((N, d), 1.0, True, seed)
+    W = random_dense((V, d), 0.05, True, seed + 1)
+    rng = np.random.default_rng(seed + 2)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    weights = rng.uniform(0.05, 1, N).astype(np.float32)
+    return h, W, labels, weights, np.array([0, 300, N], np.int64)
+
+
+def test_ce_fused_abort_falls_back_to_exact(attt):
+    """The label-referenced pass of the persistent backward forced to abort (every wait bounded
+    by 0 us, set from the host): the exact pass reruns and the outputs still match the oracle."""
+    h, W, labels, weights, off = _ce_bf16_small_case(81)
+    note("ce fused: label pass aborted on purpose (zero wait bound)")
+    attt.ce_set_wait_limit(0, 20000)
+    try:
+        _ce_case(attt, h, W, labels, weights, off, True)
+    finally:
+        attt.ce_set_wait_limit()
+
+
+def test_ce_fused_both_passes_aborted_give_nan(attt):
+    """Both passes forced to abort: no result is trusted, loss, lse and dL/dh are all NaN."""
+    h, W, labels, weights, off = _ce_bf16_small_case(82)
+    note("ce fused: both passes aborted on purpose (zero wait bounds)")
+    attt.ce_set_wait_limit(0, 0)
+    try:
+        loss, lse, dH = attt.weighted_ce_fwd_bwd(dev_dense(h), dev_dense(W), dev_i32(labels), dev_f32(weights),
+                                                 row_offsets=off)
+        loss, lse, dH = host(loss), host(lse), host(dH)
+    finally:
+        attt.ce_set_wait_limit()
+    assert np.all(np.isnan(loss)) and np.all(np.isnan(lse)) and np.all(np.isnan(dH))
+    # and the next call with the default bounds is correct again
+    _ce_case(attt, h, W, labels, weights, off, True)
