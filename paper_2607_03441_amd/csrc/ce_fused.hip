@@ -6,14 +6,18 @@
 // 32 CUs of each XCD:
 //   producers  compute a 256 (vocab) x 256 (token) logit tile z^T = W h^T on MFMA, turn it into
 //              the tile's share of the gradient (label mode: e = exp(z - z_y) off the label, the
-//              softmax numerators referenced to the label logit; exact mode: coef exp(z - lse))
-//              in bf16, and publish it into a slot of a small ring that stays in the XCD's L2;
+//              softmax numerators referenced to the label logit; exact mode: coef p with
+//              p = exp(z - lse), for rows with p_y > 1/2 coef (p - onehot(y)), the label entry's
+//              p_y - 1 formed in float32) in bf16, and publish it into a slot of a small ring that
+//              stays in the XCD's L2;
 //   consumers  own one 256-column slice of d for a 256-row tile and accumulate
 //              acc (+)= W^T[slice, vocab tile] * tile^T in float32 registers over the whole
 //              vocabulary, reading the ring, then write dL/dh = sa acc - sb W_y (label mode:
-//              sa = coef / (1 + sigma), sb = sigma sa, sigma from the producers' per-tile sums;
-//              exact mode: sa = 1, sb = coef). The label term is applied in float32 from W and
-//              never rounded into a bf16 tile.
+//              sa = coef / (1 + sigma), sb = sigma sa, sigma from the producers' per-tile sums,
+//              the label term applied in float32 from W; exact mode: sa = 1, sb = coef, or 0 for
+//              rows whose label term is in the tile). Neither mode rounds a value near coef (the
+//              label entry's p_y of a confident row) to bf16 and subtracts the label term
+//              afterwards: that would leave (1 - p_y) with the absolute error of bf16 at 1.
 // Teams form at run time: every workgroup reads the id of the XCD it runs on, takes a rank in that
 // XCD's team by an atomic counter, and after a grid barrier all workgroups check that every team
 // has exactly kTeam members. Team x works on the row tiles x, x + 8, x + 16, ...; a ring slot is
@@ -93,6 +97,13 @@ __device__ __forceinline__ bool acquire_geq(const int* p, int target, int* abort
   l1_invalidate();
   return ok;
 }
+
+// Exact mode, where the label term -coef W_y of a row goes. Folded into the tile entry
+// coef (p_y - 1) (formed in float32, then rounded to bf16) its error is 2^-9 coef (1 - p_y) |W_y|;
+// kept out (the entry is coef p_y, the consumer subtracts coef W_y in float32) it is
+// 2^-9 coef p_y |W_y|. Fold when p_y = exp(z_y - lse) > 1/2. Producer and consumer take the
+// decision from the same stored z_y and lse, so they always agree.
+__device__ __forceinline__ bool exact_fold(float z_y, float lse) { return z_y - lse > -0.69314718f; }
 
 // The consumer's GEMM: acc += A[0:256, 0:K] T^T with T the ring tiles of items gbase ..
 // gbase + nitems - 1 laid end to end along K (each [256 tokens][256 vocab]); A = W^T rows of the
@@ -336,10 +347,12 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
         const bool tok = tl < R;
         float ref = 0.0f, cf = 0.0f;
         int y = -1;
+        bool fold = false;  // exact mode: the label term goes into the tile (see exact_fold)
         if (tok) {
           y = a.labels[t0 + tl];
           ref = kLabel ? a.label_logit[t0 + tl] : a.lse[t0 + tl];
           cf = kLabel ? 0.0f : a.coef[t0 + tl];
+          if (!kLabel) fold = exact_fold(a.label_logit[t0 + tl], ref);
         }
         const float nref = -ref * kLog2e;
         const int ylane = y - vb - 4 * (lane >> 5);
@@ -358,7 +371,7 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
               const int vv = vb + i * 32 + mfma_row(r, lane);
               const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i][jj][r], kLog2e, nref));
               if (kLabel) e[r] = (vv < a.V && vv != y) ? ex : 0.0f;
-              else e[r] = vv < a.V ? cf * ex : 0.0f;
+              else e[r] = vv < a.V ? cf * ((fold && vv == y) ? ex - 1.0f : ex) : 0.0f;
             }
           } else {
 #pragma unroll
@@ -476,12 +489,12 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
             const float inv = __fdiv_rn(1.0f, 1.0f + sigma);
             sa = cf * inv;
             sb = cf * (sigma * inv);
-          } else {
-            sb = cf;
+          } else if (!exact_fold(a.label_logit[row], a.lse[row])) {
+            sb = cf;  // the label term in float32; a folded one is inside acc already
           }
           const int y = a.labels[row];
-          if (y >= 0 && y < a.V) wy = a.W + (int64_t)y * a.d;
-          else sa = __int_as_float(0x7FC00000);  // outside the contract: NaN row, no read
+          if (y < 0 || y >= a.V) sa = __int_as_float(0x7FC00000);  // outside the contract: NaN row
+          else if (sb != 0.0f) wy = a.W + (int64_t)y * a.d;
         }
 #pragma unroll
         for (int i = 0; i < C::TM; ++i) {

@@ -117,8 +117,25 @@ def test_ce_full_deterministic(attt, wl):
     for rep in range(5):
         kw = dict(lm_head_t=head_t) if rep < 4 else {}
         loss, lse, dH = attt.weighted_ce_fwd_bwd(*args, row_offsets=ce["row_offsets"], **kw)
-        out = (host(loss).tobytes(), host(lse).tobytes(), dH.contiguous().view(torch.int16).cpu().numpy().tobytes())
+        bits = dH.contiguous().view(torch.int16).cpu().numpy()
+        out = (host(loss).tobytes(), host(lse).tobytes(), bits)
         if first is None:
             first = out
-        for what, a, b in zip(("loss", "lse", "dL/dh"), out, first):
+            continue
+        if not np.array_equal(bits, first[2]):
+            _report_mismatch(bits, first[2], cfg.key, rep)
+        for what, a, b in zip(("loss", "lse"), out[:2], first[:2]):
             assert a == b, (cfg.key, rep, what)
+        assert np.array_equal(bits, first[2]), (cfg.key, rep, "dL/dh")
+
+
+def _report_mismatch(bits, ref, key, rep):
+    # which 256-row tiles and 256-column slices of dL/dh differ, and by how much
+    diff = bits != ref
+    rows, cols = np.nonzero(diff)
+    blocks = sorted(set(zip((rows // 256).tolist(), (cols // 256).tolist())))
+    to_f = lambda b: (b.astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    a, b = to_f(bits[rows, cols]), to_f(ref[rows, cols])
+    note(f"{key} call {rep}: {diff.sum()} elements differ in {len(set(rows.tolist()))} rows, "
+         f"{len(blocks)} (row tile, d-slice) blocks {blocks[:16]}; max |diff| {np.max(np.abs(a - b)):.3e}, "
+         f"rows {sorted(set(rows.tolist()))[:16]}")
