@@ -94,6 +94,22 @@ attt_status attt_ngram_weights(const int32_t* history, const int64_t* history_of
                                uint32_t* exposure, float* weights,
                                void* workspace, size_t workspace_bytes, void* stream);
 
+/* attt_ngram_weights_noalloc: attt_ngram_weights without a workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation). Same arguments, results and errors as attt_ngram_weights, except that the scratch
+ * (16-bit partial counts, the size attt_ngram_workspace_size reports) lives in a static device
+ * buffer of ATTT_NGRAM_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends. A call needing more returns ATTT_EUNSUPPORTED (before any HIP call).
+ * Nothing is allocated: no hipMalloc, no hipFree. Every call on one GPU uses that GPU's buffer,
+ * so calls that overlap in time on one GPU (other streams, other host threads) race and give
+ * wrong results; calls ordered on one stream are fine. The buffer needs no initialisation: every
+ * count a call reads was written earlier in the same call. */
+#define ATTT_NGRAM_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+attt_status attt_ngram_weights_noalloc(const int32_t* history, const int64_t* history_offsets,
+                                       const int32_t* tokens, const int64_t* token_offsets,
+                                       int32_t num_episodes, int32_t n, float w_min,
+                                       uint32_t* exposure, float* weights, void* stream);
+
 /* --------------------------------------------------------------------------------------
  * Persistent n-gram sets: the history update of Algorithm 1 (H^tok_{k+1} = H^tok_k followed by
  * x_k) kept as device-resident n-gram counts, so that the weights of the next update (Eq. 8-9)

@@ -11,7 +11,7 @@ import os
 
 import numpy as np
 
-__all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_workspace_size",
+__all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_weights_noalloc", "ngram_workspace_size",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
            "weighted_ce_fwd_bwd", "ce_workspace_size", "ce_head_t_size", "ce_head_transpose", "lora_grad", "lora_workspace_size", "lora_sgd_step",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
@@ -71,6 +71,8 @@ def load():
     L.attt_ngram_workspace_size.argtypes = [p64, p64, i32, i32, psz]
     L.attt_ngram_weights.restype = i32
     L.attt_ngram_weights.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp, sz, vp]
+    L.attt_ngram_weights_noalloc.restype = i32
+    L.attt_ngram_weights_noalloc.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp]
     vpp = ctypes.POINTER(ctypes.c_void_p)
     L.attt_ngram_set_size.restype = i32
     L.attt_ngram_set_size.argtypes = [i64, i32, psz]
@@ -194,6 +196,29 @@ def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.
     ws = _workspace(need.value, dev, workspace)
     _check(L.attt_ngram_weights(_dptr(history), hp, _dptr(tokens), tp, E, n, float(w_min), _dptr(f),
                                 _dptr(w), _dptr(ws), ws.numel(), _stream_ptr()))
+    return f, w
+
+
+def ngram_weights_noalloc(history, history_offsets, tokens, token_offsets, n=3, w_min=0.05,
+                          want_exposure=True, out=None):
+    """ngram_weights through the allocation-free entry point (its scratch is a static device
+    buffer of the library). With `out` given, nothing is allocated on this path either."""
+    torch = _torch()
+    L = load()
+    ho, hp = _offsets(history_offsets)
+    to, tp = _offsets(token_offsets)
+    _dev(tokens, "tokens")
+    _dev(history, "history")
+    if tokens.dtype != torch.int32 or history.dtype != torch.int32:
+        raise TypeError("history and tokens must be int32")
+    T = int(to[-1])
+    if out is not None:
+        f, w = out
+    else:
+        f = torch.empty(T, dtype=torch.int32, device=tokens.device) if want_exposure else None
+        w = torch.empty(T, dtype=torch.float32, device=tokens.device)
+    _check(L.attt_ngram_weights_noalloc(_dptr(history), hp, _dptr(tokens), tp, len(ho) - 1, n, float(w_min),
+                                        _dptr(f), _dptr(w), _stream_ptr()))
     return f, w
 
 

@@ -17,6 +17,8 @@
 
 using namespace attt;
 
+static_assert(kNgramScratchBytes == ATTT_NGRAM_NOALLOC_SCRATCH_BYTES, "header and library agree on the scratch size");
+
 // ------------------------------------------------------------------------------------------
 // Status, messages, timing registry
 // ------------------------------------------------------------------------------------------
@@ -270,6 +272,25 @@ extern "C" attt_status attt_ngram_weights(const int32_t* history, const int64_t*
   if (!aligned256(workspace)) return fail(ATTT_EINVAL, "ngram: workspace must be 256-byte aligned");
   if (token_offsets[num_episodes] == 0) return ATTT_OK;
   return ngram_run(P, history, tokens, num_episodes, n, w_min, exposure, weights, workspace,
+                   static_cast<hipStream_t>(stream));
+}
+
+extern "C" attt_status attt_ngram_weights_noalloc(const int32_t* history, const int64_t* history_offsets,
+                                                  const int32_t* tokens, const int64_t* token_offsets,
+                                                  int32_t num_episodes, int32_t n, float w_min,
+                                                  uint32_t* exposure, float* weights, void* stream) {
+  attt_status st = ngram_check_args(history, history_offsets, tokens, token_offsets, num_episodes, n, w_min,
+                                    weights);
+  if (st) return st;
+  NgramPlan P = ngram_plan(history_offsets, token_offsets, num_episodes, n);
+  if (P.total > kNgramScratchBytes)
+    return fail(ATTT_EUNSUPPORTED,
+                "ngram_noalloc: the call needs %zu bytes of scratch, beyond the static %zu-byte buffer "
+                "(use attt_ngram_weights with a workspace)", P.total, kNgramScratchBytes);
+  if (token_offsets[num_episodes] == 0) return ATTT_OK;
+  void* scratch = nullptr;
+  HIP_TRY(ngram_scratch(&scratch), "ngram_noalloc: scratch address");
+  return ngram_run(P, history, tokens, num_episodes, n, w_min, exposure, weights, scratch,
                    static_cast<hipStream_t>(stream));
 }
 

@@ -93,6 +93,12 @@ struct NgramEpBatch {
   NgramEp e[kEpBatch];
 };
 
+// The allocation-free n-gram entry point keeps its partial counts in a static device array of
+// this many bytes (2048 rows of kQMax 16-bit counts); ngram_scratch gives its address on the
+// current device.
+constexpr size_t kNgramScratchBytes = (size_t)16 << 20;  // ATTT_NGRAM_NOALLOC_SCRATCH_BYTES
+hipError_t ngram_scratch(void** ptr);
+
 size_t ngram_count_lds(int slots, int n);
 hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max_slots,
                               const int32_t* history, const int32_t* tokens, int n,

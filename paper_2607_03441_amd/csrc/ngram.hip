@@ -20,12 +20,38 @@
 // No global atomics and no table in global memory: each workgroup's table lives only in its
 // LDS, and which query position stands for a repeated n-gram (insertion order) never leaves
 // the workgroup. Results are integers, so f and w are bit-reproducible.
+#include <mutex>
 #include <utility>
 
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace attt {
+
+// Scratch of the allocation-free entry point: the partial-count rows of the count kernel live
+// in this file-scope array instead of a caller workspace. Host code never passes the array's
+// name to a kernel (in host code it names a host-side stand-in); it passes the device address
+// that hipGetSymbolAddress returns for the current device, looked up once per device.
+static __device__ __align__(256) uint8_t scratch[kNgramScratchBytes];
+
+hipError_t ngram_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 constexpr uint32_t kEmpty = 0xFFFFFFFFu;  // tag field of a real entry never has bit 31 set
 constexpr int kHistTile = 1984;           // positions per history tile (two tiles per workgroup)

@@ -252,6 +252,26 @@ def test_lora_row_limit(L):
     assert b"rows < 2^24" in L.attt_last_error()
 
 
+def test_ngram_noalloc_validation(L):
+    _, hp = _off([0, 10])
+    _, tp = _off([0, 5])
+    assert L.attt_ngram_weights_noalloc(FAKE, hp, FAKE, tp, 1, 0, 0.05, None, FAKE, None) == attt.EINVAL
+    assert L.attt_ngram_weights_noalloc(FAKE, hp, FAKE, tp, 1, 3, 0.0, None, FAKE, None) == attt.EINVAL
+    assert L.attt_ngram_weights_noalloc(FAKE, hp, FAKE, tp, 1, 3, 0.05, None, None, None) == attt.EINVAL
+    # a call whose partial counts exceed the static scratch is refused before any HIP call:
+    # 64 episodes of 40 partitions (4096 update n-grams each) with at least one history chunk
+    # each give 2560 rows of 8 KiB
+    E = 64
+    hoff = np.arange(E + 1, dtype=np.int64) * 3000
+    toff = np.arange(E + 1, dtype=np.int64) * 40 * 4096
+    need = attt.ngram_workspace_size(hoff, toff, 3)
+    assert need > (16 << 20)
+    _, hp2 = _off(hoff)
+    _, tp2 = _off(toff)
+    assert L.attt_ngram_weights_noalloc(FAKE, hp2, FAKE, tp2, E, 3, 0.05, None, FAKE, None) == attt.EUNSUPPORTED
+    assert b"static" in L.attt_last_error()
+
+
 def test_ce_wait_limit_validation(L):
     assert L.attt_ce_set_wait_limit(-1, 10) == attt.EINVAL
     assert L.attt_ce_set_wait_limit(10, -1) == attt.EINVAL
