@@ -43,6 +43,8 @@
 namespace attt {
 
 constexpr int kSlotBytes = 256 * 256 * 2;  // one bf16 tile [256 tokens][256 vocab]
+// dynamic LDS: the mainloops' two stage buffers, then the producer's per-token sums [2][256]
+constexpr size_t kFusedLds = CfgBig::LDS + 2 * 256 * sizeof(float);
 
 // sync area (ints): team counts [8], arrive, abort, the site of the first wait that ran out
 // (diagnostics: 1 grid barrier, 2 consumer awaiting a tile, 3 producer awaiting a free slot,
@@ -116,18 +118,16 @@ template <class C>
 __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                                   const uint8_t* ring, int nval, int nitems, int gbase, int S,
                                                   const int* published, int* consumed, int* abort, uint64_t limit,
-                                                  bf16_t* lds, f32x16 (&acc)[C::TM][C::TN], int tid) {
+                                                  bf16_t* lds, Acc16& acc, int tid) {
   static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4 && C::BN == 256, "8 waves over 256-token tiles");
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int grp = wave >> 2;
 #pragma unroll
-  for (int i = 0; i < C::TM; ++i)
+  for (int i = 0; i < Mma16::TM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int j = 0; j < Mma16::TN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   const __amdgpu_buffer_rsrc_t rA = make_rsrc(A);
   const __amdgpu_buffer_rsrc_t rR = buffer_rsrc(ring, S * kSlotBytes);
@@ -169,38 +169,13 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
                                                ok ? off : kOOB, 0, 0, 1);
     }
   };
-  const int l32 = lane & 31, hi = lane >> 5;
-  const int swz = (l32 >> 1) & 7;
-  const int arow = (wm * C::WTM + l32) * 64, brow = (wn * C::WTN + l32) * 64;
-  bf16x8 fa[4][C::TM], fb[4][C::TN];
+  bf16x8 fa[2][Mma16::TM], fb[2][Mma16::TN];
   auto mem = [&](int k) {
     const bf16_t* As = lds + (k & 1) * (C::SA + C::SB);
-    const bf16_t* Bs = As + C::SA;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int sw = ((kk * 2 + hi) ^ swz) << 3;
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-        fa[kk][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 32 * 64 + sw));
-#pragma unroll
-      for (int j = 0; j < C::TN; ++j)
-        fb[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 32 * 64 + sw));
-    }
+    mma16_frags<C>(As, As + C::SA, lane, wm, wn, fa, fb);
   };
-  auto compute = [&]() {
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][i], fb[kk][j], acc[i][j], 0, 0, 0);
-  };
-  auto pin = [&]() {
-    static_assert(C::TM == 4 && C::TN == 2, "pin lists the 8 accumulators of a 128x64 wave tile");
-    asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[1][0]), "+v"(acc[1][1]),
-                 "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[3][0]), "+v"(acc[3][1]));
-  };
+  auto compute = [&]() { mma16_step(fa, fb, acc); };
+  auto pin = [&]() { mma16_pin(acc); };
   auto slot_of = [&](int item) { return (gbase + item) % S; };
   // Items [0, known) of this mainloop are known to be published. ensure(i) makes item i known:
   // one 16-byte memory-side load (sc1, as a relaxed agent-scope atomic load is) reads the
@@ -329,21 +304,33 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
       const int t0 = (x + 8 * j) * 256, v0 = v * 256;
       const int R = min(256, a.N - t0);
       const int slot = g % S;
-      f32x16 acc[C::TM][C::TN];
-      mfma_mainloop_pp<C>(a.W + (int64_t)v0 * a.d, a.d, a.V - v0, a.h + (int64_t)t0 * a.d, a.d, R, a.d, lds, acc,
-                          tix);
+      Acc16 acc;
+      // the first stages of every item after the first were issued during the previous epilogue
+      mfma_mainloop_pp16<C>(a.W + (int64_t)v0 * a.d, a.d, a.V - v0, a.h + (int64_t)t0 * a.d, a.d, R, a.d, lds, acc,
+                          tix, g != rank);
       // the slot's previous use must have been read by every consumer (four waves each)
       wait_geq(consumed + slot, 4 * Cn * (g / S), abort, a.limit, kSiteSlot);
+      // start the next item's first stages now, so that their latency hides behind this epilogue
+      // (they land before the publish below; an abort at the next item's check finds them landed)
+      if (g + P < items) {
+        const int gn = g + P, jn = gn / per_tile, vn = gn % per_tile % a.nv;
+        const int t0n = (x + 8 * jn) * 256, v0n = vn * 256;
+        mfma_pp_prologue<C>(a.W + (int64_t)v0n * a.d, a.d, a.V - v0n, a.h + (int64_t)t0n * a.d, a.d,
+                            min(256, a.N - t0n), a.d, lds, tix);
+      }
       bf16_t* tile = reinterpret_cast<bf16_t*>(ring + (size_t)slot * kSlotBytes);
-      float* red = reinterpret_cast<float*>(smem);  // [WGM][256] per-token sums of the tile
+      // [WGM][256] per-token sums of the tile, after the two stage buffers (which hold the next
+      // item's first stages by now)
+      float* red = reinterpret_cast<float*>(smem + C::LDS);
       const int vb = v0 + wm * C::WTM;
       const bool full = v0 + C::BM <= a.V;
       constexpr float kLog2e = 1.4426950408889634f;
       constexpr float kOverSum = 6.2351491e27f;  // e^64
+      const int q4 = lane >> 4;
       bool over = false;
 #pragma unroll
-      for (int jj = 0; jj < C::TN; ++jj) {
-        const int tl = wn * C::WTN + jj * 32 + (lane & 31);
+      for (int jj = 0; jj < Mma16::TN; ++jj) {
+        const int tl = wn * C::WTN + jj * 16 + Mma16::col(lane);
         const bool tok = tl < R;
         float ref = 0.0f, cf = 0.0f;
         int y = -1;
@@ -355,59 +342,62 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
           if (!kLabel) fold = exact_fold(a.label_logit[t0 + tl], ref);
         }
         const float nref = -ref * kLog2e;
-        const int ylane = y - vb - 4 * (lane >> 5);
+        const int ylane = y - vb - 4 * q4;  // the label's offset from this lane's first vocab row
         // exact mode, label outside [0, V) (outside the contract): NaN gradient row
         const bool bad = !kLabel && tok && (y < 0 || y >= a.V);
         if (bad) cf = __int_as_float(0x7FC00000);
         float sum = 0.0f;
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i) {
-          const int yl = ylane - i * 32;
-          const bool mine = yl >= 0 && yl < 32 && (yl & 4) == 0;
-          float e[16];
-          if (!full || __ballot(mine) != 0) {
+        for (int i = 0; i < Mma16::TM; i += 2) {
+          uint32_t pk[2][2];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int vv = vb + i * 32 + mfma_row(r, lane);
-              const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i][jj][r], kLog2e, nref));
-              if (kLabel) e[r] = (vv < a.V && vv != y) ? ex : 0.0f;
-              else e[r] = vv < a.V ? cf * ((fold && vv == y) ? ex - 1.0f : ex) : 0.0f;
+          for (int h = 0; h < 2; ++h) {
+            const int yl = ylane - (i + h) * 16;
+            float e[4];
+            if (!full || __ballot(yl >= 0 && yl < 4) != 0) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int vv = vb + (i + h) * 16 + Mma16::row(r, lane);
+                const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i + h][jj][r], kLog2e, nref));
+                if (kLabel) e[r] = (vv < a.V && vv != y) ? ex : 0.0f;
+                else e[r] = vv < a.V ? cf * ((fold && vv == y) ? ex - 1.0f : ex) : 0.0f;
+              }
+            } else {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i + h][jj][r], kLog2e, nref));
+                e[r] = kLabel ? ex : cf * ex;
+              }
             }
-          } else {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i][jj][r], kLog2e, nref));
-              e[r] = kLabel ? ex : cf * ex;
-            }
+            sum += e[0];
+            sum += e[1];
+            sum += e[2];
+            sum += e[3];
+            pk[h][0] = pack_bf16x2(e[0], e[1]);
+            pk[h][1] = pack_bf16x2(e[2], e[3]);
           }
-          uint32_t pk[8];
+          // Lane row q4 holds vocab 4 q4 .. 4 q4 + 3 of tiles i and i + 1. Swapping the odd
+          // 16-lane rows of tile i's words with the even rows of tile i + 1's leaves every even-row
+          // lane with 8 consecutive vocab entries of tile i (its own four, then those of the lane
+          // 16 above) and every odd-row lane with 8 of tile i + 1: one 16-byte store each.
+          uint32_t w[4];
 #pragma unroll
-          for (int r = 0; r < 16; r += 2) {
-            sum += e[r];
-            sum += e[r + 1];
-            pk[r >> 1] = pack_bf16x2(e[r], e[r + 1]);
-          }
-          // Lanes 0-31 hold vocab rows {0-3, 8-11, 16-19, 24-27} of the 32-row MFMA tile, lanes
-          // 32-63 the other four groups; swapping groups {16-19, 24-27} of the low half with
-          // {4-7, 12-15} of the high half leaves rows 0-15 in the low lanes and 16-31 in the high
-          // lanes, in the same register order, so each lane stores 32 contiguous bytes.
-          uint32_t Pw[4] = {pk[0], pk[1], pk[2], pk[3]}, Qw[4] = {pk[4], pk[5], pk[6], pk[7]};
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const auto sw = __builtin_amdgcn_permlane32_swap(Pw[k], Qw[k], false, false);
-            Pw[k] = sw[0];
-            Qw[k] = sw[1];
+          for (int k = 0; k < 2; ++k) {
+            const auto sw = __builtin_amdgcn_permlane16_swap(pk[0][k], pk[1][k], false, false);
+            w[k] = sw[0];
+            w[2 + k] = sw[1];
           }
           if (tok) {
-            u32x4* dst = reinterpret_cast<u32x4*>(tile + tl * 256 + (vb - v0) + i * 32 + (lane >> 5) * 16);
-            dst[0] = u32x4{Pw[0], Pw[1], Qw[0], Qw[1]};
-            dst[1] = u32x4{Pw[2], Pw[3], Qw[2], Qw[3]};
+            const int odd = q4 & 1;
+            const int voff = (vb - v0) + (i + odd) * 16 + 4 * (q4 - odd);
+            *reinterpret_cast<u32x4*>(tile + tl * 256 + voff) = u32x4{w[0], w[1], w[2], w[3]};
           }
         }
         if (kLabel) {
           over |= sum > kOverSum;
+          sum += __shfl_xor(sum, 16, 64);
           sum += __shfl_xor(sum, 32, 64);
-          if (lane < 32) red[wm * C::BN + tl] = sum;
+          if (q4 == 0) red[wm * C::BN + tl] = sum;
         }
       }
       if (kLabel) {
@@ -453,7 +443,7 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
         continue;
       }
       const int m0 = slice * 256;  // first column of dL/dh
-      f32x16 acc[C::TM][C::TN];
+      Acc16 acc;
       consumer_mainloop<C>(a.WT + (int64_t)m0 * a.Vp, a.Vp, a.d - m0, ring, R, a.nv, gbase, S, published,
                            consumed, abort, a.limit, lds, acc, tix);
       // row scales: sigma_t from the producers' per-tile sums in a fixed order (two threads per
@@ -474,10 +464,10 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
         sig[tix] = s;
         __syncthreads();
       }
-      const int hi = lane >> 5;
+      const int q4 = lane >> 4;
 #pragma unroll
-      for (int jj = 0; jj < C::TN; ++jj) {
-        const int tl = wn * C::WTN + jj * 32 + (lane & 31);
+      for (int jj = 0; jj < Mma16::TN; ++jj) {
+        const int tl = wn * C::WTN + jj * 16 + Mma16::col(lane);
         const bool tok = tl < R;
         float sa = 1.0f, sb = 0.0f;
         const bf16_t* wy = nullptr;
@@ -497,12 +487,12 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
           else if (sb != 0.0f) wy = a.W + (int64_t)y * a.d;
         }
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i) {
-          const int cb = m0 + wm * C::WTM + i * 32;
-          uint32_t pk[8];
+        for (int i = 0; i < Mma16::TM; i += 2) {
+          uint32_t pk[2][2];
 #pragma unroll
-          for (int gq = 0; gq < 4; ++gq) {
-            const int cc = cb + 8 * gq + 4 * hi;
+          for (int h = 0; h < 2; ++h) {
+            // this lane's four columns of d in tile i + h
+            const int cc = m0 + wm * C::WTM + (i + h) * 16 + Mma16::row(0, lane);
             float wv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             if (wy && cc + 4 <= a.d) {
               const uint2 u = *reinterpret_cast<const uint2*>(wy + cc);
@@ -513,23 +503,23 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
             }
             float vv[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) vv[e] = sa * acc[i][jj][4 * gq + e] - sb * wv[e];
-            pk[2 * gq] = pack_bf16x2(vv[0], vv[1]);
-            pk[2 * gq + 1] = pack_bf16x2(vv[2], vv[3]);
+            for (int e = 0; e < 4; ++e) vv[e] = sa * acc[i + h][jj][e] - sb * wv[e];
+            pk[h][0] = pack_bf16x2(vv[0], vv[1]);
+            pk[h][1] = pack_bf16x2(vv[2], vv[3]);
           }
-          uint32_t Pw[4] = {pk[0], pk[1], pk[2], pk[3]}, Qw[4] = {pk[4], pk[5], pk[6], pk[7]};
+          // as in the producer: even-row lanes end up with 8 consecutive columns of tile i,
+          // odd-row lanes with 8 of tile i + 1
+          uint32_t w[4];
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const auto sw = __builtin_amdgcn_permlane32_swap(Pw[k], Qw[k], false, false);
-            Pw[k] = sw[0];
-            Qw[k] = sw[1];
+          for (int k = 0; k < 2; ++k) {
+            const auto sw = __builtin_amdgcn_permlane16_swap(pk[0][k], pk[1][k], false, false);
+            w[k] = sw[0];
+            w[2 + k] = sw[1];
           }
-          const int c0w = cb + 16 * hi;
-          if (tok && c0w + 8 <= a.d) {
-            u32x4* dst = reinterpret_cast<u32x4*>(a.grad + (int64_t)(t0 + tl) * a.d + c0w);
-            dst[0] = u32x4{Pw[0], Pw[1], Qw[0], Qw[1]};
-            if (c0w + 16 <= a.d) dst[1] = u32x4{Pw[2], Pw[3], Qw[2], Qw[3]};
-          }
+          const int odd = q4 & 1;
+          const int c8 = m0 + wm * C::WTM + (i + odd) * 16 + 4 * (q4 - odd);
+          if (tok && c8 + 8 <= a.d)
+            *reinterpret_cast<u32x4*>(a.grad + (int64_t)(t0 + tl) * a.d + c8) = u32x4{w[0], w[1], w[2], w[3]};
         }
       }
       __syncthreads();  // sig and the mainloop's LDS are reused by the next pass
@@ -572,10 +562,10 @@ hipError_t launch_ce_fused(bool label, const CeFusedArgs& a, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(ce_fused_bwd_kernel<true>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)CfgBig::LDS);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLds);
     if (e == hipSuccess)
       e = hipFuncSetAttribute(reinterpret_cast<const void*>(ce_fused_bwd_kernel<false>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)CfgBig::LDS);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLds);
     if (e != hipSuccess) return e;
     attr = true;
   }
@@ -584,7 +574,7 @@ hipError_t launch_ce_fused(bool label, const CeFusedArgs& a, hipStream_t s) {
   KernelTimer t(label ? K_CE_FUSED : K_CE_GUARD, s);
   const void* fn = label ? reinterpret_cast<const void*>(ce_fused_bwd_kernel<true>)
                          : reinterpret_cast<const void*>(ce_fused_bwd_kernel<false>);
-  return hipLaunchCooperativeKernel(fn, dim3(8 * kCeTeam), dim3(CfgBig::NT), args, (unsigned)CfgBig::LDS, s);
+  return hipLaunchCooperativeKernel(fn, dim3(8 * kCeTeam), dim3(CfgBig::NT), args, (unsigned)kFusedLds, s);
 }
 
 hipError_t launch_ce_fused_status(const int* sync, int* gate, hipStream_t s) {

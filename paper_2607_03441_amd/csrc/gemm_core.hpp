@@ -1,7 +1,7 @@
 // The bf16 MFMA GEMM core shared by the LM-head kernels: tile order, tile configurations,
 // buffer-descriptor loads and the two mainloops (plain double-buffered for 4 waves, ping-pong
 // for 8 waves), accumulating acc += A[0:BM, 0:K] B[0:BN, 0:K]^T with both operands contiguous
-// along K. MFMA v_mfma_f32_32x32x16_bf16.
+// along K. MFMA v_mfma_f32_32x32x16_bf16, and the ping-pong also on v_mfma_f32_16x16x32_bf16.
 #pragma once
 
 #include "common.hpp"
@@ -171,38 +171,35 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // phase carries a whole stage of load issue.
 // `tid` is the thread's index in the workgroup (a caller inside a loop may pass it through an
 // empty asm so that the per-lane offsets derived from it are not hoisted out of that loop).
+//
+// The stage loads of the ping-pong mainloop: a stage's 64 blocks of 8 rows x 128 bytes are block
+// (wave & 3) + 4 j for j in [0, 16). Blocks j < 8 are A rows, the rest B rows; both groups use the
+// same numbering. Offsets are formed per load: the block's first row is wave-uniform, and the
+// swizzled chunk of a lane depends only on the lane and on the parity of the block.
 template <class C>
-__device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
-                                                 const bf16_t* __restrict__ B, int64_t ldb, int nval,
-                                                 int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN],
-                                                 int tid = (int)threadIdx.x) {
-  static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4, "ping-pong needs 8 waves in 2 groups of 4");
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / C::WGN, wn = wave % C::WGN;
-  const int grp = wave >> 2;
-#pragma unroll
-  for (int i = 0; i < C::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  // A stage's 64 blocks of 8 rows x 128 bytes: block (wave & 3) + 4 j for j in [0, 16). Blocks
-  // j < 8 are A rows, the rest B rows; both groups use the same numbering.
-  const __amdgpu_buffer_rsrc_t rA = make_rsrc(A), rB = make_rsrc(B);
-  constexpr int LW = 4;                               // waves per group
-  constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
-  constexpr int BPW = (ABLK + BBLK) / LW;             // blocks per wave of a group per stage
-  constexpr int kG0 = 6;                              // group 0's share per wave
+struct PpLoader {
+  static constexpr int LW = 4;                        // waves per group
+  static constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
+  static constexpr int BPW = (ABLK + BBLK) / LW;      // blocks per wave of a group per stage
+  static constexpr int kG0 = 6;                       // group 0's share per wave
   static_assert(ABLK % LW == 0 && BBLK % LW == 0 && kG0 < BPW, "stage blocks must split evenly");
-  // Offsets are formed per load: the block's first row is wave-uniform, and the swizzled chunk
-  // of a lane depends only on the lane and on the parity of the block (rows 8b .. 8b+7).
-  const int lr = lane >> 3;
-  const int c_even = (lane & 7) ^ ((lr >> 1) & 7);
-  const int c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
-  const uint32_t la = (uint32_t)(lr * lda * 2), lb = (uint32_t)(lr * ldb * 2);
-  auto dma = [&](int st, int k0, int j0, int j1) {
+  __amdgpu_buffer_rsrc_t rA, rB;
+  int64_t lda, ldb;
+  int mval, nval, K, wave, lr, c_even, c_odd;
+  uint32_t la, lb;
+  __device__ __forceinline__ PpLoader(const bf16_t* A, int64_t lda_, int mval_, const bf16_t* B, int64_t ldb_,
+                                      int nval_, int K_, int tid)
+      : rA(make_rsrc(A)), rB(make_rsrc(B)), lda(lda_), ldb(ldb_), mval(mval_), nval(nval_), K(K_) {
+    const int lane = tid & 63;
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    lr = lane >> 3;
+    c_even = (lane & 7) ^ ((lr >> 1) & 7);
+    c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
+    la = (uint32_t)(lr * lda * 2);
+    lb = (uint32_t)(lr * ldb * 2);
+  }
+  // blocks j in [j0, j1) of this wave for the stage at K offset k0, into LDS stage buffer st
+  __device__ __forceinline__ void issue(bf16_t* lds, int st, int k0, int j0, int j1) const {
     bf16_t* base = lds + st * (C::SA + C::SB);
 #pragma unroll
     for (int j = j0; j < j1; ++j) {
@@ -217,7 +214,46 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
                                                (__attribute__((address_space(3))) void*)(base + blk * 512),
                                                16, ok ? off : kOOB, 0, 0, 0);
     }
-  };
+  }
+  // the loads that precede the loop: group 0 all of stage 0, group 1 its share of stage 1
+  __device__ __forceinline__ void prologue(bf16_t* lds, bool wait_between) const {
+    const int grp = wave >> 2;
+    if (grp == 0) issue(lds, 0, 0, 0, BPW);
+    if (wait_between) __builtin_amdgcn_s_waitcnt(0);
+    if (grp == 1 && K > 64) issue(lds, 1, 64, kG0, BPW);
+  }
+};
+
+// Issues the ping-pong mainloop's prologue loads for a later call with `issued` set: a caller
+// can start the next tile's first stages before it spends time on this tile's epilogue. The
+// LDS stage buffers must be free (the previous mainloop has returned) and must stay untouched
+// until that call.
+template <class C>
+__device__ __forceinline__ void mfma_pp_prologue(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                                 const bf16_t* __restrict__ B, int64_t ldb, int nval, int K,
+                                                 bf16_t* lds, int tid) {
+  PpLoader<C>(A, lda, mval, B, ldb, nval, K, tid).prologue(lds, false);
+}
+
+template <class C>
+__device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                                 const bf16_t* __restrict__ B, int64_t ldb, int nval,
+                                                 int K, bf16_t* lds, f32x16 (&acc)[C::TM][C::TN],
+                                                 int tid = (int)threadIdx.x, bool issued = false) {
+  static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4, "ping-pong needs 8 waves in 2 groups of 4");
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int grp = wave >> 2;
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const PpLoader<C> ld(A, lda, mval, B, ldb, nval, K, tid);
+  constexpr int BPW = PpLoader<C>::BPW, kG0 = PpLoader<C>::kG0;
 
   const int l32 = lane & 31, hi = lane >> 5;
   const int swz = (l32 >> 1) & 7;
@@ -258,15 +294,15 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
   // group 1, one phase later: fragments(k); wait for own reads and loads; loads [kG0, 16) of
   //                        stage k+2 | MFMA(k) |
   // Group 1 takes one extra barrier before its loop, group 0 one after it, so every wave
-  // executes 2 nk + 2 barriers. Group 1's share of stage 1 is issued before the loop.
+  // executes 2 nk + 2 barriers. Group 1's share of stage 1 is issued before the loop (with
+  // `issued`, the caller has issued both prologue loads already, see mfma_pp_prologue).
   const int nk = (K + 63) / 64;
-  if (grp == 0) dma(0, 0, 0, BPW);
-  __builtin_amdgcn_s_waitcnt(0);
-  if (grp == 1 && nk > 1) dma(1, 64, kG0, BPW);
+  if (!issued) ld.prologue(lds, true);
+  else if (grp == 0) __builtin_amdgcn_s_waitcnt(0);  // stage 0 has landed (group 1 waits in its loop)
   wg_barrier();
   if (grp == 0) {
     for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) dma((k + 1) & 1, (k + 1) * 64, 0, kG0);
+      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, 0, kG0);
       mem(k);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
@@ -282,11 +318,123 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     for (int k = 0; k < nk; ++k) {
       mem(k);
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-      if (k + 2 < nk) dma(k & 1, (k + 2) * 64, kG0, BPW);
+      if (k + 2 < nk) ld.issue(lds, k & 1, (k + 2) * 64, kG0, BPW);
       wg_barrier();
       pin();
       compute();
       pin();
+      wg_barrier();
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// The same 8-wave ping-pong on v_mfma_f32_16x16x32_bf16. A wave's 128 x 64 block is 8 x 4 tiles
+// of 16 x 16; register r of lane l of a tile holds row 4 (l / 16) + r, column l % 16 (Mma16).
+// Per FLOP this moves fewer accumulator bytes through the register file than the 32x32x16
+// form, and the chip holds a higher clock for the same work.
+// ------------------------------------------------------------------------------------------
+struct Mma16 {
+  static constexpr int TM = 8, TN = 4;  // 16 x 16 tiles of a 128 x 64 wave block
+  __device__ static __forceinline__ int row(int r, int lane) { return ((lane >> 4) << 2) + r; }
+  __device__ static __forceinline__ int col(int lane) { return lane & 15; }
+};
+using Acc16 = f32x4[Mma16::TM][Mma16::TN];
+
+// Fragments of one K-step (64) from an LDS stage: two K-halves of 32; lane l reads row
+// (l % 16) of each 16-row tile at K chunk 4 kk + l / 16 (8 bf16), through the stage's swizzle.
+template <class C>
+__device__ __forceinline__ void mma16_frags(const bf16_t* As, const bf16_t* Bs, int lane, int wm, int wn,
+                                            bf16x8 (&fa)[2][Mma16::TM], bf16x8 (&fb)[2][Mma16::TN]) {
+  static_assert(C::WTM == 16 * Mma16::TM && C::WTN == 16 * Mma16::TN, "128 x 64 wave blocks");
+  const int l16 = lane & 15, q4 = lane >> 4, swz = (l16 >> 1) & 7;
+  const int arow = (wm * C::WTM + l16) * 64, brow = (wn * C::WTN + l16) * 64;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int sw = ((kk * 4 + q4) ^ swz) << 3;
+#pragma unroll
+    for (int i = 0; i < Mma16::TM; ++i)
+      fa[kk][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(As + arow + i * 16 * 64 + sw));
+#pragma unroll
+    for (int j = 0; j < Mma16::TN; ++j)
+      fb[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(Bs + brow + j * 16 * 64 + sw));
+  }
+}
+
+__device__ __forceinline__ void mma16_step(const bf16x8 (&fa)[2][Mma16::TM], const bf16x8 (&fb)[2][Mma16::TN],
+                                           Acc16& acc) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int i = 0; i < Mma16::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < Mma16::TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[kk][i], fb[kk][j], acc[i][j], 0, 0, 0);
+}
+
+// Ties the accumulators to empty asm statements so that the MFMAs between two pins stay between
+// the barriers around them (MFMAs touch no memory; the compiler could move them across).
+__device__ __forceinline__ void mma16_pin(Acc16& acc) {
+  static_assert(Mma16::TM == 8 && Mma16::TN == 4, "pins list 32 accumulators");
+  asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[0][2]), "+v"(acc[0][3]), "+v"(acc[1][0]),
+               "+v"(acc[1][1]), "+v"(acc[1][2]), "+v"(acc[1][3]), "+v"(acc[2][0]), "+v"(acc[2][1]),
+               "+v"(acc[2][2]), "+v"(acc[2][3]), "+v"(acc[3][0]), "+v"(acc[3][1]), "+v"(acc[3][2]),
+               "+v"(acc[3][3]));
+  asm volatile("" : "+v"(acc[4][0]), "+v"(acc[4][1]), "+v"(acc[4][2]), "+v"(acc[4][3]), "+v"(acc[5][0]),
+               "+v"(acc[5][1]), "+v"(acc[5][2]), "+v"(acc[5][3]), "+v"(acc[6][0]), "+v"(acc[6][1]),
+               "+v"(acc[6][2]), "+v"(acc[6][3]), "+v"(acc[7][0]), "+v"(acc[7][1]), "+v"(acc[7][2]),
+               "+v"(acc[7][3]));
+}
+
+// mfma_mainloop_pp with 16x16x32 MFMAs: the same loads, barriers and phases.
+template <class C>
+__device__ __forceinline__ void mfma_mainloop_pp16(const bf16_t* __restrict__ A, int64_t lda, int mval,
+                                                   const bf16_t* __restrict__ B, int64_t ldb, int nval, int K,
+                                                   bf16_t* lds, Acc16& acc, int tid = (int)threadIdx.x,
+                                                   bool issued = false) {
+  static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4, "ping-pong needs 8 waves in 2 groups of 4");
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int grp = wave >> 2;
+#pragma unroll
+  for (int i = 0; i < Mma16::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < Mma16::TN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  const PpLoader<C> ld(A, lda, mval, B, ldb, nval, K, tid);
+  constexpr int BPW = PpLoader<C>::BPW, kG0 = PpLoader<C>::kG0;
+  bf16x8 fa[2][Mma16::TM], fb[2][Mma16::TN];
+  auto mem = [&](int k) {
+    const bf16_t* As = lds + (k & 1) * (C::SA + C::SB);
+    mma16_frags<C>(As, As + C::SA, lane, wm, wn, fa, fb);
+  };
+  const int nk = (K + 63) / 64;
+  if (!issued) ld.prologue(lds, true);
+  else if (grp == 0) __builtin_amdgcn_s_waitcnt(0);
+  wg_barrier();
+  if (grp == 0) {
+    for (int k = 0; k < nk; ++k) {
+      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, 0, kG0);
+      mem(k);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      wg_barrier();
+      mma16_pin(acc);
+      mma16_step(fa, fb, acc);
+      mma16_pin(acc);
+      __builtin_amdgcn_s_waitcnt(0);
+      wg_barrier();
+    }
+    wg_barrier();
+  } else {
+    wg_barrier();
+    for (int k = 0; k < nk; ++k) {
+      mem(k);
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      if (k + 2 < nk) ld.issue(lds, k & 1, (k + 2) * 64, kG0, BPW);
+      wg_barrier();
+      mma16_pin(acc);
+      mma16_step(fa, fb, acc);
+      mma16_pin(acc);
       wg_barrier();
     }
   }
