@@ -376,6 +376,8 @@ def main():
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved / 1e12, "peak": peak / 1e12,
                 "unit": "TFLOP/s", "frac": achieved / peak,
                 "traffic": counter_traffic(cfg.name, dom),
+                "traffic_source": "rocprofv3 FETCH_SIZE/WRITE_SIZE summary committed under profiles/ "
+                                  "(null unless the CE sources still hash to its recorded values)",
                 "flops_per_launch": per_launch}
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
                 ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_fused_bwd",
