@@ -382,7 +382,7 @@ def main():
     ce_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in
                 ("ce_fwd_lse", "ce_label_logit", "ce_row_reduce", "ce_loss", "ce_head_transpose", "ce_fused_bwd",
                  "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard"))
-    ng_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("ngram_count", "ngram_weight"))
+    ng_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("ngram_table", "ngram_count", "ngram_weight"))
     lo_ms = sum(kern.get(n, {}).get("ms_per_step", 0.0) for n in ("lora_u_du", "lora_dadb", "lora_reduce"))
     parts = {
         "ce_pass": {"ms": ce_ms, "algorithmic_tflops": 4 * cfg.rows * cfg.vocab * cfg.d / (ce_ms * 1e-3) / 1e12,

@@ -48,7 +48,7 @@ static attt_status hip_fail(hipError_t e, const char* where) {
 namespace attt {
 
 static const char* kKernelNames[K_NUM_KERNELS] = {
-    "ngram_count", "ngram_weight", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
+    "ngram_count", "ngram_weight", "ngram_table", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard", "lora_u_du", "lora_dadb",
     "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd"};
 
@@ -169,13 +169,16 @@ static attt_status check_offsets(const char* what, const int64_t* off, int32_t E
 namespace {
 
 struct NgramEpPlan {
-  int64_t tok_base, hist_base, chunk_base;
+  int64_t tok_base, hist_base, chunk_base, part_base;
   int32_t L, Q, hist_ngrams, parts, chunks;
 };
 
+// workspace: partial counts [total_chunks][kQMax] u16, then canon [total_parts][kQMax] u16, then
+// list [total_parts][kQMax] uint2
 struct NgramPlan {
   std::vector<NgramEpPlan> eps;
-  int64_t total_chunks = 0;
+  int64_t total_chunks = 0, total_parts = 0;
+  size_t off_canon = 0, off_list = 0;
   size_t total = 0;
 };
 
@@ -207,7 +210,9 @@ NgramPlan ngram_plan(const int64_t* hoff, const int64_t* toff, int32_t E, int32_
     const int64_t Q = std::max<int64_t>(0, L - n + 1);
     work += ceil_div(Q, kQMax) * std::max<int64_t>(0, H - n + 1);
   }
-  const int64_t chunk_len = std::min<int64_t>(65535, std::max<int64_t>(2048, ceil_div(work, 512)));
+  // one count workgroup per CU (its LDS table takes most of the CU): about 256 chunks in all,
+  // so every workgroup sets its table up once
+  const int64_t chunk_len = std::min<int64_t>(65535, std::max<int64_t>(2048, ceil_div(work, 256)));
   for (int32_t e = 0; e < E; ++e) {
     NgramEpPlan ep{};
     ep.tok_base = toff[e];
@@ -218,10 +223,14 @@ NgramPlan ngram_plan(const int64_t* hoff, const int64_t* toff, int32_t E, int32_
     ep.parts = (int32_t)ceil_div(ep.Q, kQMax);
     ep.chunks = ep.hist_ngrams > 0 ? (int32_t)ceil_div(ep.hist_ngrams, chunk_len) : 0;
     ep.chunk_base = P.total_chunks;
+    ep.part_base = P.total_parts;
     P.total_chunks += (int64_t)ep.parts * ep.chunks;
+    if (ep.chunks > 0) P.total_parts += ep.parts;
     P.eps.push_back(ep);
   }
-  P.total = std::max<size_t>(align256((size_t)P.total_chunks * kQMax * 2), 256);
+  P.off_canon = align256((size_t)P.total_chunks * kQMax * 2);
+  P.off_list = P.off_canon + align256((size_t)P.total_parts * kQMax * 2);
+  P.total = std::max<size_t>(P.off_list + align256((size_t)P.total_parts * kQMax * 8), 256);
   return P;
 }
 
@@ -300,13 +309,17 @@ attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t*
                       hipStream_t s) {
 
   uint16_t* partial = static_cast<uint16_t*>(workspace);
+  uint16_t* canon = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(workspace) + P.off_canon);
+  uint2* list = reinterpret_cast<uint2*>(static_cast<uint8_t*>(workspace) + P.off_list);
 
-  // count kernel: batches of partitions; a partition's chunks are consecutive blocks
+  // table and count kernels: batches of partitions; a partition's chunks are consecutive
+  // count-kernel blocks
   NgramPartBatch batch{};
   int blocks = 0, max_slots = 64;
   auto flush = [&]() -> attt_status {
     if (batch.count == 0) return ATTT_OK;
-    HIP_TRY(launch_ngram_count(batch, blocks, max_slots, history, tokens, n, partial, s), "ngram_count");
+    HIP_TRY(launch_ngram_table(batch, max_slots, tokens, n, canon, list, s), "ngram_table");
+    HIP_TRY(launch_ngram_count(batch, blocks, max_slots, history, tokens, list, n, partial, s), "ngram_count");
     batch = NgramPartBatch{};
     blocks = 0;
     max_slots = 64;
@@ -325,10 +338,11 @@ attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t*
       q.hist_ngrams = ep.hist_ngrams;
       q.q0 = p * kQMax;
       q.qn = std::min(kQMax, ep.Q - p * kQMax);
-      q.slots = std::max(64, next_pow2(2 * q.qn));
+      q.slots = std::max(64, next_pow2(8 * q.qn));  // load factor <= 1/8: a second bucket is rare
       q.chunks = ep.chunks;
       q.chunk_begin = blocks;
       q.chunk_begin_global = ep.chunk_base + (int64_t)p * ep.chunks;
+      q.part_global = ep.part_base + p;
       blocks += ep.chunks;
       max_slots = std::max(max_slots, q.slots);
     }
@@ -345,12 +359,13 @@ attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t*
       const NgramEpPlan& ep = P.eps[e0 + i];
       wb.e[i].tok_base = ep.tok_base;
       wb.e[i].chunk_base = ep.chunk_base;
+      wb.e[i].part_base = ep.part_base;
       wb.e[i].L = ep.L;
       wb.e[i].chunks = ep.chunks;
       wb.e[i].block_begin = wblocks;
       wblocks += (int)ceil_div(ep.L, 256);
     }
-    HIP_TRY(launch_ngram_weight(wb, wblocks, n, w_min, partial, exposure, weights, s), "ngram_weight");
+    HIP_TRY(launch_ngram_weight(wb, wblocks, n, w_min, partial, canon, exposure, weights, s), "ngram_weight");
   }
   return ATTT_OK;
 }

@@ -13,6 +13,7 @@ typedef uint16_t bf16_t;  // raw bfloat16 bits
 enum KernelId {
   K_NGRAM_COUNT = 0,
   K_NGRAM_WEIGHT,
+  K_NGRAM_TABLE,
   K_CE_FWD,
   K_CE_LABEL,
   K_CE_ROW_REDUCE,
@@ -64,10 +65,11 @@ struct NgramPart {
   int64_t tok_base;            // first update token of the episode in `tokens`
   int64_t hist_base;           // first history token of the episode in `history`
   int64_t chunk_begin_global;  // first row of this partition in the partial-count array
+  int64_t part_global;         // index of this partition in the canon / list arrays
   int32_t hist_ngrams;         // history n-gram starts of the episode: max(0, H_e - n + 1)
   int32_t q0;                  // first query start of this partition, relative to the episode
   int32_t qn;                  // query starts in this partition, 1 .. kQMax
-  int32_t slots;               // LDS table size, power of two >= 2 * qn
+  int32_t slots;               // LDS table size, power of two >= 8 * qn (at most 32768)
   int32_t chunk_begin;         // first count-kernel block of this partition within the launch
   int32_t chunks;              // history chunks (count-kernel blocks) of the partition
 };
@@ -81,6 +83,7 @@ struct NgramPartBatch {
 struct NgramEp {
   int64_t tok_base;
   int64_t chunk_base;  // partial-count row of the episode's first partition, first chunk
+  int64_t part_base;   // canon row of the episode's first partition
   int32_t L;
   int32_t chunks;      // chunks per partition (the same for every partition of the episode)
   int32_t block_begin;
@@ -100,12 +103,16 @@ constexpr size_t kNgramScratchBytes = (size_t)16 << 20;  // ATTT_NGRAM_NOALLOC_S
 hipError_t ngram_scratch(void** ptr);
 
 size_t ngram_count_lds(int slots, int n);
+// canon [partitions][kQMax] u16: canonical query position of every query position;
+// list [partitions][kQMax] (table slot or 0xFFFFFFFF for a repeat, entry) per query position
+hipError_t launch_ngram_table(const NgramPartBatch& b, int max_slots, const int32_t* tokens, int n,
+                              uint16_t* canon, uint2* list, hipStream_t s);
 hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max_slots,
-                              const int32_t* history, const int32_t* tokens, int n,
+                              const int32_t* history, const int32_t* tokens, const uint2* list, int n,
                               uint16_t* partial, hipStream_t s);
 hipError_t launch_ngram_weight(const NgramEpBatch& b, int total_blocks, int n, float w_min,
-                               const uint16_t* partial, uint32_t* exposure, float* weights,
-                               hipStream_t s);
+                               const uint16_t* partial, const uint16_t* canon, uint32_t* exposure,
+                               float* weights, hipStream_t s);
 
 // ---- persistent n-gram set ---------------------------------------------------------------
 struct NgramSetJob {
