@@ -10,9 +10,10 @@ Modules:
   ce     -- token-weighted cross-entropy through the LM head and dH (Eq. 10; the gradient step of Algorithm 1)
   lora   -- LoRA dA / dB for one adapted projection (Sec. 3.1; Appendix C)
   step   -- the three chained, as one update step
+  repetition -- update-text repetition rho, novelty nu and the skip filter (Eq. 6-7)
 
 Every function is pinned by tests under tests/test_oracle_*.py against brute force,
 closed forms, library routines (torch CPU cross-entropy and autograd) and finite
 differences; none is "parity unpinned".
 """
-from . import ce, lora, ngram, step  # noqa: F401
+from . import ce, lora, ngram, repetition, step  # noqa: F401
