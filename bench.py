@@ -264,6 +264,43 @@ def ngram_set_part(wl, attt, torch, reps):
             "set_bytes_per_episode": nbytes, "capacity": capacity}
 
 
+def repetition_part(wl, attt, torch, reps):
+    """The paper's sequence-level baseline (Eq. 6-7, tau = 0.5), outside the timed step: rho, nu
+    and the skip decision of every episode's update against each previous update of its history
+    (token ids as word ids). Times are the kernels' own (launch events), queued behind a GPU
+    spin; bytes are the words read once."""
+    from gpu_util import dev_i32
+    cfg, tok = wl.cfg, wl.tokens()
+    texts = []
+    for e in range(cfg.episodes):
+        h = tok["history"][e]
+        texts += [h[i * cfg.prior_len:(i + 1) * cfg.prior_len] for i in range(cfg.prior_updates)]
+        texts.append(tok["updates"][e])
+    toff = np.zeros(len(texts) + 1, np.int64)
+    toff[1:] = np.cumsum([len(t) for t in texts])
+    etx = np.arange(cfg.episodes + 1, dtype=np.int64) * (cfg.prior_updates + 1)
+    words = dev_i32(np.concatenate(texts))
+    toff_d = torch.from_numpy(toff).cuda()
+    ws = torch.empty(attt.repetition_workspace_size(toff, etx), dtype=torch.uint8, device="cuda")
+    attt.update_repetition(words, toff, etx, text_offsets_dev=toff_d, workspace=ws)
+    torch.cuda.synchronize()
+    attt.timing_enable(True)
+    attt.timing_reset()
+    gpu_hold(torch, reps)
+    for _ in range(reps):
+        rho, nu, skip, best, _ = attt.update_repetition(words, toff, etx, text_offsets_dev=toff_d, workspace=ws)
+    torch.cuda.synchronize()
+    c_ms, c_n = attt.timing_read("rep_count")
+    r_ms, r_n = attt.timing_read("rep_reduce")
+    attt.timing_enable(False)
+    ms = c_ms / max(1, reps) + r_ms / max(1, reps)
+    nbytes = 4.0 * float(toff[-1])
+    return {"ms": ms, "count_ms": c_ms / max(1, reps), "reduce_ms": r_ms / max(1, reps),
+            "texts": len(texts), "words": int(toff[-1]), "algorithmic_gbs": nbytes / (ms * 1e-3) / 1e9,
+            "frac_of_hbm_peak": nbytes / (ms * 1e-3) / PEAK_HBM,
+            "skipped_updates": int(skip.sum().item()), "mean_rho": float(rho.mean().item())}
+
+
 def gpu_hold(torch, calls):
     """Keep the GPU busy (torch.cuda._sleep, ~1 ms per 2e6 cycles) while `calls` small calls are
     queued behind it, so the launch events around each kernel measure the kernel and not the
@@ -399,6 +436,7 @@ def main():
         ns = ngram_set_part(wl, attt, torch, max(args.steps, 10))
         ns["streaming_ngram_pass_ms"] = ng_ms
         parts["ngram_set_per_update"] = ns
+    parts["repetition_filter"] = repetition_part(wl, attt, torch, 10)
     out = {
         "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,

@@ -111,6 +111,45 @@ attt_status attt_ngram_weights_noalloc(const int32_t* history, const int64_t* hi
                                        uint32_t* exposure, float* weights, void* stream);
 
 /* --------------------------------------------------------------------------------------
+ * Update-text repetition and the sequence-level filter (Sec. 3.2, Eq. 6-7; tau of Appendix C):
+ *     rho(x_k) = max over x' in H_k of J(W(x_k), W(x')),   J(A, B) = |A & B| / |A | B|,
+ *     nu(x_k) = 1 - rho(x_k),   skip the update when nu < tau   (tau = 0.5 in the paper)
+ * W(x) is the set of whitespace-separated words of an update text. Texts arrive as word ids, one
+ * int32 per word, equal words equal ids (splitting and mapping strings is the caller's work).
+ * Episodes are independent; the texts of episode e are texts episode_texts[e] ..
+ * episode_texts[e+1] - 1 in order, the last of them the candidate x_k and the others H_k. An
+ * episode with one text has rho = 0. J of two empty word sets is 0. Counts are exact integers;
+ * rho is the float64 nearest to the largest |A & B| / |A | B|, nu = RN(1 - rho) in float64,
+ * skip = (nu < tau) in float64, so every output is bit-reproducible.
+ *
+ * words             device int32 [text_offsets[T]]: the word ids of all texts back to back;
+ *                   ids in [0, 2^31) (a negative id is outside the contract: the counts of its
+ *                   text are then not meaningful, nothing is read or written out of bounds)
+ * text_offsets      host int64 [T+1], T = episode_texts[E]: text t is words[text_offsets[t] ..
+ *                   text_offsets[t+1]); text_offsets[0] = 0, non-decreasing; a text may be empty
+ * text_offsets_dev  the same T+1 values in device memory (the kernels read text ranges there)
+ * episode_texts     host int64 [E+1], episode_texts[0] = 0, at least one text per episode
+ * tau               the skip threshold, finite
+ * rho, nu           device double [E];  skip  device int32 [E] (1 = skip the update)
+ * best              device int32 [E]: index within the episode's texts of the first previous
+ *                   text that attains rho, -1 for an episode with one text
+ * pair_counts       device int32 [P][2] or NULL: (|A & B|, |A | B|) of every previous text
+ *                   against its episode's candidate, episodes and texts in order;
+ *                   P = sum over episodes of (texts - 1)
+ * workspace         device, >= attt_repetition_workspace_size bytes, 256-byte aligned
+ * Errors (before any HIP call): ATTT_EINVAL for bad offsets, null pointers, a non-finite tau or
+ * E < 1; ATTT_EUNSUPPORTED for more than 2^31 - 1 words, more than 2^26 pairs x partitions, or a
+ * text of more than 2^20 words. Should an LDS word set ever fill (not possible for hashes of
+ * distinct ids spread as planned), that episode's rho and nu are NaN, skip 0 and best -1. */
+attt_status attt_repetition_workspace_size(const int64_t* text_offsets, const int64_t* episode_texts,
+                                           int32_t num_episodes, size_t* bytes);
+attt_status attt_update_repetition(const int32_t* words, const int64_t* text_offsets,
+                                   const int64_t* text_offsets_dev, const int64_t* episode_texts,
+                                   int32_t num_episodes, double tau, double* rho, double* nu,
+                                   int32_t* skip, int32_t* best, int32_t* pair_counts,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* --------------------------------------------------------------------------------------
  * Persistent n-gram sets: the history update of Algorithm 1 (H^tok_{k+1} = H^tok_k followed by
  * x_k) kept as device-resident n-gram counts, so that the weights of the next update (Eq. 8-9)
  * cost O(|x_k|) lookups instead of a pass over the whole history.

@@ -12,6 +12,7 @@ import os
 import numpy as np
 
 __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_weights_noalloc", "ngram_workspace_size",
+           "update_repetition", "repetition_workspace_size",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
            "weighted_ce_fwd_bwd", "ce_workspace_size", "ce_head_t_size", "ce_head_transpose", "lora_grad", "lora_workspace_size", "lora_sgd_step",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
@@ -71,6 +72,10 @@ def load():
     L.attt_ngram_workspace_size.argtypes = [p64, p64, i32, i32, psz]
     L.attt_ngram_weights.restype = i32
     L.attt_ngram_weights.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp, sz, vp]
+    L.attt_repetition_workspace_size.restype = i32
+    L.attt_repetition_workspace_size.argtypes = [p64, p64, i32, psz]
+    L.attt_update_repetition.restype = i32
+    L.attt_update_repetition.argtypes = [vp, p64, vp, p64, i32, ctypes.c_double, vp, vp, vp, vp, vp, vp, sz, vp]
     L.attt_ngram_weights_noalloc.restype = i32
     L.attt_ngram_weights_noalloc.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp]
     vpp = ctypes.POINTER(ctypes.c_void_p)
@@ -197,6 +202,50 @@ def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.
     _check(L.attt_ngram_weights(_dptr(history), hp, _dptr(tokens), tp, E, n, float(w_min), _dptr(f),
                                 _dptr(w), _dptr(ws), ws.numel(), _stream_ptr()))
     return f, w
+
+
+def repetition_workspace_size(text_offsets, episode_texts):
+    L = load()
+    to, tp = _offsets(text_offsets)
+    eo, ep = _offsets(episode_texts)
+    need = ctypes.c_size_t()
+    _check(L.attt_repetition_workspace_size(tp, ep, len(eo) - 1, ctypes.byref(need)))
+    return need.value
+
+
+def update_repetition(words, text_offsets, episode_texts, tau=0.5, text_offsets_dev=None, want_pairs=False,
+                      workspace=None):
+    """Update-text repetition rho, novelty nu and the skip decision per episode (Eq. 6-7).
+
+    words: device int32 word ids of all texts back to back; text_offsets: host int64 [T+1];
+    episode_texts: host int64 [E+1] (the last text of each episode is the candidate).
+    text_offsets_dev: the same offsets already on the device (copied here when not given).
+    Returns (rho, nu, skip, best, pairs): device tensors [E] (float64, float64, int32, int32) and
+    pairs [P, 2] int32 (|A & B|, |A | B|) when want_pairs, else None."""
+    torch = _torch()
+    L = load()
+    to, tp = _offsets(text_offsets)
+    eo, ep = _offsets(episode_texts)
+    _dev(words, "words")
+    if words.dtype != torch.int32:
+        raise TypeError("words must be int32")
+    E = len(eo) - 1
+    dev = words.device
+    if text_offsets_dev is None:
+        text_offsets_dev = torch.from_numpy(to).to(dev)
+    need = ctypes.c_size_t()
+    _check(L.attt_repetition_workspace_size(tp, ep, E, ctypes.byref(need)))
+    ws = _workspace(need.value, dev, workspace)
+    rho = torch.empty(E, dtype=torch.float64, device=dev)
+    nu = torch.empty(E, dtype=torch.float64, device=dev)
+    skip = torch.empty(E, dtype=torch.int32, device=dev)
+    best = torch.empty(E, dtype=torch.int32, device=dev)
+    P = int((eo[1:] - eo[:-1] - 1).sum()) if E > 0 else 0
+    pairs = torch.empty((max(P, 1), 2), dtype=torch.int32, device=dev) if want_pairs else None
+    _check(L.attt_update_repetition(_dptr(words), tp, _dptr(text_offsets_dev), ep, E, float(tau), _dptr(rho),
+                                    _dptr(nu), _dptr(skip), _dptr(best), _dptr(pairs), _dptr(ws), ws.numel(),
+                                    _stream_ptr()))
+    return rho, nu, skip, best, (pairs[:P] if want_pairs else None)
 
 
 def ngram_weights_noalloc(history, history_offsets, tokens, token_offsets, n=3, w_min=0.05,

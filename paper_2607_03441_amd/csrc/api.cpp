@@ -50,7 +50,7 @@ namespace attt {
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ngram_table", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard", "lora_u_du", "lora_dadb",
-    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd"};
+    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd", "rep_count", "rep_reduce"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -370,6 +370,101 @@ attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t*
   return ATTT_OK;
 }
 }  // namespace
+
+// ------------------------------------------------------------------------------------------
+// Update-text repetition (Eq. 6-7)
+// ------------------------------------------------------------------------------------------
+namespace {
+constexpr int64_t kRepMaxTextWords = (int64_t)1 << 20;
+constexpr int64_t kRepMaxRecords = (int64_t)1 << 26;
+
+struct RepPlan {
+  std::vector<RepEp> eps;  // wg_begin relative to the episode's launch batch is set at launch
+  int64_t records = 0, pairs = 0;
+  size_t total = 0;
+};
+
+attt_status rep_plan(const int64_t* toff, const int64_t* etx, int32_t E, RepPlan& P) {
+  if (E < 1) return fail(ATTT_EINVAL, "repetition: num_episodes must be >= 1 (got %d)", E);
+  if (!toff || !etx) return fail(ATTT_EINVAL, "repetition: offsets pointer is null");
+  if (etx[0] != 0) return fail(ATTT_EINVAL, "repetition: episode_texts[0] must be 0");
+  for (int32_t e = 0; e < E; ++e)
+    if (etx[e + 1] <= etx[e]) return fail(ATTT_EINVAL, "repetition: episode %d has no text", e);
+  const int64_t T = etx[E];
+  if (T > INT32_MAX) return fail(ATTT_EUNSUPPORTED, "repetition: %lld texts (limit 2^31 - 1)", (long long)T);
+  if (toff[0] != 0) return fail(ATTT_EINVAL, "repetition: text_offsets[0] must be 0");
+  for (int64_t t = 0; t < T; ++t) {
+    if (toff[t + 1] < toff[t]) return fail(ATTT_EINVAL, "repetition: text_offsets decrease at text %lld", (long long)t);
+    if (toff[t + 1] - toff[t] > kRepMaxTextWords)
+      return fail(ATTT_EUNSUPPORTED, "repetition: text %lld holds %lld words (limit 2^20)", (long long)t,
+                  (long long)(toff[t + 1] - toff[t]));
+  }
+  if (toff[T] > INT32_MAX) return fail(ATTT_EUNSUPPORTED, "repetition: %lld words (limit 2^31 - 1)", (long long)toff[T]);
+  for (int32_t e = 0; e < E; ++e) {
+    RepEp ep{};
+    ep.text0 = etx[e];
+    ep.ntexts = (int32_t)(etx[e + 1] - etx[e]);
+    ep.ep = e;
+    const int64_t cand = etx[e + 1] - 1;
+    int64_t longest = toff[cand + 1] - toff[cand];
+    for (int64_t t = etx[e]; t < cand; ++t) longest = std::max(longest, toff[t + 1] - toff[t]);
+    // a partition sees about kRepPartWords words of each text: its LDS sets stay below 1/4 full
+    ep.parts = (int32_t)std::max<int64_t>(1, ceil_div(longest, kRepPartWords));
+    ep.wg_global = P.records;
+    ep.pair_base = P.pairs;
+    P.records += (int64_t)(ep.ntexts - 1) * ep.parts;
+    P.pairs += ep.ntexts - 1;
+    P.eps.push_back(ep);
+  }
+  if (P.records > kRepMaxRecords)
+    return fail(ATTT_EUNSUPPORTED, "repetition: %lld pairs x partitions (limit 2^26)", (long long)P.records);
+  P.total = std::max<size_t>(align256((size_t)P.records * 16), 256);
+  return ATTT_OK;
+}
+}  // namespace
+
+extern "C" attt_status attt_repetition_workspace_size(const int64_t* text_offsets, const int64_t* episode_texts,
+                                                      int32_t num_episodes, size_t* bytes) {
+  if (!bytes) return fail(ATTT_EINVAL, "repetition: bytes is null");
+  RepPlan P;
+  attt_status st = rep_plan(text_offsets, episode_texts, num_episodes, P);
+  if (st) return st;
+  *bytes = P.total;
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_update_repetition(const int32_t* words, const int64_t* text_offsets,
+                                              const int64_t* text_offsets_dev, const int64_t* episode_texts,
+                                              int32_t num_episodes, double tau, double* rho, double* nu,
+                                              int32_t* skip, int32_t* best, int32_t* pair_counts,
+                                              void* workspace, size_t workspace_bytes, void* stream) {
+  RepPlan P;
+  attt_status st = rep_plan(text_offsets, episode_texts, num_episodes, P);
+  if (st) return st;
+  if (!std::isfinite(tau)) return fail(ATTT_EINVAL, "repetition: tau must be finite");
+  if (!rho || !nu || !skip || !best) return fail(ATTT_EINVAL, "repetition: null output pointer");
+  if (!text_offsets_dev) return fail(ATTT_EINVAL, "repetition: text_offsets_dev is null");
+  if (text_offsets[episode_texts[num_episodes]] > 0 && !words) return fail(ATTT_EINVAL, "repetition: words is null");
+  if (workspace_bytes < P.total)
+    return fail(ATTT_ENOSPACE, "repetition: workspace %zu bytes, need %zu", workspace_bytes, P.total);
+  if (!workspace) return fail(ATTT_EINVAL, "repetition: workspace is null");
+  if (!aligned256(workspace)) return fail(ATTT_EINVAL, "repetition: workspace must be 256-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* counts = static_cast<int32_t*>(workspace);
+  for (size_t e0 = 0; e0 < P.eps.size(); e0 += kEpBatch) {
+    RepBatch b{};
+    b.count = (int32_t)std::min<size_t>(kEpBatch, P.eps.size() - e0);
+    int wgs = 0;
+    for (int i = 0; i < b.count; ++i) {
+      b.e[i] = P.eps[e0 + i];
+      b.e[i].wg_begin = wgs;
+      wgs += (b.e[i].ntexts - 1) * b.e[i].parts;
+    }
+    HIP_TRY(launch_rep_count(b, wgs, words, text_offsets_dev, counts, s), "rep_count");
+    HIP_TRY(launch_rep_reduce(b, counts, tau, rho, nu, skip, best, pair_counts, s), "rep_reduce");
+  }
+  return ATTT_OK;
+}
 
 // ------------------------------------------------------------------------------------------
 // Persistent n-gram sets

@@ -29,6 +29,8 @@ enum KernelId {
   K_NGRAM_SET_WEIGHT,
   K_LORA_SGD,
   K_CE_FUSED,
+  K_REP_COUNT,
+  K_REP_REDUCE,
   K_NUM_KERNELS
 };
 
@@ -113,6 +115,28 @@ hipError_t launch_ngram_count(const NgramPartBatch& b, int total_blocks, int max
 hipError_t launch_ngram_weight(const NgramEpBatch& b, int total_blocks, int n, float w_min,
                                const uint16_t* partial, const uint16_t* canon, uint32_t* exposure,
                                float* weights, hipStream_t s);
+
+// ---- update-text repetition (Eq. 6-7) ------------------------------------------------------
+constexpr int kRepSlots = 16384;        // entries of each LDS word set of the count kernel
+constexpr int kRepPartWords = 4096;     // words per hash partition the host plans for (load <= 1/4)
+struct RepEp {
+  int64_t text0;      // first text of the episode (index into the text offsets)
+  int64_t wg_global;  // first count record of the episode ([pair][part] order, 4 ints each)
+  int64_t pair_base;  // first pair of the episode in pair_counts
+  int32_t ntexts;     // texts of the episode, >= 1; the last is the candidate
+  int32_t parts;      // hash partitions per pair
+  int32_t wg_begin;   // first count-kernel workgroup of the episode within the launch
+  int32_t ep;         // episode index (outputs)
+};
+struct RepBatch {
+  int32_t count;
+  int32_t pad;
+  RepEp e[kEpBatch];
+};
+hipError_t launch_rep_count(const RepBatch& b, int total_wgs, const int32_t* words, const int64_t* toff,
+                            int32_t* counts, hipStream_t s);
+hipError_t launch_rep_reduce(const RepBatch& b, const int32_t* counts, double tau, double* rho, double* nu,
+                             int32_t* skip, int32_t* best, int32_t* pair_counts, hipStream_t s);
 
 // ---- persistent n-gram set ---------------------------------------------------------------
 struct NgramSetJob {

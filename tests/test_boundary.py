@@ -276,3 +276,39 @@ def test_ce_wait_limit_validation(L):
     assert L.attt_ce_set_wait_limit(-1, 10) == attt.EINVAL
     assert L.attt_ce_set_wait_limit(10, -1) == attt.EINVAL
     assert L.attt_ce_set_wait_limit(20000, 20000) == attt.OK
+
+
+def _rep(L, toff, etx, E=None, tau=0.5, outs=True, ws_bytes=1 << 30, words=FAKE, toff_dev=FAKE):
+    _, tp = _off(toff)
+    _, ep = _off(etx)
+    E = len(etx) - 1 if E is None else E
+    o = FAKE if outs else None
+    return L.attt_update_repetition(words, tp, toff_dev, ep, E, tau, o, o, o, o, None, FAKE_WS, ws_bytes, None)
+
+
+def test_repetition_validation(L):
+    # two episodes: texts 0-1 and 2; words 0..9
+    toff, etx = [0, 4, 7, 10], [0, 2, 3]
+    need = attt.repetition_workspace_size(toff, etx)
+    assert need >= 256 and need % 256 == 0
+    assert _rep(L, toff, etx, E=0) == attt.EINVAL
+    assert _rep(L, toff, [0, 0, 3]) == attt.EINVAL            # an episode without text
+    assert _rep(L, toff, [1, 2, 3]) == attt.EINVAL            # episode_texts[0] != 0
+    assert _rep(L, [0, 4, 3, 10], etx) == attt.EINVAL         # text offsets decrease
+    assert _rep(L, [1, 4, 7, 10], etx) == attt.EINVAL         # text_offsets[0] != 0
+    assert _rep(L, toff, etx, tau=float("nan")) == attt.EINVAL
+    assert _rep(L, toff, etx, tau=float("inf")) == attt.EINVAL
+    assert _rep(L, toff, etx, outs=False) == attt.EINVAL
+    assert _rep(L, toff, etx, toff_dev=None) == attt.EINVAL
+    assert _rep(L, toff, etx, words=None) == attt.EINVAL
+    assert _rep(L, toff, etx, ws_bytes=need - 1) == attt.ENOSPACE
+    # a text longer than 2^20 words is refused from the offsets alone
+    assert _rep(L, [0, (1 << 20) + 1], [0, 1]) == attt.EUNSUPPORTED
+    assert b"2^20" in L.attt_last_error()
+    # one record per (pair, partition): 2^26 of them at most. A 2^20-word candidate takes 256
+    # partitions, so 2^18 + 1 (empty) previous texts exceed it.
+    T = (1 << 18) + 2
+    toff2 = np.zeros(T + 1, dtype=np.int64)
+    toff2[-1] = 1 << 20
+    assert _rep(L, toff2, [0, T]) == attt.EUNSUPPORTED
+    assert b"2^26" in L.attt_last_error()
