@@ -111,6 +111,35 @@ attt_status attt_ngram_weights_noalloc(const int32_t* history, const int64_t* hi
                                        uint32_t* exposure, float* weights, void* stream);
 
 /* --------------------------------------------------------------------------------------
+ * Backward of one adapted attention block: the gradients dY_q, dY_k, dY_v of the q, k and v
+ * projection outputs, which are the upstream gradients of the LoRA gradient below (the
+ * episode adapter on q/k/v/o of Sec. 3.1; rank and alpha in Appendix C). Causal attention with
+ * grouped key/value heads, each episode an independent sequence:
+ *     S = scale Q K^T (query t sees keys s <= t of its episode), P = softmax(S), O = P V,
+ *     D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
+ *     dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO
+ * with query head h reading key/value head h / (heads / kv_heads); dK and dV of a key/value
+ * head are summed over its query heads. Q and K are the attention's inputs (after any position
+ * encoding); dO is the gradient of the attention output (the o projection's input).
+ * bf16 in and out, float32 accumulation; between the two products of each step P and dS are
+ * carried as bf16 pairs hi + lo. Deterministic (fixed accumulation orders, no atomics).
+ *
+ * q, dout         device bf16 [N][heads][128] (token-major: row t is [heads x 128])
+ * k, v            device bf16 [N][kv_heads][128]
+ * row_offsets     host int64 [E+1] (episodes of rows; NULL: one episode of N rows)
+ * heads, kv_heads kv_heads >= 1 divides heads; head_dim must be 128
+ * scale           finite, > 0 (1/sqrt(128) for the standard block)
+ * dq / dk, dv     device bf16, the layouts of q / k, v (written in full)
+ * lse, dsum       device float32 [heads][N]: the forward's log-sum-exp and D (written)
+ * All device pointers 16-byte aligned. Errors (before any HIP call): ATTT_EINVAL for bad
+ * offsets, null or misaligned pointers, heads not a multiple of kv_heads, a bad scale;
+ * ATTT_EUNSUPPORTED for head_dim != 128 or N >= 2^31 / heads. */
+attt_status attt_attention_bwd(const void* q, const void* k, const void* v, const void* dout,
+                               const int64_t* row_offsets, int32_t num_episodes, int64_t N,
+                               int32_t heads, int32_t kv_heads, int32_t head_dim, float scale,
+                               void* dq, void* dk, void* dv, float* lse, float* dsum, void* stream);
+
+/* --------------------------------------------------------------------------------------
  * Update-text repetition and the sequence-level filter (Sec. 3.2, Eq. 6-7; tau of Appendix C):
  *     rho(x_k) = max over x' in H_k of J(W(x_k), W(x')),   J(A, B) = |A & B| / |A | B|,
  *     nu(x_k) = 1 - rho(x_k),   skip the update when nu < tau   (tau = 0.5 in the paper)

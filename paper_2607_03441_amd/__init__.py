@@ -12,7 +12,7 @@ import os
 import numpy as np
 
 __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_weights_noalloc", "ngram_workspace_size",
-           "update_repetition", "repetition_workspace_size",
+           "update_repetition", "repetition_workspace_size", "attention_bwd",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
            "weighted_ce_fwd_bwd", "ce_workspace_size", "ce_head_t_size", "ce_head_transpose", "lora_grad", "lora_workspace_size", "lora_sgd_step",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
@@ -72,6 +72,8 @@ def load():
     L.attt_ngram_workspace_size.argtypes = [p64, p64, i32, i32, psz]
     L.attt_ngram_weights.restype = i32
     L.attt_ngram_weights.argtypes = [vp, p64, vp, p64, i32, i32, f32, vp, vp, vp, sz, vp]
+    L.attt_attention_bwd.restype = i32
+    L.attt_attention_bwd.argtypes = [vp, vp, vp, vp, p64, i32, i64, i32, i32, i32, f32, vp, vp, vp, vp, vp, vp]
     L.attt_repetition_workspace_size.restype = i32
     L.attt_repetition_workspace_size.argtypes = [p64, p64, i32, psz]
     L.attt_update_repetition.restype = i32
@@ -202,6 +204,35 @@ def ngram_weights(history, history_offsets, tokens, token_offsets, n=3, w_min=0.
     _check(L.attt_ngram_weights(_dptr(history), hp, _dptr(tokens), tp, E, n, float(w_min), _dptr(f),
                                 _dptr(w), _dptr(ws), ws.numel(), _stream_ptr()))
     return f, w
+
+
+def attention_bwd(q, k, v, dout, row_offsets=None, scale=None, out=None):
+    """Backward of one causal grouped-head attention block: (dq, dk, dv, lse, dsum).
+
+    q, dout: device bf16 [N, heads, 128]; k, v: [N, kv_heads, 128]; row_offsets: host int64
+    episode offsets or None; scale defaults to 1/sqrt(128). lse, dsum: float32 [heads, N]."""
+    torch = _torch()
+    L = load()
+    for t, name in ((q, "q"), (k, "k"), (v, "v"), (dout, "dout")):
+        _dev(t, name)
+        if t.dtype != torch.bfloat16 or t.dim() != 3:
+            raise TypeError(f"{name} must be bfloat16 [N, heads, head_dim]")
+    N, H, dh = q.shape
+    Hkv = k.shape[1]
+    scale = (1.0 / dh ** 0.5) if scale is None else float(scale)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+               torch.empty(H, N, dtype=torch.float32, device=q.device),
+               torch.empty(H, N, dtype=torch.float32, device=q.device))
+    dq, dk, dv, lse, dsum = out
+    if row_offsets is None:
+        E, op = 1, None
+    else:
+        oo, op = _offsets(row_offsets)
+        E = len(oo) - 1
+    _check(L.attt_attention_bwd(_dptr(q), _dptr(k), _dptr(v), _dptr(dout), op, E, N, H, Hkv, dh, scale,
+                                _dptr(dq), _dptr(dk), _dptr(dv), _dptr(lse), _dptr(dsum), _stream_ptr()))
+    return dq, dk, dv, lse, dsum
 
 
 def repetition_workspace_size(text_offsets, episode_texts):

@@ -50,7 +50,8 @@ namespace attt {
 static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ngram_table", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard", "lora_u_du", "lora_dadb",
-    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd", "rep_count", "rep_reduce"};
+    "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd", "rep_count", "rep_reduce", "attn_fwd_stats",
+    "attn_dkdv", "attn_dq"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -370,6 +371,73 @@ attt_status ngram_run(const NgramPlan& P, const int32_t* history, const int32_t*
   return ATTT_OK;
 }
 }  // namespace
+
+// ------------------------------------------------------------------------------------------
+// Attention-block backward
+// ------------------------------------------------------------------------------------------
+extern "C" attt_status attt_attention_bwd(const void* q, const void* k, const void* v, const void* dout,
+                                          const int64_t* row_offsets, int32_t num_episodes, int64_t N,
+                                          int32_t heads, int32_t kv_heads, int32_t head_dim, float scale,
+                                          void* dq, void* dk, void* dv, float* lse, float* dsum, void* stream) {
+  if (head_dim != 128) return fail(ATTT_EUNSUPPORTED, "attention: head_dim must be 128 (got %d)", head_dim);
+  if (heads < 1 || kv_heads < 1 || heads % kv_heads != 0)
+    return fail(ATTT_EINVAL, "attention: heads (%d) must be a positive multiple of kv_heads (%d)", heads, kv_heads);
+  if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(ATTT_EINVAL, "attention: scale must be finite and > 0");
+  if (N < 0) return fail(ATTT_EINVAL, "attention: N must be >= 0");
+  if (N * heads >= INT32_MAX) return fail(ATTT_EUNSUPPORTED, "attention: N x heads must be < 2^31");
+  if (num_episodes < 1) return fail(ATTT_EINVAL, "attention: num_episodes must be >= 1 (got %d)", num_episodes);
+  int64_t single[2] = {0, N};
+  const int64_t* off = row_offsets;
+  if (!off) {
+    if (num_episodes != 1) return fail(ATTT_EINVAL, "attention: row_offsets may be NULL only for one episode");
+    off = single;
+  }
+  attt_status st = check_offsets("attention rows", off, num_episodes, INT32_MAX);
+  if (st) return st;
+  if (off[num_episodes] != N)
+    return fail(ATTT_EINVAL, "attention: row_offsets[E] (%lld) != N (%lld)", (long long)off[num_episodes], (long long)N);
+  if (N == 0) return ATTT_OK;
+  const void* ptrs[] = {q, k, v, dout, dq, dk, dv, lse, dsum};
+  for (const void* ptr : ptrs) {
+    if (!ptr) return fail(ATTT_EINVAL, "attention: null pointer");
+    if (!aligned16(ptr)) return fail(ATTT_EINVAL, "attention: device pointers must be 16-byte aligned");
+  }
+  AttnArgs a{};
+  a.q = static_cast<const bf16_t*>(q);
+  a.k = static_cast<const bf16_t*>(k);
+  a.v = static_cast<const bf16_t*>(v);
+  a.dout = static_cast<const bf16_t*>(dout);
+  a.dq = static_cast<bf16_t*>(dq);
+  a.dk = static_cast<bf16_t*>(dk);
+  a.dv = static_cast<bf16_t*>(dv);
+  a.lse = lse;
+  a.dsum = dsum;
+  a.N = (int32_t)N;
+  a.heads = heads;
+  a.kv_heads = kv_heads;
+  a.scale = scale;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int32_t e0 = 0; e0 < num_episodes; e0 += kEpBatch) {
+    AttnBatch b{};
+    b.count = std::min<int32_t>(kEpBatch, num_episodes - e0);
+    for (int i = 0; i < b.count; ++i) {
+      b.e[i].row0 = off[e0 + i];
+      b.e[i].L = (int32_t)(off[e0 + i + 1] - off[e0 + i]);
+      b.e[i].blocks = (int32_t)ceil_div(b.e[i].L, 64);
+    }
+    // workgroups per episode: blocks x heads (forward statistics, dQ) or x kv_heads (dK, dV)
+    for (int kernel = 0; kernel < 3; ++kernel) {
+      const int per = kernel == 1 ? kv_heads : heads;
+      int wgs = 0;
+      for (int i = 0; i < b.count; ++i) {
+        b.e[i].wg_begin = wgs;
+        wgs += b.e[i].blocks * per;
+      }
+      HIP_TRY(launch_attn(kernel, a, b, wgs, s), kernel == 0 ? "attn_fwd_stats" : kernel == 1 ? "attn_dkdv" : "attn_dq");
+    }
+  }
+  return ATTT_OK;
+}
 
 // ------------------------------------------------------------------------------------------
 // Update-text repetition (Eq. 6-7)

@@ -31,6 +31,9 @@ enum KernelId {
   K_CE_FUSED,
   K_REP_COUNT,
   K_REP_REDUCE,
+  K_ATTN_FWD,
+  K_ATTN_DKDV,
+  K_ATTN_DQ,
   K_NUM_KERNELS
 };
 
@@ -137,6 +140,35 @@ hipError_t launch_rep_count(const RepBatch& b, int total_wgs, const int32_t* wor
                             int32_t* counts, hipStream_t s);
 hipError_t launch_rep_reduce(const RepBatch& b, const int32_t* counts, double tau, double* rho, double* nu,
                              int32_t* skip, int32_t* best, int32_t* pair_counts, hipStream_t s);
+
+// ---- attention-block backward -----------------------------------------------------------------
+struct AttnArgs {
+  const bf16_t* q;     // [N][heads][128]
+  const bf16_t* k;     // [N][kv_heads][128]
+  const bf16_t* v;
+  const bf16_t* dout;  // [N][heads][128]
+  bf16_t* dq;
+  bf16_t* dk;
+  bf16_t* dv;
+  float* lse;          // [heads][N]
+  float* dsum;         // [heads][N]
+  int32_t N, heads, kv_heads;
+  float scale;
+};
+struct AttnEp {
+  int64_t row0;     // first row of the episode
+  int32_t L;        // rows
+  int32_t blocks;   // 64-row blocks
+  int32_t wg_begin; // first workgroup of the episode within the launch
+  int32_t pad;
+};
+struct AttnBatch {
+  int32_t count;
+  int32_t pad;
+  AttnEp e[kEpBatch];
+};
+// kernel 0: forward statistics, 1: dK and dV, 2: dQ
+hipError_t launch_attn(int kernel, const AttnArgs& a, const AttnBatch& b, int wgs, hipStream_t s);
 
 // ---- persistent n-gram set ---------------------------------------------------------------
 struct NgramSetJob {

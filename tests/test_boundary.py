@@ -312,3 +312,28 @@ def test_repetition_validation(L):
     toff2[-1] = 1 << 20
     assert _rep(L, toff2, [0, T]) == attt.EUNSUPPORTED
     assert b"2^26" in L.attt_last_error()
+
+
+def _attn(L, N=64, H=4, Hkv=2, dh=128, scale=0.088, off=None, E=1, ptr=FAKE):
+    op = None
+    if off is not None:
+        _, op = _off(off)
+        E = len(off) - 1
+    p = ptr
+    return L.attt_attention_bwd(p, p, p, p, op, E, N, H, Hkv, dh, scale, p, p, p, p, p, None)
+
+
+def test_attention_validation(L):
+    assert _attn(L, dh=64) == attt.EUNSUPPORTED
+    assert _attn(L, H=6, Hkv=4) == attt.EINVAL
+    assert _attn(L, Hkv=0) == attt.EINVAL
+    assert _attn(L, scale=0.0) == attt.EINVAL
+    assert _attn(L, scale=float("nan")) == attt.EINVAL
+    assert _attn(L, N=-1) == attt.EINVAL
+    assert _attn(L, E=2) == attt.EINVAL                       # NULL offsets need one episode
+    assert _attn(L, off=[0, 10, 60]) == attt.EINVAL           # offsets end != N
+    assert _attn(L, off=[0, 40, 30, 64]) == attt.EINVAL       # decreasing
+    assert _attn(L, ptr=None) == attt.EINVAL
+    assert _attn(L, ptr=ctypes.c_void_p(0x7F0000000008)) == attt.EINVAL  # misaligned
+    assert _attn(L, N=1 << 29, H=8, Hkv=8) == attt.EUNSUPPORTED
+    assert _attn(L, N=0, off=[0, 0]) == attt.OK               # nothing to do, nothing touched
