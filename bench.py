@@ -301,6 +301,43 @@ def repetition_part(wl, attt, torch, reps):
             "skipped_updates": int(skip.sum().item()), "mean_rho": float(rho.mean().item())}
 
 
+def attention_part(wl, attt, torch, reps):
+    """The adapted attention block's backward at the workload's shape (dY_q, dY_k, dY_v: the
+    LoRA gradient's upstream gradients), outside the timed step: one call per episode batch
+    of the update rows, heads = d / 128, key/value heads from the k projection. Synthetic bf16
+    inputs. Algorithmic flops: the causal forward (QK^T and PV) plus the backward at 2.5x the
+    forward, 7 N^2/2-sized products of 2 dh flops per (query, key, head)."""
+    from workloads.gen import random_dense
+    from gpu_util import dev_dense
+    cfg = wl.cfg
+    kproj = [p for p in cfg.projections if p.name == "k"]
+    if not kproj or cfg.d % 128 or cfg.dtype != "bf16":
+        return None
+    H, Hkv = cfg.d // 128, kproj[0].d_out // 128
+    N = cfg.rows
+    off = np.arange(cfg.episodes + 1, dtype=np.int64) * cfg.update_len
+    q = dev_dense(random_dense((N, H, 128), 1.0, True, 901))
+    k = dev_dense(random_dense((N, Hkv, 128), 1.0, True, 902))
+    v = dev_dense(random_dense((N, Hkv, 128), 1.0, True, 903))
+    do = dev_dense(random_dense((N, H, 128), 0.05, True, 904))
+    out = attt.attention_bwd(q, k, v, do, row_offsets=off)
+    torch.cuda.synchronize()
+    attt.timing_enable(True)
+    attt.timing_reset()
+    gpu_hold(torch, reps)
+    for _ in range(reps):
+        attt.attention_bwd(q, k, v, do, row_offsets=off, out=out)
+    torch.cuda.synchronize()
+    times = {n: attt.timing_read(n)[0] / reps for n in ("attn_fwd_stats", "attn_dkdv", "attn_dq")}
+    attt.timing_enable(False)
+    ms = sum(times.values())
+    L = cfg.update_len
+    pairs = cfg.episodes * L * (L + 1) / 2.0  # causal (query, key) pairs per head
+    flops = 7.0 * 2.0 * 128 * pairs * H
+    return {"ms": ms, **{k + "_ms": t for k, t in times.items()}, "heads": H, "kv_heads": Hkv,
+            "algorithmic_tflops": flops / (ms * 1e-3) / 1e12, "frac_of_mfma_peak": flops / (ms * 1e-3) / PEAK_BF16}
+
+
 def gpu_hold(torch, calls):
     """Keep the GPU busy (torch.cuda._sleep, ~1 ms per 2e6 cycles) while `calls` small calls are
     queued behind it, so the launch events around each kernel measure the kernel and not the
@@ -437,6 +474,9 @@ def main():
         ns["streaming_ngram_pass_ms"] = ng_ms
         parts["ngram_set_per_update"] = ns
     parts["repetition_filter"] = repetition_part(wl, attt, torch, 10)
+    ap = attention_part(wl, attt, torch, 5)
+    if ap is not None:
+        parts["attention_bwd"] = ap
     out = {
         "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
