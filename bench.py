@@ -157,7 +157,7 @@ def algorithmic(cfg, tok, probs):
 
 
 KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_",
-                 "ce_fused_bwd": "void attt::ce_fused_bwd_kernel<true>"}
+                 "ce_fused_bwd": "attt::ce_fused_bwd_kernel<true>"}
 
 
 def counter_traffic(workload, kernel):
@@ -179,7 +179,7 @@ def counter_traffic(workload, kernel):
                 return None
     prefix = KERNEL_SYMBOL.get(kernel)
     for name, b in rec["bytes_per_dispatch"].items():
-        if prefix and name.startswith(prefix):
+        if prefix and name.removeprefix("void ").startswith(prefix):
             return b
     return None
 
