@@ -12,9 +12,10 @@ Modules:
   step   -- the three chained, as one update step
   repetition -- update-text repetition rho, novelty nu and the skip filter (Eq. 6-7)
   attention  -- backward of one adapted attention block: dY_q, dY_k, dY_v (the LoRA's dy)
+  serve      -- grouped multi-adapter forward y += s (x A^T) B^T per episode, and the adapter swap
 
 Every function is pinned by tests under tests/test_oracle_*.py against brute force,
 closed forms, library routines (torch CPU cross-entropy and autograd) and finite
 differences; none is "parity unpinned".
 """
-from . import attention, ce, lora, ngram, repetition, step  # noqa: F401
+from . import attention, ce, lora, ngram, repetition, serve, step  # noqa: F401
