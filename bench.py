@@ -338,6 +338,91 @@ def attention_part(wl, attt, torch, reps):
             "algorithmic_tflops": flops / (ms * 1e-3) / 1e12, "frac_of_mfma_peak": flops / (ms * 1e-3) / PEAK_BF16}
 
 
+def serve_part(wl, attt, torch, reps):
+    """The serving side, outside the timed step, at the workload's projection shapes with 16
+    concurrent episode adapters (the paper's concurrency): a decoding step (one token per
+    episode through q, k, v, o), a prefill of the workload's update rows through the same
+    adapters, and the hot swap of one whole adapter of a 32-layer model (float32 masters to
+    bf16). Bytes: every input once and y read and written; for the swap 4 + 2 bytes per
+    parameter."""
+    cfg = wl.cfg
+    if cfg.dtype != "bf16":
+        return None
+    E, r, s = 16, cfg.rank, cfg.scale
+    projs = cfg.projections
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1100)
+
+    def randn(shape, std):
+        return (torch.randn(shape, generator=gen, device="cuda") * std).to(torch.bfloat16)
+    adapters = [[(randn((r, p.d_in), 0.02), randn((p.d_out, r), 0.02)) for p in projs] for _ in range(E)]
+    ad_bytes = sum(2.0 * (A.numel() + B.numel()) for ad in adapters for A, B in ad)
+
+    def problems(rows_of):
+        out, nbytes = [], ad_bytes
+        for e in range(E):
+            L = rows_of(e)
+            xs = {}
+            for i, p in enumerate(projs):
+                if p.x_group not in xs:
+                    xs[p.x_group] = randn((L, p.d_in), 1.0)
+                    nbytes += 2.0 * L * p.d_in
+                y = randn((L, p.d_out), 1.0)
+                nbytes += 4.0 * L * p.d_out
+                A, B = adapters[e][i]
+                out.append(dict(x=xs[p.x_group], y=y, A=A, B=B, scale=s))
+        return out, nbytes
+
+    def timed(probs):
+        attt.lora_forward(probs)
+        torch.cuda.synchronize()
+        attt.timing_enable(True)
+        attt.timing_reset()
+        gpu_hold(torch, reps)
+        for _ in range(reps):
+            attt.lora_forward(probs)
+        torch.cuda.synchronize()
+        ms, n = attt.timing_read("lora_fwd")
+        attt.timing_enable(False)
+        return ms / reps, n / reps
+
+    dec, dec_bytes = problems(lambda e: 1)
+    dec_ms, dec_l = timed(dec)
+    rows_per = max(1, cfg.rows // E)
+    pre, pre_bytes = problems(lambda e: rows_per)
+    pre_ms, pre_l = timed(pre)
+    del pre
+    # hot swap: q, k, v, o adapters of 32 layers at this shape
+    layer = [(r, p.d_in) for p in projs] + [(p.d_out, r) for p in projs]
+    n_par = 32 * sum(a * b for a, b in layer)
+    masters = torch.randn(n_par, generator=gen, dtype=torch.float32, device="cuda") * 0.02
+    slot = torch.empty(n_par, dtype=torch.bfloat16, device="cuda")
+    pairs, o = [], 0
+    for _ in range(32):
+        for a, b in layer:
+            pairs.append((masters[o:o + a * b], slot[o:o + a * b]))
+            o += a * b
+    attt.lora_hot_swap(pairs)
+    torch.cuda.synchronize()
+    attt.timing_enable(True)
+    attt.timing_reset()
+    gpu_hold(torch, reps)
+    for _ in range(reps):
+        attt.lora_hot_swap(pairs)
+    torch.cuda.synchronize()
+    sw_ms, sw_n = attt.timing_read("lora_swap")
+    attt.timing_enable(False)
+    sw_ms /= reps
+    return {"adapters": E, "rank": r,
+            "decode": {"rows": E, "ms": dec_ms, "launches": dec_l, "bytes": dec_bytes,
+                       "gbs": dec_bytes / (dec_ms * 1e-3) / 1e9},
+            "prefill": {"rows": E * rows_per, "ms": pre_ms, "launches": pre_l, "bytes": pre_bytes,
+                        "gbs": pre_bytes / (pre_ms * 1e-3) / 1e9,
+                        "frac_of_hbm_peak": pre_bytes / (pre_ms * 1e-3) / PEAK_HBM},
+            "hot_swap": {"layers": 32, "tensors": len(pairs), "params": n_par, "ms": sw_ms,
+                         "launches": sw_n / reps, "gbs": 6.0 * n_par / (sw_ms * 1e-3) / 1e9}}
+
+
 def gpu_hold(torch, calls):
     """Keep the GPU busy (torch.cuda._sleep, ~1 ms per 2e6 cycles) while `calls` small calls are
     queued behind it, so the launch events around each kernel measure the kernel and not the
@@ -477,6 +562,9 @@ def main():
     ap = attention_part(wl, attt, torch, 5)
     if ap is not None:
         parts["attention_bwd"] = ap
+    sp = serve_part(wl, attt, torch, 10)
+    if sp is not None:
+        parts["lora_serve"] = sp
     out = {
         "metric": METRIC, "value": cfg.rows / (ms_step * 1e-3), "unit": "update tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,

@@ -363,6 +363,68 @@ attt_status attt_lora_sgd_step(const attt_lora_param* params, int32_t count, flo
                                void* stream);
 
 /* --------------------------------------------------------------------------------------
+ * Serving side: grouped multi-adapter forward. Concurrent episodes (16 in the paper's runs)
+ * decode through one base model, each with its own episode adapter (Appendix A; adapter of
+ * Sec. 3.1, rank and alpha in Appendix C). The adapted projection is
+ *     y = x W0^T + scale * (x A^T) B^T.
+ * The base product x W0^T is a plain GEMM the caller has already written into y; this call
+ * adds the adapter term of every (episode, projection) in one grouped launch:
+ *     y <- RN_bf16(y + scale * (x A^T) B^T)
+ * with x A^T and the sum over the rank in float32, one rounding to bf16 (nearest even) at the
+ * end. A result can differ from the correctly rounded value of the exact sum by one bf16 ulp
+ * where that sum lies within float32 error of a rounding boundary. Deterministic.
+ *
+ * problems   HOST array of `count` descriptors (typically one per episode and projection):
+ *   x      device bf16 [rows, d_in]   (the rows of one episode)
+ *   y      device bf16 [rows, d_out]  read and written in place
+ *   A      device bf16 [rank, d_in]
+ *   B      device bf16 [d_out, rank]
+ *   rows >= 0 (0: skipped), d_in and d_out positive multiples of 8, 1 <= rank <=
+ *   ATTT_LORA_MAX_RANK; rows < 2^24 and d_in, d_out < 2^20 (ATTT_EUNSUPPORTED beyond);
+ *   scale finite. x, y, A, B 16-byte aligned. The y of different problems must not overlap
+ *   each other or any input. Problems with the same x pointer, d_in and rows (q, k and v of
+ *   one layer) are computed together, x read once for up to 64 of their combined (16-padded)
+ *   ranks.
+ * Nothing is allocated and no workspace is needed (x A^T stays on chip). Asynchronous on
+ * `stream`. Errors (before any HIP call): ATTT_EINVAL, ATTT_EUNSUPPORTED; ATTT_EHIP.
+ * ------------------------------------------------------------------------------------ */
+typedef struct attt_lora_fwd_problem {
+  const void* x;
+  void* y;
+  const void* A;
+  const void* B;
+  int64_t rows;
+  int64_t d_in;
+  int64_t d_out;
+  int32_t rank;
+  float scale;
+} attt_lora_fwd_problem;
+
+attt_status attt_lora_forward(const attt_lora_fwd_problem* problems, int32_t count, void* stream);
+
+/* --------------------------------------------------------------------------------------
+ * Adapter hot swap into serving (Appendix A: the adapter trained by an update replaces the
+ * episode's serving adapter): every float32 tensor of an adapter (the masters that
+ * attt_lora_sgd_step updates) rounded to nearest even into the bf16 copy that
+ * attt_lora_forward reads, in one launch per 16 tensors. Bit-exact.
+ *
+ * items  HOST array of `count` descriptors:
+ *   src  device float [n]
+ *   dst  device bf16 [n], written
+ *   0 <= n < 2^31 (ATTT_EUNSUPPORTED beyond); n == 0 is skipped; src 4-byte and dst 2-byte
+ *   aligned (16-byte alignment of both takes the vector path); no dst may overlap any array.
+ * Ordered before later work on `stream`: a forward launched after the swap on the same stream
+ * reads the new adapter. Errors: ATTT_EINVAL, ATTT_EUNSUPPORTED, ATTT_EHIP.
+ * ------------------------------------------------------------------------------------ */
+typedef struct attt_lora_swap_item {
+  const float* src;
+  void* dst;
+  int64_t n;
+} attt_lora_swap_item;
+
+attt_status attt_lora_hot_swap(const attt_lora_swap_item* items, int32_t count, void* stream);
+
+/* --------------------------------------------------------------------------------------
  * Kernel timing (diagnostics). When enabled, every launch of a named kernel is bracketed
  * by HIP events recorded on the launch stream. attt_timing_read waits for those events and
  * returns the summed duration and launch count of one kernel since the last reset; names

@@ -15,8 +15,9 @@ __all__ = ["load", "lib_path", "AtttError", "ngram_weights", "ngram_weights_noal
            "update_repetition", "repetition_workspace_size", "attention_bwd",
            "ngram_set_size", "ngram_set_init", "ngram_set_append", "ngram_set_weights",
            "weighted_ce_fwd_bwd", "ce_workspace_size", "ce_head_t_size", "ce_head_transpose", "lora_grad", "lora_workspace_size", "lora_sgd_step",
+           "lora_forward", "lora_hot_swap",
            "timing_enable", "timing_reset", "timing_read", "kernel_names", "version",
-           "F32", "BF16", "LoraProblem", "LoraParam"]
+           "F32", "BF16", "LoraProblem", "LoraParam", "LoraFwdProblem", "LoraSwapItem"]
 
 F32 = 0
 BF16 = 1
@@ -44,6 +45,16 @@ class LoraProblem(ctypes.Structure):
 class LoraParam(ctypes.Structure):
     _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("param_bf16", ctypes.c_void_p),
                 ("n", ctypes.c_int64)]
+
+
+class LoraFwdProblem(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("y", ctypes.c_void_p), ("A", ctypes.c_void_p),
+                ("B", ctypes.c_void_p), ("rows", ctypes.c_int64), ("d_in", ctypes.c_int64),
+                ("d_out", ctypes.c_int64), ("rank", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class LoraSwapItem(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("n", ctypes.c_int64)]
 
 
 def lib_path():
@@ -109,6 +120,10 @@ def load():
     L.attt_lora_grad.argtypes = [ctypes.POINTER(LoraProblem), i32, i32, vp, sz, vp]
     L.attt_lora_sgd_step.restype = i32
     L.attt_lora_sgd_step.argtypes = [ctypes.POINTER(LoraParam), i32, f32, i32, vp]
+    L.attt_lora_forward.restype = i32
+    L.attt_lora_forward.argtypes = [ctypes.POINTER(LoraFwdProblem), i32, vp]
+    L.attt_lora_hot_swap.restype = i32
+    L.attt_lora_hot_swap.argtypes = [ctypes.POINTER(LoraSwapItem), i32, vp]
     L.attt_timing_enable.restype = i32
     L.attt_timing_enable.argtypes = [i32]
     L.attt_timing_reset.restype = i32
@@ -498,6 +513,39 @@ def lora_sgd_step(params, lr, zero_grad=False):
                 raise ValueError("param_bf16 must be a bfloat16 tensor of the param's size")
         arr[i] = LoraParam(_dptr(P), _dptr(G), _dptr(Pb), P.numel())
     _check(L.attt_lora_sgd_step(arr, len(params), float(lr), 1 if zero_grad else 0, _stream_ptr()))
+
+
+def lora_forward(problems):
+    """Grouped multi-adapter forward: for every problem, y <- RN_bf16(y + scale (x A^T) B^T) in
+    place (y already holds the base projection). Each problem: dict(x, y, A, B, scale), bf16
+    tensors x [rows, d_in], y [rows, d_out], A [r, d_in], B [d_out, r]."""
+    L = load()
+    torch = _torch()
+    arr = (LoraFwdProblem * max(len(problems), 1))()
+    for i, p in enumerate(problems):
+        x, y, A, B = p["x"], p["y"], p["A"], p["B"]
+        for k, t in (("x", x), ("y", y), ("A", A), ("B", B)):
+            _dev(t, k)
+            if t.dtype != torch.bfloat16 or t.dim() != 2:
+                raise ValueError(f"{k} must be a 2-D bfloat16 tensor")
+        arr[i] = LoraFwdProblem(_dptr(x), _dptr(y), _dptr(A), _dptr(B), x.shape[0], x.shape[1], y.shape[1],
+                                A.shape[0], float(p["scale"]))
+    _check(L.attt_lora_forward(arr, len(problems), _stream_ptr()))
+
+
+def lora_hot_swap(pairs):
+    """Adapter swap into serving: each (src, dst) pair, src a float32 tensor and dst a bfloat16
+    tensor of equal numel, gets dst = src rounded to nearest even, all in one launch."""
+    L = load()
+    torch = _torch()
+    arr = (LoraSwapItem * max(len(pairs), 1))()
+    for i, (src, dst) in enumerate(pairs):
+        _dev(src, "src")
+        _dev(dst, "dst")
+        if src.dtype != torch.float32 or dst.dtype != torch.bfloat16 or src.numel() != dst.numel():
+            raise ValueError("src must be float32 and dst bfloat16 of the same numel")
+        arr[i] = LoraSwapItem(_dptr(src), _dptr(dst), src.numel())
+    _check(L.attt_lora_hot_swap(arr, len(pairs), _stream_ptr()))
 
 
 # ------------------------------------------------------------------------------------------

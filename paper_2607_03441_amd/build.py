@@ -15,7 +15,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libattt.so")
 
-DEVICE_SOURCES = ["ngram.hip", "ngram_set.hip", "ce.hip", "ce_fused.hip", "lora.hip", "repetition.hip", "attention.hip"]
+DEVICE_SOURCES = ["ngram.hip", "ngram_set.hip", "ce.hip", "ce_fused.hip", "lora.hip", "repetition.hip", "attention.hip", "lora_serve.hip"]
 HOST_SOURCES = ["api.cpp"]
 ARCH = "gfx950"
 

@@ -51,7 +51,7 @@ static const char* kKernelNames[K_NUM_KERNELS] = {
     "ngram_count", "ngram_weight", "ngram_table", "ce_fwd_lse", "ce_label_logit", "ce_row_reduce",
     "ce_loss", "ce_head_transpose", "ce_bwd_dz", "ce_bwd_dh", "ce_overflow_guard", "lora_u_du", "lora_dadb",
     "lora_reduce", "ngram_set", "ngram_set_weight", "lora_sgd", "ce_fused_bwd", "rep_count", "rep_reduce", "attn_fwd_stats",
-    "attn_dkdv", "attn_dq"};
+    "attn_dkdv", "attn_dq", "lora_fwd", "lora_swap"};
 
 const char* kernel_name(int id) { return (id >= 0 && id < K_NUM_KERNELS) ? kKernelNames[id] : nullptr; }
 
@@ -1255,4 +1255,125 @@ extern "C" attt_status attt_lora_sgd_step(const attt_lora_param* params, int32_t
   return lora_launch_all(
       jobs, [](const LoraSgdJob& J) { return (int)ceil_div(J.n, (int64_t)kLoraSgdPerBlock); },
       [&](const LoraSgdBatch& b, int n) { return launch_lora_sgd(b, n, lr, zero_grad, s); }, "lora_sgd");
+}
+
+// ------------------------------------------------------------------------------------------
+// Serving: grouped multi-adapter forward, adapter swap
+// ------------------------------------------------------------------------------------------
+extern "C" attt_status attt_lora_forward(const attt_lora_fwd_problem* problems, int32_t count, void* stream) {
+  if (count < 0) return fail(ATTT_EINVAL, "lora_forward: count must be >= 0");
+  if (count > 0 && !problems) return fail(ATTT_EINVAL, "lora_forward: problems is null");
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_fwd_problem& q = problems[i];
+    if (q.rank < 1 || q.rank > ATTT_LORA_MAX_RANK)
+      return fail(ATTT_EINVAL, "lora_forward[%d]: rank must be in [1, %d] (got %d)", i, ATTT_LORA_MAX_RANK, q.rank);
+    if (q.rows < 0 || q.d_in < 1 || q.d_out < 1 || q.d_in % 8 || q.d_out % 8)
+      return fail(ATTT_EINVAL, "lora_forward[%d]: need rows >= 0 and d_in, d_out positive multiples of 8", i);
+    // phase 1 addresses 16 rows of x, and a unit of A, through one 32-bit buffer range
+    if (q.rows >= ((int64_t)1 << 24) || q.d_in >= ((int64_t)1 << 20) || q.d_out >= ((int64_t)1 << 20))
+      return fail(ATTT_EUNSUPPORTED, "lora_forward[%d]: dimensions beyond this build's limits (rows < 2^24, "
+                  "d_in and d_out < 2^20)", i);
+    if (!std::isfinite(q.scale)) return fail(ATTT_EINVAL, "lora_forward[%d]: scale is not finite", i);
+    if (q.rows > 0 && (!q.x || !q.y || !q.A || !q.B)) return fail(ATTT_EINVAL, "lora_forward[%d]: null array", i);
+    if (q.rows > 0 && (!aligned16(q.x) || !aligned16(q.y) || !aligned16(q.A) || !aligned16(q.B)))
+      return fail(ATTT_EINVAL, "lora_forward[%d]: x, y, A and B must be 16-byte aligned", i);
+  }
+  // jobs: problems reading the same x (pointer, d_in, rows), at most four 16-rank units each
+  std::vector<std::vector<int>> groups;
+  std::vector<int> units(count, 0);
+  for (int32_t i = 0; i < count; ++i) {
+    if (problems[i].rows == 0) continue;
+    units[i] = (int)ceil_div(problems[i].rank, 16);
+    bool placed = false;
+    for (auto& gr : groups) {
+      const attt_lora_fwd_problem& f = problems[gr[0]];
+      int used = 0;
+      for (int m : gr) used += units[m];
+      if (f.x == problems[i].x && f.d_in == problems[i].d_in && f.rows == problems[i].rows &&
+          used + units[i] <= kLoraMaxTiles) {
+        gr.push_back(i);
+        placed = true;
+        break;
+      }
+    }
+    if (!placed) groups.push_back({i});
+  }
+  std::vector<LoraFwdJob> jobs;
+  int64_t row_blocks = 0;
+  int64_t max_dout = 8;
+  for (const auto& gr : groups) {
+    const attt_lora_fwd_problem& f = problems[gr[0]];
+    LoraFwdJob J{};
+    J.x = f.x;
+    J.rows = (int32_t)f.rows;
+    J.d_in = (int32_t)f.d_in;
+    J.rb = f.rows <= 16 ? 16 : 64;
+    J.kw = f.rows <= 16 ? 4 : 1;
+    for (int i : gr) {
+      const attt_lora_fwd_problem& q = problems[i];
+      LoraFwdOut& O = J.o[J.no++];
+      O.B = q.B;
+      O.y = q.y;
+      O.d_out = (int32_t)q.d_out;
+      O.rank = q.rank;
+      O.u0 = 16 * J.nu;
+      for (int t = 0; t < units[i]; ++t) {
+        LoraFwdUnit& U = J.u[J.nu++];
+        U.A = static_cast<const uint8_t*>(q.A) + (int64_t)16 * t * q.d_in * 2;
+        U.valid = std::min(16, q.rank - 16 * t);
+        U.scale = q.scale;
+      }
+      max_dout = std::max<int64_t>(max_dout, q.d_out);
+    }
+    row_blocks += ceil_div(f.rows, J.rb);
+    jobs.push_back(J);
+  }
+  // Few row blocks (decoding): split each block's columns over several workgroups, each
+  // recomputing x A^T (x and A stay in the XCD's L2), so that the launch still fills the chip.
+  int ncs = 1;
+  if (row_blocks > 0 && row_blocks < 512)
+    ncs = (int)std::min<int64_t>({16, ceil_div(1024, row_blocks), ceil_div(max_dout, 64)});
+  ncs = std::max(ncs, 1);
+  std::stable_sort(jobs.begin(), jobs.end(), [](const LoraFwdJob& a, const LoraFwdJob& b) { return a.nu > b.nu; });
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (size_t j0 = 0; j0 < jobs.size(); j0 += kLoraFwdBatch) {
+    LoraFwdBatch b{};
+    b.count = (int32_t)std::min<size_t>(kLoraFwdBatch, jobs.size() - j0);
+    int64_t total = 0;
+    for (int i = 0; i < b.count; ++i) {
+      b.j[i] = jobs[j0 + i];
+      b.j[i].ncs = ncs;
+      b.j[i].b_begin = (int32_t)total;
+      total += ceil_div(b.j[i].rows, b.j[i].rb) * ncs;
+    }
+    if (total >= ((int64_t)1 << 31) - 8) return fail(ATTT_EUNSUPPORTED, "lora_forward: too many row blocks");
+    b.total = (int32_t)total;
+    HIP_TRY(launch_lora_fwd(b.j[0].nu, b, s), "lora_fwd");
+  }
+  return ATTT_OK;
+}
+
+extern "C" attt_status attt_lora_hot_swap(const attt_lora_swap_item* items, int32_t count, void* stream) {
+  if (count < 0) return fail(ATTT_EINVAL, "lora_hot_swap: count must be >= 0");
+  if (count > 0 && !items) return fail(ATTT_EINVAL, "lora_hot_swap: items is null");
+  std::vector<LoraSwapJob> jobs;
+  for (int32_t i = 0; i < count; ++i) {
+    const attt_lora_swap_item& q = items[i];
+    if (q.n < 0) return fail(ATTT_EINVAL, "lora_hot_swap[%d]: n must be >= 0", i);
+    if (q.n >= ((int64_t)1 << 31)) return fail(ATTT_EUNSUPPORTED, "lora_hot_swap[%d]: n beyond this build's limits", i);
+    if (q.n == 0) continue;
+    if (!q.src || !q.dst) return fail(ATTT_EINVAL, "lora_hot_swap[%d]: src / dst is null", i);
+    if (reinterpret_cast<uintptr_t>(q.src) % 4 || reinterpret_cast<uintptr_t>(q.dst) % 2)
+      return fail(ATTT_EINVAL, "lora_hot_swap[%d]: misaligned array", i);
+    LoraSwapJob J{};
+    J.src = q.src;
+    J.dst = static_cast<uint16_t*>(q.dst);
+    J.n = q.n;
+    J.vec = aligned16(q.src) && aligned16(q.dst);
+    jobs.push_back(J);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return lora_launch_all(
+      jobs, [](const LoraSwapJob& J) { return (int)ceil_div(J.n, (int64_t)kLoraSwapPerBlock); },
+      [&](const LoraSwapBatch& b, int n) { return launch_lora_swap(b, n, s); }, "lora_swap");
 }

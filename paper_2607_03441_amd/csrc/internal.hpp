@@ -34,6 +34,8 @@ enum KernelId {
   K_ATTN_FWD,
   K_ATTN_DKDV,
   K_ATTN_DQ,
+  K_LORA_FWD,
+  K_LORA_SWAP,
   K_NUM_KERNELS
 };
 
@@ -362,5 +364,54 @@ hipError_t launch_lora_pass1(int dtype, int nt, const LoraP1Batch& b, int blocks
                              hipStream_t s);
 hipError_t launch_lora_pass2(int dtype, const LoraP2Batch& b, int blocks, uint8_t* ws, hipStream_t s);
 hipError_t launch_lora_reduce(const LoraRedBatch& b, int blocks, uint8_t* ws, hipStream_t s);
+
+// ---- serving: grouped multi-adapter forward, adapter swap --------------------------------
+// A job is a group of adapted projections reading one input x [rows, d_in] (one episode's
+// rows; q, k and v of a layer together). Phase 1 computes U = x A^T for up to four units of
+// 16 ranks; phase 2 adds scale-weighted U B^T into each projection's y [rows, d_out].
+struct LoraFwdUnit {
+  const void* A;    // first row of the unit in its problem's A [rank, d_in]
+  float scale;
+  int32_t valid;    // ranks in the unit (<= 16); the rest read as zero
+};
+struct LoraFwdOut {
+  const void* B;    // [d_out, rank]
+  void* y;          // [rows, d_out], updated in place
+  int32_t d_out, rank;
+  int32_t u0;       // first column of U that belongs to this projection
+  int32_t pad;
+};
+struct LoraFwdJob {
+  const void* x;
+  int32_t rows, d_in;
+  int32_t nu, no;   // units, projections
+  int32_t rb;       // rows per workgroup: 64 (one wave per 16 rows) or 16 (four waves split d_in)
+  int32_t kw;       // waves splitting d_in: 1 or 4
+  int32_t ncs;      // column splits of the outputs (workgroups per row block)
+  int32_t b_begin;  // first logical workgroup
+  LoraFwdUnit u[kLoraMaxTiles];
+  LoraFwdOut o[kLoraMaxTiles];
+};
+constexpr int kLoraFwdBatch = 16;
+struct LoraFwdBatch {
+  int32_t count;
+  int32_t total;    // logical workgroups
+  LoraFwdJob j[kLoraFwdBatch];
+};
+static_assert(sizeof(LoraFwdBatch) <= 3840, "kernel arguments");
+// nu: the largest unit count of the batch's jobs
+hipError_t launch_lora_fwd(int nu, const LoraFwdBatch& b, hipStream_t s);
+
+// Swap: dst (bf16) = RN(src (float32)) for every tensor of the batch.
+struct LoraSwapJob {
+  const float* src;
+  uint16_t* dst;
+  int64_t n;
+  int32_t b_begin;
+  int32_t vec;      // src and dst 16-byte aligned
+};
+using LoraSwapBatch = LoraBatchOf<LoraSwapJob>;
+constexpr int kLoraSwapPerBlock = 2048;  // elements per workgroup (256 threads x 8)
+hipError_t launch_lora_swap(const LoraSwapBatch& b, int blocks, hipStream_t s);
 
 }  // namespace attt

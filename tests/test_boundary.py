@@ -337,3 +337,47 @@ def test_attention_validation(L):
     assert _attn(L, ptr=ctypes.c_void_p(0x7F0000000008)) == attt.EINVAL  # misaligned
     assert _attn(L, N=1 << 29, H=8, Hkv=8) == attt.EUNSUPPORTED
     assert _attn(L, N=0, off=[0, 0]) == attt.OK               # nothing to do, nothing touched
+
+
+def _fwd(L, count=1, **kw):
+    p = dict(x=FAKE, y=FAKE_WS, A=FAKE, B=FAKE_WS, rows=32, d_in=64, d_out=64, rank=8, scale=2.0)
+    p.update(kw)
+    arr = (attt.LoraFwdProblem * 1)(attt.LoraFwdProblem(**p))
+    return L.attt_lora_forward(arr, count, None)
+
+
+def test_lora_forward_validation(L):
+    assert _fwd(L, rank=0) == attt.EINVAL
+    assert _fwd(L, rank=65) == attt.EINVAL
+    assert _fwd(L, d_in=60) == attt.EINVAL
+    assert _fwd(L, d_out=0) == attt.EINVAL
+    assert _fwd(L, rows=-1) == attt.EINVAL
+    assert _fwd(L, y=None) == attt.EINVAL
+    assert _fwd(L, B=ctypes.c_void_p(0x7F0000000008)) == attt.EINVAL
+    assert _fwd(L, scale=float("nan")) == attt.EINVAL
+    assert _fwd(L, rows=1 << 24) == attt.EUNSUPPORTED
+    assert _fwd(L, d_in=1 << 20) == attt.EUNSUPPORTED
+    assert _fwd(L, count=-1) == attt.EINVAL
+    assert L.attt_lora_forward(None, 1, None) == attt.EINVAL
+    # nothing to do: no launch
+    assert _fwd(L, rows=0, x=None, y=None, A=None, B=None) == attt.OK
+    assert L.attt_lora_forward(None, 0, None) == attt.OK
+
+
+def _swap(L, count=1, **kw):
+    p = dict(src=FAKE, dst=FAKE_WS, n=100)
+    p.update(kw)
+    arr = (attt.LoraSwapItem * 1)(attt.LoraSwapItem(**p))
+    return L.attt_lora_hot_swap(arr, count, None)
+
+
+def test_lora_hot_swap_validation(L):
+    assert _swap(L, n=-1) == attt.EINVAL
+    assert _swap(L, src=None) == attt.EINVAL
+    assert _swap(L, dst=None) == attt.EINVAL
+    assert _swap(L, src=ctypes.c_void_p(0x7F0000000002)) == attt.EINVAL
+    assert _swap(L, dst=ctypes.c_void_p(0x7F0000000001)) == attt.EINVAL
+    assert _swap(L, n=1 << 31) == attt.EUNSUPPORTED
+    assert _swap(L, count=-1) == attt.EINVAL
+    assert L.attt_lora_hot_swap(None, 1, None) == attt.EINVAL
+    assert _swap(L, src=None, dst=None, n=0) == attt.OK
