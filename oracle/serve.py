@@ -29,28 +29,23 @@ def round_f64_to_bf16_bits(v):
     float32, which could round twice). bf16 keeps 7 of float64's 52 fraction bits; below
     2^-126 its spacing is the fixed 2^-133, past its largest finite value it gives infinity."""
     v = np.asarray(v, np.float64)
-    out = np.empty(v.shape, np.uint16)
-    flat, res = v.reshape(-1), out.reshape(-1)
-    for i, x in enumerate(flat.tolist()):
-        if x != x:
-            res[i] = 0x7FC0
-            continue
-        neg = x < 0 or (x == 0 and np.signbit(x))
-        a = abs(x)
-        if a < 2.0 ** -126:
-            q = np.rint(a / 2.0 ** -133) * 2.0 ** -133       # exact scaling, ties to even
-        elif a == np.inf:
-            q = a
-        else:
-            b = np.float64(a).view(np.uint64).item()
-            keep = 52 - 7
-            b = (b + (1 << (keep - 1)) - 1 + ((b >> keep) & 1)) >> keep << keep
-            q = np.uint64(b).view(np.float64).item()
-            if q >= 2.0 ** 128:
-                q = np.inf
-        bits = int(np.float32(q).view(np.uint32)) >> 16      # q is exact in bf16, so in float32
-        res[i] = bits | (0x8000 if neg else 0)
-    return out
+    a = np.abs(v)
+    neg = np.signbit(v)
+    # normal range: round the float64 bit pattern at bit 45, half to even
+    b = a.view(np.uint64)
+    keep = np.uint64(52 - 7)
+    half = np.uint64(1 << 44)
+    odd = (b >> keep) & np.uint64(1)
+    r = ((b + half - np.uint64(1) + odd) >> keep) << keep
+    q = r.view(np.float64)
+    # below 2^-126: multiples of 2^-133 (exact scaling, np.rint ties to even)
+    small = a < 2.0 ** -126
+    q = np.where(small, np.rint(a * 2.0 ** 133) * 2.0 ** -133, q)
+    q = np.where(q >= 2.0 ** 128, np.inf, q)
+    with np.errstate(over="ignore"):
+        bits = (q.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)   # q is exact in bf16
+    bits = bits | np.where(neg, np.uint16(0x8000), np.uint16(0))
+    return np.where(np.isnan(v), np.uint16(0x7FC0), bits).astype(np.uint16)
 
 
 def lora_forward(x_bits, y_bits, A_bits, B_bits, scale):
