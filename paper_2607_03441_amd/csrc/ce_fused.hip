@@ -43,8 +43,12 @@
 namespace attt {
 
 constexpr int kSlotBytes = 256 * 256 * 2;  // one bf16 tile [256 tokens][256 vocab]
-// dynamic LDS: the mainloops' two stage buffers, then the producer's per-token sums [2][256]
-constexpr size_t kFusedLds = CfgBig::LDS + 2 * 256 * sizeof(float);
+// Dynamic LDS: the mainloops' two stage buffers, the producer's per-token sums [2][256], then
+// four ints of workgroup state.
+// There is no static LDS, so the stage buffers start at LDS address 0 and every LDS-DMA
+// destination is 1 KiB-aligned.
+constexpr size_t kFusedLdsData = CfgBig::LDS + 2 * 256 * sizeof(float);
+constexpr size_t kFusedLds = kFusedLdsData + 4 * sizeof(int);
 
 // sync area (ints): team counts [8], arrive, abort, the site of the first wait that ran out
 // (diagnostics: 1 grid barrier, 2 consumer awaiting a tile, 3 producer awaiting a free slot,
@@ -254,7 +258,7 @@ template <bool kLabel>
 __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
   using C = CfgBig;
   extern __shared__ __align__(16) uint8_t smem[];
-  __shared__ int info[4];
+  int* info = reinterpret_cast<int*>(smem + kFusedLdsData);
   int* sync = a.sync;
   int* abort = sync + kSyncAbort;
   const int tid = threadIdx.x;

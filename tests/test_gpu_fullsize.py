@@ -10,7 +10,7 @@ element against the bound of the oracle-sized tests."""
 import numpy as np
 import pytest
 
-from gpu_util import check_rows, cosine, dev_dense, dev_f32, dev_i32, host, note
+from gpu_util import check_rows, cosine, dev_dense, dev_f32, dev_i32, host, note, rel_norm
 from oracle import ce as oce
 from oracle import lora as olora
 from oracle import ngram as ongram
@@ -97,6 +97,14 @@ def test_lora_full(attt, wl):
     for p, q in zip(probs, dev):
         dA_o, dB_o = olora.lora_grad(p["x"].f32, p["dy"].f32, p["A"].f32, p["B"].f32, p["scale"])
         dA, dB = host(q["dA"]), host(q["dB"])
+        # error figures: the GPU (U, dU carried as bf16 pairs between its passes) against a
+        # plain float32 evaluation of the same products, both against the float64 oracle
+        x32, dy32 = p["x"].f32, p["dy"].f32
+        U32 = x32 @ p["A"].f32.T
+        dU32 = np.float32(p["scale"]) * (dy32 @ p["B"].f32)
+        dA32, dB32 = dU32.T @ x32, np.float32(p["scale"]) * (dy32.T @ U32)
+        note(f"{p['name']}: normwise rel err dA {rel_norm(dA, dA_o):.2e} (float32 {rel_norm(dA32, dA_o):.2e}), "
+             f"dB {rel_norm(dB, dB_o):.2e} (float32 {rel_norm(dB32, dB_o):.2e})")
         assert cosine(dA, dA_o) >= BF16_COS and cosine(dB, dB_o) >= BF16_COS, p["name"]
         check_rows(dA, dA_o, BF16_COS, BF16_ELEM, f"dA {p['name']}")
         check_rows(dB, dB_o, BF16_COS, BF16_ELEM, f"dB {p['name']}")
