@@ -71,22 +71,24 @@ __device__ __forceinline__ void mma_nt(const bf16_t* A, int lda, int row0, const
   }
 }
 
-// The block a workgroup works on: episode, head, block index.
-__device__ __forceinline__ void attn_locate(const AttnBatch& b, int heads, int& ei, int& head, int& blk) {
+// The block a workgroup works on: episode, head, block index. Workgroups start in launch
+// order, so the long causal rows go first: the last query blocks for the per-query kernels
+// (`late_first`), the first key blocks for the per-key kernel.
+__device__ __forceinline__ void attn_locate(const AttnBatch& b, int heads, bool late_first, int& ei, int& head,
+                                            int& blk) {
   ei = 0;
   while (ei + 1 < b.count && b.e[ei + 1].wg_begin <= (int)blockIdx.x) ++ei;
   const int local = (int)blockIdx.x - b.e[ei].wg_begin;
   const int nb = b.e[ei].blocks;
-  // long rows of blocks first (causal work grows with the block index)
   head = local % heads;
-  blk = nb - 1 - local / heads;
+  blk = late_first ? nb - 1 - local / heads : local / heads;
 }
 
 }  // namespace
 
 __global__ __launch_bounds__(256) void attn_fwd_stats_kernel(AttnArgs a, AttnBatch b) {
   int ei, h, qb;
-  attn_locate(b, a.heads, ei, h, qb);
+  attn_locate(b, a.heads, true, ei, h, qb);
   const AttnEp E = b.e[ei];
   const int kh = h / (a.heads / a.kv_heads);
   const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
@@ -182,79 +184,175 @@ __global__ __launch_bounds__(256) void attn_fwd_stats_kernel(AttnArgs a, AttnBat
   }
 }
 
-__global__ __launch_bounds__(256) void attn_dkdv_kernel(AttnArgs a, AttnBatch b) {
+// This wave's 16 keys as MFMA B operands over the head dimension: lane (l16, q4) holds key
+// `key` (its own) at columns 32 s + 8 q4 .. +7 for s = 0..3. Keys at or past nvalid read as zero.
+__device__ __forceinline__ void load_key_frags(bf16x8 (&f)[4], const bf16_t* src, int64_t stride, int key,
+                                               int nvalid, int q4) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (key < nvalid) v = *reinterpret_cast<const u32x4*>(src + (int64_t)key * stride + 32 * s + 8 * q4);
+    f[s] = __builtin_bit_cast(bf16x8, v);
+  }
+}
+
+// Rows [0, BLK) of a [rows][DH] block, staged in LDS twice: row-major into dst (pitch PR) and
+// transposed into dstT[c][r] (pitch PT). Thread tid takes rows 4 (tid / 16) .. +3 and columns
+// 8 (tid % 16) .. +7: fetch_block issues its four 16-byte loads (rows >= nvalid read as zero),
+// store_block writes them with four 16-byte stores and, for each of its eight columns, one
+// 8-byte store of the four rows.
+__device__ __forceinline__ void fetch_block(u32x4 (&v)[4], const bf16_t* src, int64_t stride, int nvalid, int tid) {
+  const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 8;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = u32x4{0u, 0u, 0u, 0u};
+    if (r0 + i < nvalid) v[i] = *reinterpret_cast<const u32x4*>(src + (int64_t)(r0 + i) * stride + c0);
+  }
+}
+
+__device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, bf16_t* dstT, int tid) {
+  const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 8;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
+  if (!dstT) return;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int wi = e >> 1, sh = (e & 1) * 16;
+    const uint32_t x0 = (v[0][wi] >> sh) & 0xFFFFu, x1 = (v[1][wi] >> sh) & 0xFFFFu;
+    const uint32_t x2 = (v[2][wi] >> sh) & 0xFFFFu, x3 = (v[3][wi] >> sh) & 0xFFFFu;
+    *reinterpret_cast<uint2*>(dstT + (c0 + e) * PT + r0) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
+  }
+}
+
+// hi = RN(x), lo = RN(x - hi) of the eight values of an MFMA operand, as bf16x8 pairs.
+__device__ __forceinline__ void split_frag(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+  u32x4 h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
+    l[i] = pack_bf16x2(x[2 * i] - bf16_bits_to_f32(h[i] & 0xFFFFu), x[2 * i + 1] - bf16_bits_to_f32(h[i] >> 16));
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// B operand over 32 queries of chunk u from a transposed tile T[c][q] (pitch PT): lane (l16, q4)
+// takes column c = c0 + l16 at queries 32 u + 4 q4 .. +3 and 32 u + 16 + 4 q4 .. +3, the order in
+// which the P / dS fragments hold them.
+__device__ __forceinline__ bf16x8 tfrag(const bf16_t* T, int c, int u, int q4) {
+  const bf16_t* p = T + c * PT + 32 * u + 4 * q4;
+  const uint2 a = *reinterpret_cast<const uint2*>(p);
+  const uint2 b = *reinterpret_cast<const uint2*>(p + 16);
+  return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
+}
+
+// dK, dV of one (key/value head, 64-key block). Wave w owns keys 16 w .. 16 w + 15; their K and
+// V fragments stay in registers. Per query block: S = Q K^T and dP = dO V^T with the queries on
+// the MFMA rows (four tiles of 16) and this wave's keys on the columns, so each lane holds 16
+// (query, key) values of its own key. P and dS = P (dP - D) then feed dV += P^T dO and
+// dK += dS^T Q straight from those registers as the A operand: the contraction runs over the
+// queries, and the 8 values a lane holds per 32-query chunk (tile rows 4 q4 .. +3 of two tiles)
+// are its k slots; the B operand reads the transposed dO and Q tiles in the same query order.
+__global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch b) {
   int ei, kh, kb;
-  attn_locate(b, a.kv_heads, ei, kh, kb);
+  attn_locate(b, a.kv_heads, false, ei, kh, kb);
   const AttnEp E = b.e[ei];
   const int g = a.heads / a.kv_heads;
   const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
   extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* Vs = Ks + BLK * PR;
-  bf16_t* Qs = Vs + BLK * PR;
-  bf16_t* dOs = Qs + BLK * PR;
+  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
+  bf16_t* dOs = Qs + BLK * PR;                    // [64][PR]
   bf16_t* Qt = dOs + BLK * PR;                    // [128][PT]
-  bf16_t* dOt = Qt + DH * PT;
-  bf16_t* PTs = dOt + DH * PT;                    // [64 keys][PT] P^T, high part
-  bf16_t* PTl = PTs + BLK * PT;                   // P^T, low part
-  bf16_t* dSTs = PTl + BLK * PT;                  // dS^T, high part
-  bf16_t* dSTl = dSTs + BLK * PT;                 // dS^T, low part
-  float* lse_s = reinterpret_cast<float*>(dSTl + BLK * PT);  // [64]
-  float* d_s = lse_s + BLK;                                  // [64]
+  bf16_t* dOt = Qt + DH * PT;                     // [128][PT]
+  float* lse_s = reinterpret_cast<float*>(dOt + DH * PT);  // [64]
+  float* d_s = lse_s + BLK;                                // [64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
+  const int key = 16 * w + l16;  // this lane's key in the block
   const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
-  load_block(Ks, nullptr, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
-  load_block(Vs, nullptr, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
+  bf16x8 kf[4], vf[4];
+  load_key_frags(kf, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, key, nk, q4);
+  load_key_frags(vf, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, key, nk, q4);
   f32x4 dk[8], dv[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) dk[j] = f32x4{0, 0, 0, 0}, dv[j] = f32x4{0, 0, 0, 0};
   const float sl = a.scale * kLog2e;
   const int nqb = (E.L + BLK - 1) / BLK;
-  for (int hh = 0; hh < g; ++hh) {
-    const int h = kh * g + hh;
-    for (int qb = kb; qb < nqb; ++qb) {
-      const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
-      __syncthreads();  // previous step's reads are done
-      load_block(Qs, Qt, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
-      load_block(dOs, dOt, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
-      if (tid < BLK) {
-        const int64_t t = (int64_t)h * a.N + E.row0 + q0 + tid;
-        lse_s[tid] = tid < nq ? a.lse[t] * kLog2e : INFINITY;  // absent rows: P = 0
-        d_s[tid] = tid < nq ? a.dsum[t] : 0.0f;
-      }
-      __syncthreads();
-      // S^T and dP^T: this wave's 16 keys x 64 queries
-      f32x4 st[4], dpt[4];
+  // (query head, query block) steps: query heads of the group outer, the causal blocks from kb
+  const int per_head = nqb - kb, steps = g * per_head;
+  u32x4 fq[4], fo[4];
+  float fl = INFINITY, fd = 0.0f;
+  auto fetch = [&](int i) {
+    const int h = kh * g + i / per_head, q0 = (kb + i % per_head) * BLK, nq = min(BLK, E.L - q0);
+    fetch_block(fq, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
+    fetch_block(fo, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
+    if (tid < BLK) {
+      const int64_t t = (int64_t)h * a.N + E.row0 + q0 + tid;
+      fl = tid < nq ? a.lse[t] * kLog2e : INFINITY;  // absent rows: P = 0
+      fd = tid < nq ? a.dsum[t] : 0.0f;
+    }
+  };
+  fetch(0);
+  for (int i = 0; i < steps; ++i) {
+    const int q0 = (kb + i % per_head) * BLK;
+    __syncthreads();  // the previous step's reads of the tiles are done
+    store_block(fq, Qs, Qt, tid);
+    store_block(fo, dOs, dOt, tid);
+    if (tid < BLK) lse_s[tid] = fl, d_s[tid] = fd;
+    __syncthreads();
+    if (i + 1 < steps) fetch(i + 1);  // the next step's blocks load while this one computes
+    {
+      // S[16 t + 4 q4 + r][key] and dP likewise
+      f32x4 st[4], dp[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) st[j] = f32x4{0, 0, 0, 0}, dpt[j] = f32x4{0, 0, 0, 0};
-      mma_nt<DH / 32, 4>(Ks, PR, 16 * w, Qs, PR, 0, st, lane);
-      mma_nt<DH / 32, 4>(Vs, PR, 16 * w, dOs, PR, 0, dpt, lane);
+      for (int t = 0; t < 4; ++t) st[t] = f32x4{0, 0, 0, 0}, dp[t] = f32x4{0, 0, 0, 0};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int qc = 16 * j + l16;  // query column
-        const float ls = lse_s[qc], dd = d_s[qc];
+      for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const bf16x8 aq = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(Qs + (16 * t + l16) * PR + 32 * s4 + 8 * q4));
+          const bf16x8 ao = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(dOs + (16 * t + l16) * PR + 32 * s4 + 8 * q4));
+          st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, kf[s4], st[t], 0, 0, 0);
+          dp[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, vf[s4], dp[t], 0, 0, 0);
+        }
+      // P and dS of this lane's 16 (query, key) pairs, in fragment order: chunk u, slot i is
+      // query 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4
+      float pv[2][8], dsv[2][8];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const f32x4 ls = *reinterpret_cast<const f32x4*>(lse_s + 16 * t + 4 * q4);
+        const f32x4 dd = *reinterpret_cast<const f32x4*>(d_s + 16 * t + 4 * q4);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int kr = 16 * w + 4 * q4 + r;  // key row
-          const bool ok = (k0 + kr <= q0 + qc) && (kr < nk);
-          const float p = ok ? __builtin_amdgcn_exp2f(st[j][r] * sl - ls) : 0.0f;
-          const float ds = p * (dpt[j][r] - dd);
-          const bf16_t hi = f2bf(ds), phi = f2bf(p);
-          PTs[kr * PT + qc] = phi;
-          PTl[kr * PT + qc] = f2bf(p - bf2f(phi));
-          dSTs[kr * PT + qc] = hi;
-          dSTl[kr * PT + qc] = f2bf(ds - bf2f(hi));
+          const int ql = 16 * t + 4 * q4 + r;
+          const bool ok = (k0 + key <= q0 + ql) && (key < nk);
+          const float p = ok ? __builtin_amdgcn_exp2f(st[t][r] * sl - ls[r]) : 0.0f;
+          pv[t >> 1][4 * (t & 1) + r] = p;
+          dsv[t >> 1][4 * (t & 1) + r] = p * (dp[t][r] - dd[r]);
         }
       }
-      __syncthreads();
-      mma_nt<BLK / 32, 8>(PTs, PT, 16 * w, dOt, PT, 0, dv, lane);
-      mma_nt<BLK / 32, 8>(PTl, PT, 16 * w, dOt, PT, 0, dv, lane);
-      mma_nt<BLK / 32, 8>(dSTs, PT, 16 * w, Qt, PT, 0, dk, lane);
-      mma_nt<BLK / 32, 8>(dSTl, PT, 16 * w, Qt, PT, 0, dk, lane);
+      bf16x8 ph[2], pl[2], sh[2], slo[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        split_frag(pv[u], ph[u], pl[u]);
+        split_frag(dsv[u], sh[u], slo[u]);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const bf16x8 bo = tfrag(dOt, 16 * j + l16, u, q4);
+          dv[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bo, dv[j], 0, 0, 0);
+          dv[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bo, dv[j], 0, 0, 0);
+          const bf16x8 bq = tfrag(Qt, 16 * j + l16, u, q4);
+          dk[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh[u], bq, dk[j], 0, 0, 0);
+          dk[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bq, dk[j], 0, 0, 0);
+        }
     }
   }
-  // write this wave's 16 keys
+  // D of dV / dK tile j: lane (l16, q4), register r -> key 16 w + 4 q4 + r, column 16 j + l16
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int kr = 16 * w + 4 * q4 + r;
@@ -269,66 +367,89 @@ __global__ __launch_bounds__(256) void attn_dkdv_kernel(AttnArgs a, AttnBatch b)
   }
 }
 
-__global__ __launch_bounds__(256) void attn_dq_kernel(AttnArgs a, AttnBatch b) {
+// dQ of one (query head, 64-query block). Wave w owns queries 16 w .. 16 w + 15; their Q and
+// dO fragments stay in registers. Per key block: S^T = K Q^T and dP^T = V dO^T with the keys on
+// the MFMA rows and this wave's queries on the columns, so each lane holds 16 (key, query)
+// values of its own query; dS then feeds dQ += dS K as the A operand (the contraction runs over
+// the keys in the order the lane holds them), with the B operand from the transposed K tile.
+__global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b) {
   int ei, h, qb;
-  attn_locate(b, a.heads, ei, h, qb);
+  attn_locate(b, a.heads, true, ei, h, qb);
   const AttnEp E = b.e[ei];
   const int kh = h / (a.heads / a.kv_heads);
   const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
   extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* dOs = Qs + BLK * PR;
-  bf16_t* Ks = dOs + BLK * PR;
-  bf16_t* Vs = Ks + BLK * PR;
-  bf16_t* Kt = Vs + BLK * PR;   // [128][PT]
-  bf16_t* dSs = Kt + DH * PT;   // [64][PT] dS, high part
-  bf16_t* dSl = dSs + BLK * PT; // low part
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
+  bf16_t* Vs = Ks + BLK * PR;                     // [64][PR]
+  bf16_t* Kt = Vs + BLK * PR;                     // [128][PT]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
+  const int qry = 16 * w + l16;  // this lane's query in the block
   const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
-  load_block(Qs, nullptr, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
-  load_block(dOs, nullptr, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
-  float ls[4], dd[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qi = 16 * w + 4 * q4 + r;
-    const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qi;
-    ls[r] = qi < nq ? a.lse[t] * kLog2e : INFINITY;
-    dd[r] = qi < nq ? a.dsum[t] : 0.0f;
-  }
+  bf16x8 qf[4], of[4];
+  load_key_frags(qf, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  load_key_frags(of, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qry;
+  const float ls = qry < nq ? a.lse[t] * kLog2e : INFINITY;  // absent queries: P = 0
+  const float dd = qry < nq ? a.dsum[t] : 0.0f;
   f32x4 dq[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) dq[j] = f32x4{0, 0, 0, 0};
   const float sl = a.scale * kLog2e;
+  u32x4 fk[4], fv[4];
+  auto fetch = [&](int kb) {
+    const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
+    fetch_block(fk, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
+    fetch_block(fv, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
+  };
+  fetch(0);
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
+    __syncthreads();  // the previous block's reads of the tiles are done
+    store_block(fk, Ks, Kt, tid);
+    store_block(fv, Vs, nullptr, tid);
     __syncthreads();
-    load_block(Ks, Kt, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
-    load_block(Vs, nullptr, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
-    __syncthreads();
-    f32x4 s[4], dp[4];
+    if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
+    // S^T[16 t + 4 q4 + r][query] and dP^T likewise
+    f32x4 st[4], dp[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) s[j] = f32x4{0, 0, 0, 0}, dp[j] = f32x4{0, 0, 0, 0};
-    mma_nt<DH / 32, 4>(Qs, PR, 16 * w, Ks, PR, 0, s, lane);
-    mma_nt<DH / 32, 4>(dOs, PR, 16 * w, Vs, PR, 0, dp, lane);
+    for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0}, dp[tt] = f32x4{0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int kc = 16 * j + l16;
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        const bf16x8 ak = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+        const bf16x8 av = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(Vs + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+        st[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[s4], st[tt], 0, 0, 0);
+        dp[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, of[s4], dp[tt], 0, 0, 0);
+      }
+    // dS of this lane's query against 16 keys, in fragment order: chunk u, slot i is key
+    // 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4
+    float dsv[2][8];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int qi = 16 * w + 4 * q4 + r;
-        const bool ok = (k0 + kc <= q0 + qi) && (kc < nk);
-        const float p = ok ? __builtin_amdgcn_exp2f(s[j][r] * sl - ls[r]) : 0.0f;
-        const float ds = p * (dp[j][r] - dd[r]);
-        const bf16_t hi = f2bf(ds);
-        dSs[qi * PT + kc] = hi;
-        dSl[qi * PT + kc] = f2bf(ds - bf2f(hi));
+        const int kl = 16 * tt + 4 * q4 + r;
+        const bool ok = (k0 + kl <= q0 + qry) && (kl < nk);
+        const float p = ok ? __builtin_amdgcn_exp2f(st[tt][r] * sl - ls) : 0.0f;
+        dsv[tt >> 1][4 * (tt & 1) + r] = p * (dp[tt][r] - dd);
       }
-    }
-    __syncthreads();
-    mma_nt<BLK / 32, 8>(dSs, PT, 16 * w, Kt, PT, 0, dq, lane);
-    mma_nt<BLK / 32, 8>(dSl, PT, 16 * w, Kt, PT, 0, dq, lane);
+    bf16x8 sh[2], slo[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) split_frag(dsv[u], sh[u], slo[u]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const bf16x8 bk = tfrag(Kt, 16 * j + l16, u, q4);
+        dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh[u], bk, dq[j], 0, 0, 0);
+        dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bk, dq[j], 0, 0, 0);
+      }
   }
+  // D of dQ tile j: lane (l16, q4), register r -> query 16 w + 4 q4 + r, column 16 j + l16
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int qi = 16 * w + 4 * q4 + r;
@@ -341,8 +462,8 @@ __global__ __launch_bounds__(256) void attn_dq_kernel(AttnArgs a, AttnBatch b) {
 
 size_t attn_lds_bytes(int kernel) {
   if (kernel == 0) return (size_t)(2 * BLK * PR + DH * PT + 2 * BLK * PT) * 2;
-  if (kernel == 1) return (size_t)(4 * BLK * PR + 2 * DH * PT + 4 * BLK * PT) * 2 + 2 * BLK * 4;
-  return (size_t)(4 * BLK * PR + DH * PT + 2 * BLK * PT) * 2;
+  if (kernel == 1) return (size_t)(2 * BLK * PR + 2 * DH * PT) * 2 + 2 * BLK * 4;
+  return (size_t)(2 * BLK * PR + DH * PT) * 2;
 }
 
 hipError_t launch_attn(int kernel, const AttnArgs& a, const AttnBatch& b, int wgs, hipStream_t s) {
