@@ -4,18 +4,26 @@
 // accumulation. With S = scale Q K^T, P = softmax(S) over the allowed keys, O = P V:
 //   D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
 //   dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO.
-// Three kernels, each recomputing S from Q and K on v_mfma_f32_16x16x32_bf16 (64 x 64 blocks,
-// four waves of 16 rows; operands in LDS rows padded so that fragment reads do not conflict):
+// Three kernels, each recomputing S from Q and K on v_mfma_f32_16x16x32_bf16 over 64 x 64
+// blocks, 256 threads (four waves of 16 rows), blocks in the causal order with the longest rows
+// first, the next block's global loads in flight while the current one computes:
 //   attn_fwd_stats_kernel  per (query head, 64-query block): lse and D (online softmax; O kept
 //                          in float32 registers and contracted with dO, never written)
 //   attn_dkdv_kernel       per (key/value head, 64-key block): dK and dV accumulated in
 //                          registers over every query head of the group and every later query
 //                          block, in a fixed order (no atomics)
 //   attn_dq_kernel         per (query head, 64-query block): dQ over the allowed key blocks
-// P and dS enter their second products (O = P V for D, dV = P^T dO, dQ = dS K, dK = dS^T Q) as
-// bf16 pairs hi + lo (two MFMA passes, about 16 significant bits): those sums mix signs (dS even
-// sums to zero over each row), and a single bf16 rounding of P or dS would show in their small
-// elements. The final bf16 rounding of the outputs is then the main error.
+// The operand that stays in a wave (its 16 queries, or its 16 keys) is held in registers as
+// the B operand of the score products, so each lane ends up with 16 scores of its own row. The
+// probabilities (or dS) of that row then enter the second product (P V, P^T dO, dS^T Q, dS K)
+// directly as the A operand: the contraction index is the one the lane's registers run over,
+// in the order they hold it, and the B operand is read from a transposed LDS tile in the same
+// order. Every block goes to LDS once row-major and, where a product needs it, once transposed,
+// with 16- and 8-byte stores.
+// P and dS enter their second products as bf16 pairs hi + lo (two MFMA passes, about 16
+// significant bits): those sums mix signs (dS even sums to zero over each row), and a single
+// bf16 rounding of P or dS would show in their small elements. The final bf16 rounding of the
+// outputs is then the main error.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -31,46 +39,6 @@ constexpr float kLog2e = 1.4426950408889634f;
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 __device__ __forceinline__ bf16_t f2bf(float x) { return (bf16_t)(pack_bf16x2(x, 0.0f) & 0xFFFFu); }
 
-// rows [0, BLK) of a [rows][DH] bf16 tensor (row stride `stride` elements) into LDS `dst`
-// (pitch PR) if given and, if `dstT` is given, transposed into dstT[c][r] (pitch PT). Rows >=
-// nvalid read as zero.
-__device__ __forceinline__ void load_block(bf16_t* dst, bf16_t* dstT, const bf16_t* src, int64_t stride,
-                                           int nvalid, int tid) {
-#pragma unroll
-  for (int i = 0; i < (BLK * DH / 8) / 256; ++i) {
-    const int c = tid + 256 * i;
-    const int r = c >> 4, c8 = (c & 15) * 8;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (r < nvalid) v = *reinterpret_cast<const u32x4*>(src + (int64_t)r * stride + c8);
-    if (dst) *reinterpret_cast<u32x4*>(dst + r * PR + c8) = v;
-    if (dstT) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dstT[(c8 + 2 * e) * PT + r] = (bf16_t)(v[e] & 0xFFFFu);
-        dstT[(c8 + 2 * e + 1) * PT + r] = (bf16_t)(v[e] >> 16);
-      }
-    }
-  }
-}
-
-// acc[j] += A[row0 + 0..15][0..32*KS) * B[col0 + 16 j + 0..15][0..32*KS)^T, both LDS row-major
-// with K contiguous (pitches lda, ldb).
-template <int KS, int NJ>
-__device__ __forceinline__ void mma_nt(const bf16_t* A, int lda, int row0, const bf16_t* B, int ldb, int col0,
-                                       f32x4 (&acc)[NJ], int lane) {
-  const int l16 = lane & 15, q4 = lane >> 4;
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(A + (row0 + l16) * lda + ks * 32 + q4 * 8));
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const bf16x8 b = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(B + (col0 + 16 * j + l16) * ldb + ks * 32 + q4 * 8));
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
-    }
-  }
-}
-
 // The block a workgroup works on: episode, head, block index. Workgroups start in launch
 // order, so the long causal rows go first: the last query blocks for the per-query kernels
 // (`late_first`), the first key blocks for the per-key kernel.
@@ -85,104 +53,6 @@ __device__ __forceinline__ void attn_locate(const AttnBatch& b, int heads, bool 
 }
 
 }  // namespace
-
-__global__ __launch_bounds__(256) void attn_fwd_stats_kernel(AttnArgs a, AttnBatch b) {
-  int ei, h, qb;
-  attn_locate(b, a.heads, true, ei, h, qb);
-  const AttnEp E = b.e[ei];
-  const int kh = h / (a.heads / a.kv_heads);
-  const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
-  extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* Ks = Qs + BLK * PR;                     // [64][PR]
-  bf16_t* Vt = Ks + BLK * PR;                     // [128][PT]
-  bf16_t* Ps = Vt + DH * PT;                      // [64][PT] P, high part
-  bf16_t* Pl = Ps + BLK * PT;                     // low part
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l16 = lane & 15, q4 = lane >> 4;
-  const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
-  load_block(Qs, nullptr, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
-  const float sl = a.scale * kLog2e;
-  float m[4], l[4];
-  f32x4 o[8];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) m[r] = -INFINITY, l[r] = 0.0f;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) o[j] = f32x4{0, 0, 0, 0};
-  for (int kb = 0; kb <= qb; ++kb) {
-    const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
-    __syncthreads();  // previous block's reads of Ks / Vt / Ps are done
-    load_block(Ks, nullptr, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
-    load_block(nullptr, Vt, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
-    __syncthreads();
-    f32x4 s[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) s[j] = f32x4{0, 0, 0, 0};
-    mma_nt<DH / 32, 4>(Qs, PR, 16 * w, Ks, PR, 0, s, lane);
-    // online softmax over this block (base-2 exponent of scale * S)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qi = q0 + 16 * w + 4 * q4 + r;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int kj = k0 + 16 * j + l16;
-        const float v = (kj <= qi && kj < E.L) ? s[j][r] * sl : -INFINITY;
-        s[j][r] = v;
-        mx = fmaxf(mx, v);
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-      const float mn = fmaxf(m[r], mx);
-      const float alpha = (m[r] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[r] - mn);
-      float sum = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float p = (s[j][r] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(s[j][r] - mn);
-        s[j][r] = p;
-        sum += p;
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off, 64);
-      l[r] = l[r] * alpha + sum;
-      m[r] = mn;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) o[j][r] *= alpha;
-    }
-    // P (bf16) of this wave's rows to LDS (the previous block's reads of Ps ended before the
-    // barrier at the top of this block), then O += P V
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bf16_t hi = f2bf(s[j][r]);
-        Ps[(16 * w + 4 * q4 + r) * PT + 16 * j + l16] = hi;
-        Pl[(16 * w + 4 * q4 + r) * PT + 16 * j + l16] = f2bf(s[j][r] - bf2f(hi));
-      }
-    __syncthreads();
-    mma_nt<BLK / 32, 8>(Ps, PT, 16 * w, Vt, PT, 0, o, lane);
-    mma_nt<BLK / 32, 8>(Pl, PT, 16 * w, Vt, PT, 0, o, lane);
-  }
-  // lse (natural log) and D = rowsum(dO * O) of this wave's 16 rows
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qi = 16 * w + 4 * q4 + r;
-    const float inv = l[r] > 0.0f ? 1.0f / l[r] : 0.0f;
-    float d = 0.0f;
-    if (qi < nq) {
-      const bf16_t* dor = a.dout + ((int64_t)(E.row0 + q0 + qi) * a.heads + h) * DH;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) d += bf2f(dor[16 * j + l16]) * (o[j][r] * inv);
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) d += __shfl_xor(d, off, 64);
-    if (l16 == 0 && qi < nq) {
-      const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qi;
-      a.lse[t] = m[r] / kLog2e + logf(l[r]);
-      a.dsum[t] = d;
-    }
-  }
-}
 
 // This wave's 16 keys as MFMA B operands over the head dimension: lane (l16, q4) holds key
 // `key` (its own) at columns 32 s + 8 q4 .. +7 for s = 0..3. Keys at or past nvalid read as zero.
@@ -212,8 +82,9 @@ __device__ __forceinline__ void fetch_block(u32x4 (&v)[4], const bf16_t* src, in
 
 __device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, bf16_t* dstT, int tid) {
   const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 8;
+  if (dst)
 #pragma unroll
-  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
   if (!dstT) return;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -244,6 +115,124 @@ __device__ __forceinline__ bf16x8 tfrag(const bf16_t* T, int c, int u, int q4) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);
   const uint2 b = *reinterpret_cast<const uint2*>(p + 16);
   return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
+}
+
+// lse and D = rowsum(dO * O) of one (query head, 64-query block). Wave w owns queries 16 w ..
+// 16 w + 15; their Q fragments stay in registers. Per key block: S^T = K Q^T with the keys on the
+// MFMA rows, so each lane holds 16 scores of its own query and the online softmax of a query
+// is a reduction over the lane's registers and its three partner lanes (lanes l, l + 16, l + 32,
+// l + 48 hold the same query). P then feeds O += P V as the A operand (contraction over the keys
+// in the order the lane holds them) with the B operand from the transposed V tile. O stays in
+// float32 registers, its row 4 q4 + r belonging to query 16 w + 4 q4 + r, and is never written.
+__global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, AttnBatch b) {
+  int ei, h, qb;
+  attn_locate(b, a.heads, true, ei, h, qb);
+  const AttnEp E = b.e[ei];
+  const int kh = h / (a.heads / a.kv_heads);
+  const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
+  extern __shared__ __align__(16) uint8_t smem[];
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
+  bf16_t* Vt = Ks + BLK * PR;                     // [128][PT]
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, q4 = lane >> 4;
+  const int qry = 16 * w + l16;
+  const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
+  bf16x8 qf[4];
+  load_key_frags(qf, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  const float sl = a.scale * kLog2e;
+  float m = -INFINITY, l = 0.0f;  // running max (base 2) and sum of this lane's query
+  f32x4 o[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) o[j] = f32x4{0, 0, 0, 0};
+  u32x4 fk[4], fv[4];
+  auto fetch = [&](int kb) {
+    const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
+    fetch_block(fk, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
+    fetch_block(fv, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
+  };
+  fetch(0);
+  for (int kb = 0; kb <= qb; ++kb) {
+    const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
+    __syncthreads();  // the previous block's reads of the tiles are done
+    store_block(fk, Ks, nullptr, tid);
+    store_block(fv, nullptr, Vt, tid);
+    __syncthreads();
+    if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
+    f32x4 st[4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        const bf16x8 ak = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+        st[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[s4], st[tt], 0, 0, 0);
+      }
+    // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r
+    float mx = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int kl = 16 * tt + 4 * q4 + r;
+        const float v = (k0 + kl <= q0 + qry && kl < nk) ? st[tt][r] * sl : -INFINITY;
+        st[tt][r] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
+    float pv[2][8], sum = 0.0f;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = (st[tt][r] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(st[tt][r] - mn);
+        pv[tt >> 1][4 * (tt & 1) + r] = p;
+        sum += p;
+      }
+    sum += __shfl_xor(sum, 16, 64);
+    sum += __shfl_xor(sum, 32, 64);
+    l = l * alpha + sum;
+    m = mn;
+    // O row 4 q4 + r is query 16 w + 4 q4 + r: its scale factor lives in lane 16 q4 + 4 q4 + r
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float ar = __shfl(alpha, 16 * q4 + 4 * q4 + r, 64);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j][r] *= ar;
+    }
+    bf16x8 ph[2], pl[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) split_frag(pv[u], ph[u], pl[u]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const bf16x8 bv = tfrag(Vt, 16 * j + l16, u, q4);
+        o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bv, o[j], 0, 0, 0);
+        o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bv, o[j], 0, 0, 0);
+      }
+  }
+  // lse of this lane's query; D of the queries of O's rows 4 q4 + r (normalised by their l)
+  if (q4 == 0 && qry < nq) a.lse[(int64_t)h * a.N + E.row0 + q0 + qry] = m / kLog2e + logf(l);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int qi = 16 * w + 4 * q4 + r;
+    const float lr = __shfl(l, 16 * q4 + 4 * q4 + r, 64);
+    const float inv = lr > 0.0f ? 1.0f / lr : 0.0f;
+    float d = 0.0f;
+    if (qi < nq) {
+      const bf16_t* dor = a.dout + ((int64_t)(E.row0 + q0 + qi) * a.heads + h) * DH;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d += bf2f(dor[16 * j + l16]) * (o[j][r] * inv);
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) d += __shfl_xor(d, off, 64);
+    if (l16 == 0 && qi < nq) a.dsum[(int64_t)h * a.N + E.row0 + q0 + qi] = d;
+  }
 }
 
 // dK, dV of one (key/value head, 64-key block). Wave w owns keys 16 w .. 16 w + 15; their K and
@@ -461,7 +450,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
 }
 
 size_t attn_lds_bytes(int kernel) {
-  if (kernel == 0) return (size_t)(2 * BLK * PR + DH * PT + 2 * BLK * PT) * 2;
+  if (kernel == 0) return (size_t)(BLK * PR + DH * PT) * 2;
   if (kernel == 1) return (size_t)(2 * BLK * PR + 2 * DH * PT) * 2 + 2 * BLK * 4;
   return (size_t)(2 * BLK * PR + DH * PT) * 2;
 }
