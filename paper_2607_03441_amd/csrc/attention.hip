@@ -67,7 +67,7 @@ __device__ __forceinline__ void load_key_frags(bf16x8 (&f)[4], const bf16_t* src
 }
 
 // Rows [0, BLK) of a [rows][DH] block, staged in LDS twice: row-major into dst (pitch PR) and
-// transposed into dstT[c][r] (pitch PT). Thread tid takes rows 4 (tid / 16) .. +3 and columns
+// transposed into dstT[c][...] (pitch PT; row r of the block at 4 ((r / 4) ^ (c / 8)) + r % 4). Thread tid takes rows 4 (tid / 16) .. +3 and columns
 // 8 (tid % 16) .. +7: fetch_block issues its four 16-byte loads (rows >= nvalid read as zero),
 // store_block writes them with four 16-byte stores and, for each of its eight columns, one
 // 8-byte store of the four rows.
@@ -86,12 +86,15 @@ __device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, bf
 #pragma unroll
     for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
   if (!dstT) return;
+  // groups of four rows are placed at group ^ (c / 8) within a transposed row c (see tfrag),
+  // which spreads the sixteen columns a 16-lane group writes over distinct banks
+  const int unit = (r0 >> 2) ^ (c0 >> 3);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int wi = e >> 1, sh = (e & 1) * 16;
     const uint32_t x0 = (v[0][wi] >> sh) & 0xFFFFu, x1 = (v[1][wi] >> sh) & 0xFFFFu;
     const uint32_t x2 = (v[2][wi] >> sh) & 0xFFFFu, x3 = (v[3][wi] >> sh) & 0xFFFFu;
-    *reinterpret_cast<uint2*>(dstT + (c0 + e) * PT + r0) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
+    *reinterpret_cast<uint2*>(dstT + (c0 + e) * PT + 4 * unit) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
   }
 }
 
@@ -107,13 +110,13 @@ __device__ __forceinline__ void split_frag(const float (&x)[8], bf16x8& hi, bf16
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
-// B operand over 32 queries of chunk u from a transposed tile T[c][q] (pitch PT): lane (l16, q4)
-// takes column c = c0 + l16 at queries 32 u + 4 q4 .. +3 and 32 u + 16 + 4 q4 .. +3, the order in
-// which the P / dS fragments hold them.
+// B operand over 32 queries of chunk u from a transposed tile (pitch PT, store_block's layout):
+// lane (l16, q4) takes column c = c0 + l16 at queries 32 u + 4 q4 .. +3 and 32 u + 16 + 4 q4 ..
+// +3, the order in which the P / dS fragments hold them.
 __device__ __forceinline__ bf16x8 tfrag(const bf16_t* T, int c, int u, int q4) {
-  const bf16_t* p = T + c * PT + 32 * u + 4 * q4;
-  const uint2 a = *reinterpret_cast<const uint2*>(p);
-  const uint2 b = *reinterpret_cast<const uint2*>(p + 16);
+  const int f = (c >> 3) & 15;  // the row-group swizzle of store_block
+  const uint2 a = *reinterpret_cast<const uint2*>(T + c * PT + 4 * ((8 * u + q4) ^ f));
+  const uint2 b = *reinterpret_cast<const uint2*>(T + c * PT + 4 * ((8 * u + 4 + q4) ^ f));
   return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
 }
 
@@ -267,12 +270,15 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
   for (int j = 0; j < 8; ++j) dk[j] = f32x4{0, 0, 0, 0}, dv[j] = f32x4{0, 0, 0, 0};
   const float sl = a.scale * kLog2e;
   const int nqb = (E.L + BLK - 1) / BLK;
-  // (query head, query block) steps: query heads of the group outer, the causal blocks from kb
-  const int per_head = nqb - kb, steps = g * per_head;
+  // (query block, query head) steps: query blocks from the last down to kb, the group's query
+  // heads inside. Every workgroup of a key/value head walks the same blocks in the same order
+  // (starting at the last, stopping at its own key block), so those running together on an XCD
+  // read each Q and dO block from its L2.
+  const int steps = g * (nqb - kb);
   u32x4 fq[4], fo[4];
   float fl = INFINITY, fd = 0.0f;
   auto fetch = [&](int i) {
-    const int h = kh * g + i / per_head, q0 = (kb + i % per_head) * BLK, nq = min(BLK, E.L - q0);
+    const int h = kh * g + i % g, q0 = (nqb - 1 - i / g) * BLK, nq = min(BLK, E.L - q0);
     fetch_block(fq, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
     fetch_block(fo, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, nq, tid);
     if (tid < BLK) {
@@ -283,7 +289,7 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
   };
   fetch(0);
   for (int i = 0; i < steps; ++i) {
-    const int q0 = (kb + i % per_head) * BLK;
+    const int q0 = (nqb - 1 - i / g) * BLK;
     __syncthreads();  // the previous step's reads of the tiles are done
     store_block(fq, Qs, Qt, tid);
     store_block(fo, dOs, dOt, tid);
