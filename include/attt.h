@@ -406,7 +406,7 @@ attt_status attt_lora_forward(const attt_lora_fwd_problem* problems, int32_t cou
  * Adapter hot swap into serving (Appendix A: the adapter trained by an update replaces the
  * episode's serving adapter): every float32 tensor of an adapter (the masters that
  * attt_lora_sgd_step updates) rounded to nearest even into the bf16 copy that
- * attt_lora_forward reads, in one launch per 16 tensors. Bit-exact.
+ * attt_lora_forward reads, in one launch per 96 tensors. Bit-exact.
  *
  * items  HOST array of `count` descriptors:
  *   src  device float [n]

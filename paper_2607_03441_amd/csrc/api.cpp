@@ -10,6 +10,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "attt.h"
@@ -1081,12 +1082,13 @@ LoraPlan lora_plan(const attt_lora_problem* p, int32_t count, int32_t dtype) {
   return P;
 }
 
-// Launches `jobs` in batches of kLoraJobBatch; blocks(job) gives each job's workgroup count.
-template <class Job, class Blocks, class Launch>
+// Launches `jobs` in batches of Batch::kCap; blocks(job) gives each job's workgroup count.
+template <class Batch = void, class Job, class Blocks, class Launch>
 attt_status lora_launch_all(const std::vector<Job>& jobs, Blocks blocks, Launch launch, const char* name) {
-  for (size_t j0 = 0; j0 < jobs.size(); j0 += kLoraJobBatch) {
-    LoraBatchOf<Job> b{};
-    b.count = (int32_t)std::min<size_t>(kLoraJobBatch, jobs.size() - j0);
+  using B = std::conditional_t<std::is_void_v<Batch>, LoraBatchOf<Job>, Batch>;
+  for (size_t j0 = 0; j0 < jobs.size(); j0 += B::kCap) {
+    B b{};
+    b.count = (int32_t)std::min<size_t>(B::kCap, jobs.size() - j0);
     int total = 0;
     for (int i = 0; i < b.count; ++i) {
       b.j[i] = jobs[j0 + i];
@@ -1298,17 +1300,21 @@ extern "C" attt_status attt_lora_forward(const attt_lora_fwd_problem* problems, 
     }
     if (!placed) groups.push_back({i});
   }
-  std::vector<LoraFwdJob> jobs;
+  // Jobs of at most 16 rows (decoding) run on 8-wave workgroups that split d_in eight ways;
+  // larger jobs on 4-wave workgroups of 64 rows.
+  std::vector<LoraFwdJob> jobs[2];  // [0] 4-wave, [1] 8-wave
   int64_t row_blocks = 0;
-  int64_t max_dout = 8;
+  int64_t max_dout = 8, max_dout_small = 8;
   for (const auto& gr : groups) {
     const attt_lora_fwd_problem& f = problems[gr[0]];
+    const bool small = f.rows <= 16;
     LoraFwdJob J{};
     J.x = f.x;
     J.rows = (int32_t)f.rows;
     J.d_in = (int32_t)f.d_in;
-    J.rb = f.rows <= 16 ? 16 : 64;
-    J.kw = f.rows <= 16 ? 4 : 1;
+    J.rb = small ? 16 : 64;
+    J.kw = small ? 8 : 1;
+    J.ncs = 1;
     for (int i : gr) {
       const attt_lora_fwd_problem& q = problems[i];
       LoraFwdOut& O = J.o[J.no++];
@@ -1323,32 +1329,39 @@ extern "C" attt_status attt_lora_forward(const attt_lora_fwd_problem* problems, 
         U.valid = std::min(16, q.rank - 16 * t);
         U.scale = q.scale;
       }
-      max_dout = std::max<int64_t>(max_dout, q.d_out);
+      (small ? max_dout_small : max_dout) = std::max<int64_t>(small ? max_dout_small : max_dout, q.d_out);
     }
-    row_blocks += ceil_div(f.rows, J.rb);
-    jobs.push_back(J);
+    if (!small) row_blocks += ceil_div(f.rows, J.rb);
+    jobs[small ? 1 : 0].push_back(J);
   }
-  // Few row blocks (decoding): split each block's columns over several workgroups, each
-  // recomputing x A^T (x and A stay in the XCD's L2), so that the launch still fills the chip.
+  // Few row blocks: split each block's columns over several workgroups, each recomputing x A^T
+  // (x and A stay in the XCD's L2, the splits of a block running on one XCD), so that the
+  // launch still fills the chip.
   int ncs = 1;
   if (row_blocks > 0 && row_blocks < 512)
     ncs = (int)std::min<int64_t>({16, ceil_div(1024, row_blocks), ceil_div(max_dout, 64)});
   ncs = std::max(ncs, 1);
-  std::stable_sort(jobs.begin(), jobs.end(), [](const LoraFwdJob& a, const LoraFwdJob& b) { return a.nu > b.nu; });
+  for (auto& J : jobs[0]) J.ncs = ncs;
+  // decoding: every job's columns over up to 16 workgroups of at least 256 columns each
+  const int ncs_small = (int)std::max<int64_t>(1, std::min<int64_t>(16, ceil_div(max_dout_small, 256)));
+  for (auto& J : jobs[1]) J.ncs = ncs_small;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  for (size_t j0 = 0; j0 < jobs.size(); j0 += kLoraFwdBatch) {
-    LoraFwdBatch b{};
-    b.count = (int32_t)std::min<size_t>(kLoraFwdBatch, jobs.size() - j0);
-    int64_t total = 0;
-    for (int i = 0; i < b.count; ++i) {
-      b.j[i] = jobs[j0 + i];
-      b.j[i].ncs = ncs;
-      b.j[i].b_begin = (int32_t)total;
-      total += ceil_div(b.j[i].rows, b.j[i].rb) * ncs;
+  for (int kind = 0; kind < 2; ++kind) {
+    auto& js = jobs[kind];
+    std::stable_sort(js.begin(), js.end(), [](const LoraFwdJob& a, const LoraFwdJob& b) { return a.nu > b.nu; });
+    for (size_t j0 = 0; j0 < js.size(); j0 += kLoraFwdBatch) {
+      LoraFwdBatch b{};
+      b.count = (int32_t)std::min<size_t>(kLoraFwdBatch, js.size() - j0);
+      int64_t total = 0;
+      for (int i = 0; i < b.count; ++i) {
+        b.j[i] = js[j0 + i];
+        b.j[i].b_begin = (int32_t)total;
+        total += ceil_div(b.j[i].rows, b.j[i].rb) * b.j[i].ncs;
+      }
+      if (total >= ((int64_t)1 << 31) - 8) return fail(ATTT_EUNSUPPORTED, "lora_forward: too many row blocks");
+      b.total = (int32_t)total;
+      HIP_TRY(launch_lora_fwd(b.j[0].nu, kind ? 8 : 4, b, s), "lora_fwd");
     }
-    if (total >= ((int64_t)1 << 31) - 8) return fail(ATTT_EUNSUPPORTED, "lora_forward: too many row blocks");
-    b.total = (int32_t)total;
-    HIP_TRY(launch_lora_fwd(b.j[0].nu, b, s), "lora_fwd");
   }
   return ATTT_OK;
 }
@@ -1373,7 +1386,7 @@ extern "C" attt_status attt_lora_hot_swap(const attt_lora_swap_item* items, int3
     jobs.push_back(J);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return lora_launch_all(
+  return lora_launch_all<LoraSwapBatch>(
       jobs, [](const LoraSwapJob& J) { return (int)ceil_div(J.n, (int64_t)kLoraSwapPerBlock); },
       [&](const LoraSwapBatch& b, int n) { return launch_lora_swap(b, n, s); }, "lora_swap");
 }

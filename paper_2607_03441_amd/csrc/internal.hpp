@@ -334,11 +334,12 @@ struct LoraBTJob {
   int32_t b_begin;
 };
 
-template <class J>
+template <class J, int Cap = kLoraJobBatch>
 struct LoraBatchOf {
+  static constexpr int kCap = Cap;
   int32_t count;
   int32_t pad;
-  J j[kLoraJobBatch];
+  J j[Cap];
 };
 using LoraP1Batch = LoraBatchOf<LoraP1Job>;
 using LoraP2Batch = LoraBatchOf<LoraP2Job>;
@@ -385,8 +386,8 @@ struct LoraFwdJob {
   const void* x;
   int32_t rows, d_in;
   int32_t nu, no;   // units, projections
-  int32_t rb;       // rows per workgroup: 64 (one wave per 16 rows) or 16 (four waves split d_in)
-  int32_t kw;       // waves splitting d_in: 1 or 4
+  int32_t rb;       // rows per workgroup: 64 (one wave per 16 rows) or 16 (the waves split d_in)
+  int32_t kw;       // waves splitting d_in: 1, 4, or 8 (8-wave workgroups)
   int32_t ncs;      // column splits of the outputs (workgroups per row block)
   int32_t b_begin;  // first logical workgroup
   LoraFwdUnit u[kLoraMaxTiles];
@@ -399,8 +400,9 @@ struct LoraFwdBatch {
   LoraFwdJob j[kLoraFwdBatch];
 };
 static_assert(sizeof(LoraFwdBatch) <= 3840, "kernel arguments");
-// nu: the largest unit count of the batch's jobs
-hipError_t launch_lora_fwd(int nu, const LoraFwdBatch& b, hipStream_t s);
+// nu: the largest unit count of the batch's jobs; waves: 4, or 8 for jobs of at most 16 rows
+// (kw = 8)
+hipError_t launch_lora_fwd(int nu, int waves, const LoraFwdBatch& b, hipStream_t s);
 
 // Swap: dst (bf16) = RN(src (float32)) for every tensor of the batch.
 struct LoraSwapJob {
@@ -410,7 +412,8 @@ struct LoraSwapJob {
   int32_t b_begin;
   int32_t vec;      // src and dst 16-byte aligned
 };
-using LoraSwapBatch = LoraBatchOf<LoraSwapJob>;
+using LoraSwapBatch = LoraBatchOf<LoraSwapJob, 96>;  // 3 KiB of kernel arguments
+static_assert(sizeof(LoraSwapBatch) <= 3840, "kernel arguments");
 constexpr int kLoraSwapPerBlock = 2048;  // elements per workgroup (256 threads x 8)
 hipError_t launch_lora_swap(const LoraSwapBatch& b, int blocks, hipStream_t s);
 

@@ -7,9 +7,9 @@
 // projection), in one launch for all of them. A job is one x (an episode's rows) with up to
 // four projections reading it (q, k, v of a layer): x is read once for all their ranks.
 //   Phase 1: U = x A^T on v_mfma_f32_16x16x32_bf16, 16 rows per wave over the contraction
-//     (64 rows per workgroup), or, for at most 16 rows (decoding), all four waves on the same
-//     16 rows with a quarter of d_in each, summed in LDS in a fixed order. x rows and adapter
-//     rows are 16-byte loads in the MFMA's own k order, the next 128-wide step in flight.
+//     (64 rows per 4-wave workgroup), or, for at most 16 rows (decoding), an 8-wave workgroup
+//     whose waves take an eighth of d_in each, their partial U summed in LDS in a fixed order. x rows and adapter rows are 16-byte loads in the MFMA's own k order, the next
+//     128-wide step in flight.
 //     scale U (float32) stays in LDS: nothing goes through HBM between the phases.
 //   Phase 2: per projection, 256-column chunks of B [d_out, rank] staged transposed in LDS;
 //     each thread adds the rank-long dot products for 8 consecutive columns of up to 8 rows
@@ -29,9 +29,10 @@ constexpr uint32_t kOOBF = 0x7FFFFFF0u;  // offset past every descriptor's range
 constexpr int kUP = 65;                  // LDS pitch (floats) of a row of U
 constexpr int kBC = 256;                 // output columns per phase-2 chunk
 constexpr int kBP = kBC + 8;             // LDS pitch (bf16) of a rank row of the transposed B chunk
-constexpr int kUpBytes = 4 * 16 * kUP * 4;
 constexpr int kBtBytes = 64 * kBP * 2;
-constexpr int kScratchBytes = kUpBytes > kBtBytes ? kUpBytes : kBtBytes;
+// LDS scratch of a W-wave workgroup: the waves' partial U [W][16][kUP] floats, later the B chunk
+template <int W>
+constexpr int scratch_bytes() { return W * 16 * kUP * 4 > kBtBytes ? W * 16 * kUP * 4 : kBtBytes; }
 
 template <class Batch>
 __device__ __forceinline__ int job_of(const Batch& b, int li) {
@@ -44,8 +45,11 @@ __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w <<
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 }  // namespace
 
-template <int NU>
-__global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid) {
+// W waves: 4 (up to 64 rows per workgroup, 16 per wave, or 16 rows with d_in split four ways)
+// or 8 (decoding: 16 rows, d_in split eight ways, twice the loads in flight per workgroup).
+template <int NU, int W>
+__global__ __launch_bounds__(64 * W) void lora_fwd_kernel(LoraFwdBatch b, int grid) {
+  constexpr int NT = 64 * W;
   // hardware places workgroup i on XCD i % 8: give each XCD a contiguous range of logical ids
   const int per = grid >> 3;
   const int li = (int)(blockIdx.x & 7u) * per + (int)(blockIdx.x >> 3);
@@ -59,14 +63,14 @@ __global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid)
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, g = lane >> 4;
   __shared__ __align__(16) float Uf[64 * kUP];
-  __shared__ __align__(16) uint8_t scr[kScratchBytes];
+  __shared__ __align__(16) uint8_t scr[scratch_bytes<W>()];
   float* Up = reinterpret_cast<float*>(scr);    // phase 1: [wave][16][kUP] partial U
   bf16_t* Bt = reinterpret_cast<bf16_t*>(scr);  // phase 2: [rank][kBP] transposed B chunk
 
   // ---- phase 1 ------------------------------------------------------------------------
   const int d_in = J.d_in, nu = J.nu;
-  const int rg = J.kw == 4 ? 0 : w;  // this wave's 16 rows
-  const int kp = J.kw == 4 ? w : 0;  // this wave's share of d_in
+  const int rg = J.kw > 1 ? 0 : w;  // this wave's 16 rows
+  const int kp = J.kw > 1 ? w : 0;  // this wave's share of d_in
   const int r0w = row0 + 16 * rg;
   const int nrows = max(0, min(16, J.rows - r0w));
   const bf16_t* xs = static_cast<const bf16_t*>(J.x) + (int64_t)min(r0w, J.rows) * d_in;
@@ -123,25 +127,22 @@ __global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid)
     for (int v = 0; v < 4; ++v) Up[(w * 16 + 4 * g + v) * kUP + 16 * t + l16] = acc[t][v];
   }
   __syncthreads();
-  for (int i = tid; i < J.rb * 64; i += 256) {
+  for (int i = tid; i < J.rb * 64; i += NT) {
     const int row = i >> 6, c = i & 63, t = c >> 4;
     if (t >= nu) continue;
     float sc = J.u[0].scale;
 #pragma unroll
     for (int k = 1; k < NU; ++k)
       if (t == k) sc = J.u[k].scale;
-    float v;
-    if (J.kw == 4)
-      v = ((Up[row * kUP + c] + Up[(16 + row) * kUP + c]) + Up[(32 + row) * kUP + c]) + Up[(48 + row) * kUP + c];
-    else
-      v = Up[row * kUP + c];  // wave row/16 wrote row row%16 of its block at the same place
+    float v = Up[row * kUP + c];  // kw == 1: wave row/16 wrote row row%16 of its block here
+    for (int k = 1; k < J.kw; ++k) v += Up[(16 * k + row) * kUP + c];  // kw > 1: fixed order
     Uf[row * kUP + c] = sc * v;
   }
   __syncthreads();  // Up is dead from here on; its space holds the B chunks
 
   // ---- phase 2 ------------------------------------------------------------------------
-  const int og = tid & 31, rs = tid >> 5;  // 8 columns og*8 .. +7 of rows rs, rs + 8, ...
-  const int nri = J.rb >> 3;
+  const int og = tid & 31, rs = tid >> 5;  // 8 columns og*8 .. +7 of rows rs, rs + 2W, ...
+  const int nri = (J.rb + 2 * W - 1) / (2 * W);
 #pragma unroll 1
   for (int p = 0; p < kLoraMaxTiles; ++p) {
     if (p >= J.no) break;
@@ -156,7 +157,7 @@ __global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid)
       // B[oc .. oc + nvo)[0 .. rank) is contiguous: 16-byte loads, scattered into Bt[c][o]
       const int nel = nvo * rank;
       const bf16_t* src = B + (int64_t)oc * rank;
-      for (int i8 = tid * 8; i8 < nel; i8 += 256 * 8) {
+      for (int i8 = tid * 8; i8 < nel; i8 += NT * 8) {
         const u32x4 v = *reinterpret_cast<const u32x4*>(src + i8);
         int o = i8 / rank, c = i8 - o * rank;
 #pragma unroll
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid)
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
             if (i >= nri) break;
-            const float u = Uf[(rs + 8 * i) * kUP + u0 + c];
+            const float u = Uf[min(rs + 2 * W * i, 63) * kUP + u0 + c];
 #pragma unroll
             for (int e = 0; e < 8; ++e) a[i][e] = fmaf(u, bv[e], a[i][e]);
           }
@@ -189,8 +190,9 @@ __global__ __launch_bounds__(256) void lora_fwd_kernel(LoraFwdBatch b, int grid)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           if (i >= nri) break;
-          const int row = row0 + rs + 8 * i;
-          if (row >= J.rows) continue;
+          const int rl = rs + 2 * W * i;
+          const int row = row0 + rl;
+          if (rl >= J.rb || row >= J.rows) continue;
           u32x4* yp = reinterpret_cast<u32x4*>(y + (int64_t)row * d_out + oc + ocol);
           const u32x4 yv = *yp;
           u32x4 out;
@@ -224,16 +226,24 @@ __global__ __launch_bounds__(256) void lora_swap_kernel(LoraSwapBatch b) {
   }
 }
 
-hipError_t launch_lora_fwd(int nu, const LoraFwdBatch& b, hipStream_t s) {
+template <int W>
+static void launch_fwd_w(int nu, const LoraFwdBatch& b, int grid, hipStream_t s) {
+  switch (nu) {
+    case 1: hipLaunchKernelGGL((lora_fwd_kernel<1, W>), dim3(grid), dim3(64 * W), 0, s, b, grid); break;
+    case 2: hipLaunchKernelGGL((lora_fwd_kernel<2, W>), dim3(grid), dim3(64 * W), 0, s, b, grid); break;
+    case 3: hipLaunchKernelGGL((lora_fwd_kernel<3, W>), dim3(grid), dim3(64 * W), 0, s, b, grid); break;
+    default: hipLaunchKernelGGL((lora_fwd_kernel<4, W>), dim3(grid), dim3(64 * W), 0, s, b, grid); break;
+  }
+}
+
+hipError_t launch_lora_fwd(int nu, int waves, const LoraFwdBatch& b, hipStream_t s) {
   if (b.total <= 0) return hipSuccess;
   const int grid = (b.total + 7) & ~7;
   KernelTimer t(K_LORA_FWD, s);
-  switch (nu) {
-    case 1: hipLaunchKernelGGL(lora_fwd_kernel<1>, dim3(grid), dim3(256), 0, s, b, grid); break;
-    case 2: hipLaunchKernelGGL(lora_fwd_kernel<2>, dim3(grid), dim3(256), 0, s, b, grid); break;
-    case 3: hipLaunchKernelGGL(lora_fwd_kernel<3>, dim3(grid), dim3(256), 0, s, b, grid); break;
-    default: hipLaunchKernelGGL(lora_fwd_kernel<4>, dim3(grid), dim3(256), 0, s, b, grid); break;
-  }
+  if (waves == 8)
+    launch_fwd_w<8>(nu, b, grid, s);
+  else
+    launch_fwd_w<4>(nu, b, grid, s);
   return hipGetLastError();
 }
 
