@@ -169,6 +169,16 @@ __global__ __launch_bounds__(64 * W) void lora_fwd_kernel(LoraFwdBatch b, int gr
       __syncthreads();
       const int ocol = og * 8;
       if (ocol < nvo) {
+        // this thread's rows of y, loaded before the rank loop so that their latency overlaps it
+        u32x4 yv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (i >= nri) break;
+          const int rl = rs + 2 * W * i, row = row0 + rl;
+          yv[i] = u32x4{0u, 0u, 0u, 0u};
+          if (rl < J.rb && row < J.rows)
+            yv[i] = *reinterpret_cast<const u32x4*>(y + (int64_t)row * d_out + oc + ocol);
+        }
         float a[8][8];
 #pragma unroll
         for (int i = 0; i < 8; ++i)
@@ -193,13 +203,11 @@ __global__ __launch_bounds__(64 * W) void lora_fwd_kernel(LoraFwdBatch b, int gr
           const int rl = rs + 2 * W * i;
           const int row = row0 + rl;
           if (rl >= J.rb || row >= J.rows) continue;
-          u32x4* yp = reinterpret_cast<u32x4*>(y + (int64_t)row * d_out + oc + ocol);
-          const u32x4 yv = *yp;
           u32x4 out;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            out[e] = pack_bf16x2(bf_lo(yv[e]) + a[i][2 * e], bf_hi(yv[e]) + a[i][2 * e + 1]);
-          *yp = out;
+            out[e] = pack_bf16x2(bf_lo(yv[i][e]) + a[i][2 * e], bf_hi(yv[i][e]) + a[i][2 * e + 1]);
+          *reinterpret_cast<u32x4*>(y + (int64_t)row * d_out + oc + ocol) = out;
         }
       }
       __syncthreads();  // Bt is rewritten by the next chunk
