@@ -43,10 +43,9 @@
 namespace attt {
 
 constexpr int kSlotBytes = 256 * 256 * 2;  // one bf16 tile [256 tokens][256 vocab]
-// Dynamic LDS: the mainloops' two stage buffers, the producer's per-token sums [2][256], then
-// four ints of workgroup state.
-// There is no static LDS, so the stage buffers start at LDS address 0 and every LDS-DMA
-// destination is 1 KiB-aligned.
+// Dynamic LDS: the mainloops' two stage buffers and group counter (CfgBig::LDS), the producer's
+// per-token sums [2][256], then four ints of workgroup state. There is no static LDS, so the
+// stage buffers start at LDS address 0.
 constexpr size_t kFusedLdsData = CfgBig::LDS + 2 * 256 * sizeof(float);
 constexpr size_t kFusedLds = kFusedLdsData + 4 * sizeof(int);
 
@@ -113,11 +112,12 @@ __device__ __forceinline__ bool exact_fold(float z_y, float lse) { return z_y - 
 
 // The consumer's GEMM: acc += A[0:256, 0:K] T^T with T the ring tiles of items gbase ..
 // gbase + nitems - 1 laid end to end along K (each [256 tokens][256 vocab]); A = W^T rows of the
-// d-slice. The same 8-wave ping-pong as mfma_mainloop_pp; only group 1 (waves 4-7) loads ring
-// blocks inside the loop (group 0's share of a stage is A blocks), so group 1 waits for an item's
-// ready flag before issuing its first stage (ensure: flags read 16 items at a time), and signals
-// `consumed` once its loads of the item's last stage have landed. The prologue (group 0 issues
-// all of stage 0) waits for item gbase in every wave.
+// d-slice. The same 8-wave ping-pong as mfma_mainloop_pp16, with the same group counter before
+// group 1's refills; only group 1 (waves 4-7) loads ring blocks inside the loop (group 0's share
+// of a stage is A blocks), so group 1 waits for an item's ready flag before issuing its first
+// stage (ensure: flags read 16 items at a time), and signals `consumed` once its loads of the
+// item's last stage have landed. The prologue (group 0 issues all of stage 0) waits for item
+// gbase in every wave.
 template <class C>
 __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
                                                   const uint8_t* ring, int nval, int nitems, int gbase, int S,
@@ -138,8 +138,12 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
   constexpr int LW = 4;
   constexpr int ABLK = C::BM / 8;
   constexpr int BPW = (ABLK + C::BN / 8) / LW;
-  constexpr int kG0 = 6;
-  static_assert(kG0 * LW <= ABLK, "group 0's share of a stage holds A blocks only");
+  // Group 0 loads blocks [kCs, kCs + 6) of each stage, A rows only (the ring rows are loaded by
+  // group 1, which waits for their flags); group 1 loads [0, kCs), A rows of group 0's half
+  // that no wave of group 1 reads, then the ring rows [JA, BPW) once all four of its waves have
+  // read the stage (see PpLoader in gemm_core.hpp).
+  constexpr int kCs = 2;
+  static_assert(kCs + 6 == ABLK / LW && kCs * LW * 8 <= C::WTM, "group 0's share holds A blocks only");
   const int lr = lane >> 3;
   const int c_even = (lane & 7) ^ ((lr >> 1) & 7);
   const int c_odd = (lane & 7) ^ (((8 + lr) >> 1) & 7);
@@ -216,14 +220,20 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
     }
     known = i + 1;  // aborted: go on with whatever the slot holds, the result is discarded
   };
+  const uint32_t ctr = group1_counter<C>(lds);
+  group1_reset(ctr, tid);
   ensure(0);
   if (grp == 0) dma(0, 0, 0, BPW);
   __builtin_amdgcn_s_waitcnt(0);
-  if (grp == 1 && nk > 1) dma(1, 1, kG0, BPW);
+  if (grp == 1 && nk > 1) {
+    dma(1, 1, 0, kCs);
+    dma(1, 1, JA, BPW);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the counter reset has landed
   wg_barrier();
   if (grp == 0) {
     for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) dma((k + 1) & 1, k + 1, 0, kG0);
+      if (k + 1 < nk) dma((k + 1) & 1, k + 1, kCs, JA);
       mem(k);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
@@ -243,7 +253,11 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
       if ((k & 3) == 2 && __builtin_amdgcn_mbcnt_lo(~0u, 0u) == 0) add_agent(consumed + slot_of(k >> 2), 1);
       if (k + 2 < nk) {
         if (((k + 2) & 3) == 0) ensure((k + 2) >> 2);
-        dma(k & 1, k + 2, kG0, BPW);
+        group1_arrive(ctr, lane);
+        dma(k & 1, k + 2, 0, kCs);
+        // the other waves of group 1 read the ring rows this refill overwrites
+        group1_wait(ctr, k);
+        dma(k & 1, k + 2, JA, BPW);
       }
       wg_barrier();
       pin();

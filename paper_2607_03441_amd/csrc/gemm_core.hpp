@@ -44,7 +44,9 @@ struct Cfg {
   static constexpr int RPL = NT / 8;  // rows one load round covers (8 x 16-byte chunks per row)
   static constexpr int AL = BM / RPL, BL = BN / RPL;
   static constexpr int SA = BM * BK, SB = BN * BK;
-  static constexpr size_t LDS = (size_t)2 * (SA + SB) * sizeof(bf16_t);  // two stages
+  static constexpr size_t LDS_STAGES = (size_t)2 * (SA + SB) * sizeof(bf16_t);  // two stages
+  // + the ping-pong mainloops' group counter (256 bytes, so what a kernel puts after it stays aligned)
+  static constexpr size_t LDS = LDS_STAGES + 256;
 };
 using CfgBig = Cfg<256, 256, 2, 4>;    // 8 waves, 128x64 per wave
 using CfgSmall = Cfg<128, 128, 2, 2>;  // 4 waves, 64x64 per wave
@@ -158,15 +160,49 @@ __device__ __forceinline__ void mfma_mainloop_db(const bf16_t* __restrict__ A, i
 // phase) while the other runs its 32 MFMAs (compute phase).
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+// The group counter of the ping-pong mainloops: an int in LDS after the two stage buffers.
+// group1_reset() zeroes it before a mainloop's first barrier (thread 0; the caller's wait for
+// its LDS operations follows). Every wave of group 1 calls group1_arrive() once its fragment
+// reads of stage k have completed (lgkmcnt(0)), and group1_wait(k) before it refills blocks the
+// other waves of its group read: it returns once all four have arrived for stage k. All four
+// run the same loop iterations, so the wait always ends. Both use inline LDS instructions: the
+// compiler would otherwise wait for the wave's outstanding LDS-DMA loads (vmcnt) before them,
+// since it cannot tell that the counter is not among their destinations.
+template <class C>
+__device__ __forceinline__ uint32_t group1_counter(bf16_t* lds) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)(reinterpret_cast<uint8_t*>(lds) +
+                                                                        C::LDS_STAGES);
+}
+__device__ __forceinline__ void group1_reset(uint32_t ctr, int tid) {
+  if (tid == 0) asm volatile("ds_write_b32 %0, %1" ::"v"(ctr), "v"(0) : "memory");
+}
+__device__ __forceinline__ void group1_arrive(uint32_t ctr, int lane) {
+  if (lane == 0) asm volatile("ds_add_u32 %0, %1" ::"v"(ctr), "v"(1) : "memory");
+}
+__device__ __forceinline__ void group1_wait(uint32_t ctr, int k) {
+  const int target = 4 * (k + 1);
+  int v;
+  do {
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(ctr) : "memory");
+  } while (__builtin_amdgcn_readfirstlane(v) < target);
+}
+
 // Tile loads are issued only in memory phases: a wave stalls at a load instruction until the
 // load path accepts it (about 1 KiB per 25 cycles per CU here), and a stall in a compute phase
-// idles the SIMD's matrix core. A stage is 64 instructions of 1 KiB; both groups share them:
-//  * group 0 issues blocks [0, kG0) of stage k+1 at the start of its memory phase of stage k
-//    (slot (k+1)&1 was last read by group 1 in the phase before) and waits for them at the end
-//    of its compute phase of stage k;
-//  * group 1 issues blocks [kG0, 16) of stage k+2 at the end of its memory phase of stage k,
-//    after its own fragment reads of slot k&1 have completed (group 0 finished reading that
-//    slot before the barrier that opened the phase), and waits for them one memory phase later.
+// idles the SIMD's matrix core. A stage is 64 instructions of 1 KiB, 16 per wave of a group
+// (j in [0, 16), see PpLoader); both groups share them:
+//  * group 0 issues blocks [kSafe, kG1) of stage k+1 at the start of its memory phase of stage
+//    k (slot (k+1)&1 was last read by group 1 in the phase before) and waits for them at the
+//    end of its compute phase of stage k;
+//  * group 1 issues the rest of stage k+2 into slot k&1 at the end of its memory phase of
+//    stage k, after its own fragment reads of stage k have completed (group 0 finished reading
+//    that slot before the barrier that opened the phase), and waits for them one memory phase
+//    later: first blocks [0, kSafe), the A rows of group 0's half that no wave of group 1
+//    reads, then, once all four waves of group 1 have read stage k (group1_wait), blocks
+//    [kG1, 16). The four waves of group 1 read the same A rows and, pairwise with group 0, the
+//    same B rows, so a wave that refilled those after its own reads only could overwrite them
+//    before a slower wave of its group had read them (its fragments then came from stage k+2).
+//    Issuing the safe blocks first keeps the wait behind load issue that is needed anyway.
 // Group 1's share thus has three phases to land instead of one, and neither group's memory
 // phase carries a whole stage of load issue.
 // `tid` is the thread's index in the workgroup (a caller inside a loop may pass it through an
@@ -176,17 +212,17 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // (wave & 3) + 4 j for j in [0, 16). Blocks j < 8 are A rows, the rest B rows; both groups use the
 // same numbering. Offsets are formed per load: the block's first row is wave-uniform, and the
 // swizzled chunk of a lane depends only on the lane and on the parity of the block.
-// The stage buffers must start at an LDS address that is a multiple of 1 KiB, so a kernel using
-// these mainloops declares no static LDS (which the compiler places before the dynamic area):
-// with the buffers 16 bytes past such a boundary, 16-byte LDS-DMA loads occasionally left the
-// data of the lanes in the upper half of each 128-byte group of a block unwritten or wrong.
+// The stage buffers start at the kernel's LDS address 0 (the kernels declare no static LDS) and
+// are followed by the group counter at byte LDS_STAGES.
 template <class C>
 struct PpLoader {
   static constexpr int LW = 4;                        // waves per group
   static constexpr int ABLK = C::BM / 8, BBLK = C::BN / 8;
   static constexpr int BPW = (ABLK + BBLK) / LW;      // blocks per wave of a group per stage
-  static constexpr int kG0 = 6;                       // group 0's share per wave
-  static_assert(ABLK % LW == 0 && BBLK % LW == 0 && kG0 < BPW, "stage blocks must split evenly");
+  static constexpr int kSafe = C::WTM / 8 / LW;       // j < kSafe: A rows of group 0's half only
+  static constexpr int kG1 = kSafe + 6;               // group 0's share: j in [kSafe, kG1)
+  static_assert(ABLK % LW == 0 && BBLK % LW == 0 && kG1 < BPW, "stage blocks must split evenly");
+  static_assert(C::WGM == 2 && C::WGN == LW, "waves 0-3 cover A rows [0, WTM), waves 4-7 the rest");
   __amdgpu_buffer_rsrc_t rA, rB;
   int64_t lda, ldb;
   int mval, nval, K, wave, lr, c_even, c_odd;
@@ -219,12 +255,17 @@ struct PpLoader {
                                                16, ok ? off : kOOB, 0, 0, 0);
     }
   }
+  // group 1's share of a stage: blocks [0, kSafe) and [kG1, BPW)
+  __device__ __forceinline__ void issue_group1(bf16_t* lds, int st, int k0) const {
+    issue(lds, st, k0, 0, kSafe);
+    issue(lds, st, k0, kG1, BPW);
+  }
   // the loads that precede the loop: group 0 all of stage 0, group 1 its share of stage 1
   __device__ __forceinline__ void prologue(bf16_t* lds, bool wait_between) const {
     const int grp = wave >> 2;
     if (grp == 0) issue(lds, 0, 0, 0, BPW);
     if (wait_between) __builtin_amdgcn_s_waitcnt(0);
-    if (grp == 1 && K > 64) issue(lds, 1, 64, kG0, BPW);
+    if (grp == 1 && K > 64) issue_group1(lds, 1, 64);
   }
 };
 
@@ -257,7 +298,7 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const PpLoader<C> ld(A, lda, mval, B, ldb, nval, K, tid);
-  constexpr int BPW = PpLoader<C>::BPW, kG0 = PpLoader<C>::kG0;
+  constexpr int BPW = PpLoader<C>::BPW, kSafe = PpLoader<C>::kSafe, kG1 = PpLoader<C>::kG1;
 
   const int l32 = lane & 31, hi = lane >> 5;
   const int swz = (l32 >> 1) & 7;
@@ -293,20 +334,23 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     asm volatile("" : "+v"(acc[0][0]), "+v"(acc[0][1]), "+v"(acc[1][0]), "+v"(acc[1][1]),
                  "+v"(acc[2][0]), "+v"(acc[2][1]), "+v"(acc[3][0]), "+v"(acc[3][1]));
   };
-  // Group 0, iteration k:  loads [0, kG0) of stage k+1; fragments(k); wait for own reads |
+  // Group 0, iteration k:  loads [kSafe, kG1) of stage k+1; fragments(k); wait for own reads |
   //                        MFMA(k); wait for own loads |
-  // group 1, one phase later: fragments(k); wait for own reads and loads; loads [kG0, 16) of
-  //                        stage k+2 | MFMA(k) |
+  // group 1, one phase later: fragments(k); wait for own reads and loads; loads [0, kSafe) of
+  //                        stage k+2; wait for the group's reads; loads [kG1, 16) | MFMA(k) |
   // Group 1 takes one extra barrier before its loop, group 0 one after it, so every wave
   // executes 2 nk + 2 barriers. Group 1's share of stage 1 is issued before the loop (with
   // `issued`, the caller has issued both prologue loads already, see mfma_pp_prologue).
   const int nk = (K + 63) / 64;
+  const uint32_t ctr = group1_counter<C>(lds);
+  group1_reset(ctr, tid);
   if (!issued) ld.prologue(lds, true);
   else if (grp == 0) __builtin_amdgcn_s_waitcnt(0);  // stage 0 has landed (group 1 waits in its loop)
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the counter reset has landed
   wg_barrier();
   if (grp == 0) {
     for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, 0, kG0);
+      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, kSafe, kG1);
       mem(k);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
@@ -322,7 +366,12 @@ __device__ __forceinline__ void mfma_mainloop_pp(const bf16_t* __restrict__ A, i
     for (int k = 0; k < nk; ++k) {
       mem(k);
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-      if (k + 2 < nk) ld.issue(lds, k & 1, (k + 2) * 64, kG0, BPW);
+      if (k + 2 < nk) {
+        group1_arrive(ctr, lane);
+        ld.issue(lds, k & 1, (k + 2) * 64, 0, kSafe);
+        group1_wait(ctr, k);
+        ld.issue(lds, k & 1, (k + 2) * 64, kG1, BPW);
+      }
       wg_barrier();
       pin();
       compute();
@@ -406,19 +455,22 @@ __device__ __forceinline__ void mfma_mainloop_pp16(const bf16_t* __restrict__ A,
 #pragma unroll
     for (int j = 0; j < Mma16::TN; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   const PpLoader<C> ld(A, lda, mval, B, ldb, nval, K, tid);
-  constexpr int BPW = PpLoader<C>::BPW, kG0 = PpLoader<C>::kG0;
+  constexpr int BPW = PpLoader<C>::BPW, kSafe = PpLoader<C>::kSafe, kG1 = PpLoader<C>::kG1;
   bf16x8 fa[2][Mma16::TM], fb[2][Mma16::TN];
   auto mem = [&](int k) {
     const bf16_t* As = lds + (k & 1) * (C::SA + C::SB);
     mma16_frags<C>(As, As + C::SA, lane, wm, wn, fa, fb);
   };
   const int nk = (K + 63) / 64;
+  const uint32_t ctr = group1_counter<C>(lds);
+  group1_reset(ctr, tid);
   if (!issued) ld.prologue(lds, true);
   else if (grp == 0) __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the counter reset has landed
   wg_barrier();
   if (grp == 0) {
     for (int k = 0; k < nk; ++k) {
-      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, 0, kG0);
+      if (k + 1 < nk) ld.issue(lds, (k + 1) & 1, (k + 1) * 64, kSafe, kG1);
       mem(k);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       wg_barrier();
@@ -434,7 +486,12 @@ __device__ __forceinline__ void mfma_mainloop_pp16(const bf16_t* __restrict__ A,
     for (int k = 0; k < nk; ++k) {
       mem(k);
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-      if (k + 2 < nk) ld.issue(lds, k & 1, (k + 2) * 64, kG0, BPW);
+      if (k + 2 < nk) {
+        group1_arrive(ctr, lane);
+        ld.issue(lds, k & 1, (k + 2) * 64, 0, kSafe);
+        group1_wait(ctr, k);
+        ld.issue(lds, k & 1, (k + 2) * 64, kG1, BPW);
+      }
       wg_barrier();
       mma16_pin(acc);
       mma16_step(fa, fb, acc);

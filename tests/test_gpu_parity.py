@@ -486,26 +486,39 @@ def test_ce_fused_both_passes_aborted_give_nan(attt):
 
 
 def test_ce_fused_exact_after_abort_is_deterministic(attt):
-    """Regression: the exact pass after an aborted label pass, 24 calls on one reused workspace,
-    gives the same bits every time and meets the bar each time (with the stage buffers 16 bytes
-    off a 1 KiB boundary, LDS-DMA loads left wrong data in parts of some tiles now and then)."""
+    """Regression: the exact pass after an aborted label pass, back to back with a call on other
+    data, inputs uploaded afresh each time (so they land in memory the other call just used),
+    160 times: every call gives the first call's bits, and that first result meets the bar.
+    Before the four waves of the mainloops' second group synchronised ahead of refilling the
+    stage slot they had just read, a fast wave's loads of stage k+2 could land in blocks a
+    slower wave of its group had not read yet; here that changed a few 8-token groups of the
+    gradient in 2-4% of calls."""
     import torch
     h, W, labels, weights, off = _ce_bf16_small_case(81)
     N, d = h.f32.shape
     V = W.f32.shape[0]
-    ws = torch.empty(attt.ce_workspace_size(N, d, V, attt.BF16) + 4096, dtype=torch.uint8, device="cuda")
-    args = (dev_dense(h), dev_dense(W), dev_i32(labels), dev_f32(weights))
+    other_h = [random_dense((N, d), 1.0, True, 2000 + i) for i in range(4)]
+    other_W = [random_dense((V, d), 0.05, True, 1000 + i) for i in range(4)]
+    tl, tw = dev_i32(labels), dev_f32(weights)
     lo, lseo, dHo = oce.weighted_ce(h.f32, W.f32, labels, weights, off)
-    note("ce fused: exact pass after abort, 24 calls")
+    note("ce fused: exact pass after abort, 160 calls, each after a call on other data")
     first = None
-    attt.ce_set_wait_limit(0, 20000)
+    bad = []
     try:
-        for rep in range(24):
-            loss, lse, dH = attt.weighted_ce_fwd_bwd(*args, row_offsets=off, workspace=ws)
+        for rep in range(160):
+            attt.weighted_ce_fwd_bwd(dev_dense(other_h[rep % 4]), dev_dense(other_W[rep % 4]), tl, tw,
+                                     row_offsets=off)
+            th, tW = dev_dense(h), dev_dense(W)
+            attt.ce_set_wait_limit(0, 20000)
+            loss, lse, dH = attt.weighted_ce_fwd_bwd(th, tW, tl, tw, row_offsets=off)
+            attt.ce_set_wait_limit()
             bits = dH.contiguous().view(torch.int16).cpu().numpy()
             if first is None:
                 first = bits
                 check_rows(host(dH), dHo, BF16_COS, BF16_ELEM, f"dH {dH.shape} call 0")
-            assert np.array_equal(bits, first), (rep, int((bits != first).sum()))
+            elif not np.array_equal(bits, first):
+                rows = np.unique(np.nonzero(bits != first)[0])
+                bad.append((rep, int((bits != first).sum()), rows[:16].tolist()))
     finally:
         attt.ce_set_wait_limit()
+    assert not bad, bad
