@@ -156,8 +156,10 @@ def algorithmic(cfg, tok, probs):
                 ngram_bytes=float(ngram_bytes), lora_bytes=float(lora_bytes), lora_flops=float(lora_flops))
 
 
-KERNEL_SYMBOL = {"ce_fwd_lse": "attt::ce_fwd_", "ce_bwd_dz": "attt::ce_dz_", "ce_bwd_dh": "attt::ce_dh_",
-                 "ce_fused_bwd": "attt::ce_fused_bwd_kernel<true>"}
+# the fused backward's label pass runs as ce_fused_bwd_kernel, or as its vocabulary-split form
+# when d has fewer than 16 slices of 256
+KERNEL_SYMBOL = {"ce_fwd_lse": ("attt::ce_fwd_",), "ce_bwd_dz": ("attt::ce_dz_",), "ce_bwd_dh": ("attt::ce_dh_",),
+                 "ce_fused_bwd": ("attt::ce_fused_bwd_kernel<true>", "attt::ce_fused_bwd_split_kernel<true>")}
 
 
 def counter_traffic(workload, kernel):
@@ -177,9 +179,9 @@ def counter_traffic(workload, kernel):
         with open(os.path.join(ROOT, src), "rb") as fh:
             if hashlib.sha256(fh.read()).hexdigest()[:16] != digest:
                 return None
-    prefix = KERNEL_SYMBOL.get(kernel)
+    prefixes = KERNEL_SYMBOL.get(kernel, ())
     for name, b in rec["bytes_per_dispatch"].items():
-        if prefix and name.removeprefix("void ").startswith(prefix):
+        if any(name.removeprefix("void ").startswith(pre) for pre in prefixes):
             return b
     return None
 

@@ -664,9 +664,9 @@ constexpr int64_t kCeVocabChunk = 131072;
 struct CePlan {
   CeGemmShape fwd{64, 64};
   int64_t n_vb = 0, nv = 0, R = 0, Vc = 0, Vp = 0;
-  int slices = 0, consumers = 0, passes = 0, slots = 0, items_max = 0, sync_ints = 0;
+  int slices = 0, consumers = 0, passes = 0, ksplit = 1, slots = 0, items_max = 0, sync_ints = 0;
   size_t off_part = 0, off_label = 0, off_lse = 0, off_coef = 0, off_rowloss = 0;
-  size_t off_flag = 0, off_sync = 0, off_sync2 = 0, off_ring = 0;
+  size_t off_flag = 0, off_sync = 0, off_sync2 = 0, off_ring = 0, off_split = 0;
   size_t off_wt = 0, off_dz = 0, total = 0;
 };
 
@@ -719,7 +719,11 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad, bool h
       // kCeTeam; more slices take several passes), the rest produce; the ring gives every
       // producer two slots plus slack
       P.slices = (int)ceil_div(d, 256);
-      P.consumers = std::min(P.slices, 24);
+      // A producer's item costs slices times a consumer's share of it. With fewer than 16 slices,
+      // F = 16 / slices consumers per slice split the vocabulary tiles between them, so that
+      // producers and consumers stay near 16 each; their sums meet in a fixed order.
+      P.ksplit = P.slices < 16 ? (int)std::max<int64_t>(1, std::min<int64_t>(16 / P.slices, P.nv)) : 1;
+      P.consumers = P.ksplit > 1 ? P.slices * P.ksplit : std::min(P.slices, 24);
       P.passes = (int)ceil_div(P.slices, P.consumers);
       P.slots = 2 * (kCeTeam - P.consumers) + 4;
       // items of the busiest team: its row tiles (one in 8) x passes x vocabulary tiles
@@ -729,6 +733,10 @@ CePlan ce_plan(int64_t N, int64_t d, int64_t V, int32_t dtype, bool grad, bool h
       P.off_sync = o;  o += align256((size_t)P.sync_ints * 4);
       P.off_sync2 = o; o += align256((size_t)P.sync_ints * 4);
       P.off_ring = o;  o += align256(ce_fused_ring_bytes(P.slots));
+      if (P.ksplit > 1) {
+        P.off_split = o;
+        o += align256((size_t)8 * P.slices * (P.ksplit - 1) * 256 * 256 * sizeof(float));
+      }
       if (!have_head_t) {
         P.off_wt = o;
         o += align256((size_t)d * P.Vp * 2);
@@ -969,6 +977,8 @@ extern "C" attt_status attt_weighted_ce_fwd_bwd_ex(const void* hidden, const voi
   fa.slices = P.slices;
   fa.consumers = P.consumers;
   fa.passes = P.passes;
+  fa.ksplit = P.ksplit;
+  fa.partial = P.ksplit > 1 ? reinterpret_cast<float*>(ws + P.off_split) : nullptr;
   fa.slots = P.slots;
   fa.items_max = P.items_max;
   HIP_TRY(launch_ce_fused(true, fa, s), "ce_fused_bwd");

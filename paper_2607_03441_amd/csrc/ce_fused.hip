@@ -51,10 +51,11 @@ constexpr size_t kFusedLds = kFusedLdsData + 4 * sizeof(int);
 
 // sync area (ints): team counts [8], arrive, abort, the site of the first wait that ran out
 // (diagnostics: 1 grid barrier, 2 consumer awaiting a tile, 3 producer awaiting a free slot,
-// 4 idle consumer), then consumed [8][S] per ring slot and published [8][G] per item (G: the
-// most items a team has, a multiple of 4)
+// 4 idle consumer, 5 partial sums of the vocabulary split), then consumed [8][S] per ring slot,
+// published [8][G] per item (G: the most items a team has, a multiple of 4) and, per team, the
+// split's ready [kCeTeam] and freed [kCeTeam] counters
 constexpr int kSyncTeam = 0, kSyncArrive = 8, kSyncAbort = 9, kSyncSite = 10, kSyncSlots = 16;
-enum { kSiteGrid = 1, kSiteTile = 2, kSiteSlot = 3, kSiteIdle = 4 };
+enum { kSiteGrid = 1, kSiteTile = 2, kSiteSlot = 3, kSiteIdle = 4, kSitePartial = 5 };
 
 __device__ __forceinline__ int ld_agent(const int* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -110,9 +111,10 @@ __device__ __forceinline__ bool acquire_geq(const int* p, int target, int* abort
 // decision from the same stored z_y and lse, so they always agree.
 __device__ __forceinline__ bool exact_fold(float z_y, float lse) { return z_y - lse > -0.69314718f; }
 
-// The consumer's GEMM: acc += A[0:256, 0:K] T^T with T the ring tiles of items gbase ..
-// gbase + nitems - 1 laid end to end along K (each [256 tokens][256 vocab]); A = W^T rows of the
-// d-slice. The same 8-wave ping-pong as mfma_mainloop_pp16, with the same group counter before
+// The consumer's GEMM: acc += A[0:256, 0:K] T^T with T the ring tiles of items gbase,
+// gbase + step, ..., nitems of them, laid end to end along K (each [256 tokens][256 vocab]);
+// A = W^T rows of the d-slice, read at the items' vocabulary columns (item i is vocabulary tile
+// vfirst + i step). The same 8-wave ping-pong as mfma_mainloop_pp16, with the same group counter before
 // group 1's refills; only group 1 (waves 4-7) loads ring blocks inside the loop (group 0's share
 // of a stage is A blocks), so group 1 waits for an item's ready flag before issuing its first
 // stage (ensure: flags read 16 items at a time), and signals `consumed` once its loads of the
@@ -120,9 +122,9 @@ __device__ __forceinline__ bool exact_fold(float z_y, float lse) { return z_y - 
 // gbase in every wave.
 template <class C>
 __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, int64_t lda, int mval,
-                                                  const uint8_t* ring, int nval, int nitems, int gbase, int S,
-                                                  const int* published, int* consumed, int* abort, uint64_t limit,
-                                                  bf16_t* lds, Acc16& acc, int tid) {
+                                                  const uint8_t* ring, int nval, int nitems, int gbase, int step,
+                                                  int vfirst, int S, const int* published, int* consumed, int* abort,
+                                                  uint64_t limit, bf16_t* lds, Acc16& acc, int tid) {
   static_assert(C::NT == 512 && C::WGM == 2 && C::WGN == 4 && C::BN == 256, "8 waves over 256-token tiles");
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -153,15 +155,17 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
   constexpr int JA = ABLK / LW;
   auto dma = [&](int st, int k, int j0, int j1) {
     bf16_t* base = lds + st * (C::SA + C::SB);
-    const int slot = (gbase + (k >> 2)) % S;
+    const int slot = (gbase + (k >> 2) * step) % S;
     const uint32_t kcol = (uint32_t)(k & 3) * 64;
+    // the stage's vocabulary columns: item k / 4 is vocabulary tile vfirst + (k / 4) step
+    const int vcol = (vfirst + (k >> 2) * step) * 256 + (int)kcol;
 #pragma unroll
     for (int j = j0; j < j1 && j < JA; ++j) {
       const int blk = (wave & 3) + j * LW;
       const int rb = blk * 8;
       const int c = (rb & 8) ? c_odd : c_even;
       const bool ok = rb + lr < mval;
-      const uint32_t off = (uint32_t)((int64_t)rb * lda * 2) + la + (uint32_t)(k * 64 + c * 8) * 2;
+      const uint32_t off = (uint32_t)((int64_t)rb * lda * 2) + la + (uint32_t)(vcol + c * 8) * 2;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (__attribute__((address_space(3))) void*)(base + blk * 512), 16,
                                                ok ? off : kOOB, 0, 0, 0);
     }
@@ -184,27 +188,27 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
   };
   auto compute = [&]() { mma16_step(fa, fb, acc); };
   auto pin = [&]() { mma16_pin(acc); };
-  auto slot_of = [&](int item) { return (gbase + item) % S; };
+  auto slot_of = [&](int item) { return (gbase + item * step) % S; };
   // Items [0, known) of this mainloop are known to be published. ensure(i) makes item i known:
   // one 16-byte memory-side load (sc1, as a relaxed agent-scope atomic load is) reads the
   // published flags of the four items of its aligned group, and every consecutive published item
   // from i on becomes known, so while the producers run ahead the flags cost one round trip per
   // four items. New items are acquired with an L1 invalidate. The wait is bounded like wait_geq.
-  const __amdgpu_buffer_rsrc_t rP = buffer_rsrc(published, (gbase + nitems + 3) / 4 * 16);
+  const __amdgpu_buffer_rsrc_t rP = buffer_rsrc(published, ((gbase + (nitems - 1) * step) / 4 + 1) * 16);
   int known = 0;
   auto ensure = [&](int i) {
     if (i < known) return;
-    const int g = gbase + i, g4 = g & ~3;
+    const int g = gbase + i * step, g4 = g & ~3;
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     while (true) {
       const u32x4 fv = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rP, (uint32_t)g4 * 4u, 0, 16));
       // every lane read the same four flags: keep them (and what follows from them) scalar
       const uint32_t f[4] = {(uint32_t)__builtin_amdgcn_readfirstlane(fv[0]), (uint32_t)__builtin_amdgcn_readfirstlane(fv[1]),
                              (uint32_t)__builtin_amdgcn_readfirstlane(fv[2]), (uint32_t)__builtin_amdgcn_readfirstlane(fv[3])};
-      int j = g - g4;
-      while (j < 4 && f[j] != 0u) ++j;
-      if (g4 + j > g) {
-        known = g4 + j - gbase;
+      int j = g - g4, run = 0;
+      while (j < 4 && f[j] != 0u) j += step, ++run;
+      if (run > 0) {
+        known = i + run;
         l1_invalidate();
         return;
       }
@@ -268,8 +272,10 @@ __device__ __forceinline__ void consumer_mainloop(const bf16_t* __restrict__ A, 
   }
 }
 
-template <bool kLabel>
-__global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
+// The kernel body. kSplit: the consumers split the vocabulary tiles of a d-slice (F = ksplit > 1);
+// a separate instantiation, so that the kernel without it keeps its own register allocation.
+template <bool kLabel, bool kSplit>
+__device__ __forceinline__ void ce_fused_body(const CeFusedArgs& a) {
   using C = CfgBig;
   extern __shared__ __align__(16) uint8_t smem[];
   int* info = reinterpret_cast<int*>(smem + kFusedLdsData);
@@ -327,7 +333,9 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
       mfma_mainloop_pp16<C>(a.W + (int64_t)v0 * a.d, a.d, a.V - v0, a.h + (int64_t)t0 * a.d, a.d, R, a.d, lds, acc,
                           tix, g != rank);
       // the slot's previous use must have been read by every consumer (four waves each)
-      wait_geq(consumed + slot, 4 * Cn * (g / S), abort, a.limit, kSiteSlot);
+      // (four waves of every consumer that reads the slot: all of them with one consumer per
+      // d-slice, whose idle ones pace too; with the vocabulary split, one per d-slice)
+      wait_geq(consumed + slot, 4 * (kSplit ? a.slices : Cn) * (g / S), abort, a.limit, kSiteSlot);
       // start the next item's first stages now, so that their latency hides behind this epilogue
       // (they land before the publish below; an abort at the next item's check finds them landed)
       if (g + P < items) {
@@ -436,7 +444,7 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
     return;
   }
 
-  // ---- consumer: d-slice (pass * Cn + c) of every row tile of the team, items in order ----
+  // ---- consumer: a d-slice of every row tile of the team, items in order ----
   const int c = rank - P;
   for (int j = 0; j < nrt; ++j) {
     const int t0 = (x + 8 * j) * 256;
@@ -450,8 +458,12 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
       const int lane = tix & 63, wave = __builtin_amdgcn_readfirstlane(tix >> 6);
       const int wm = wave / C::WGN, wn = wave % C::WGN;
       const int gbase = (j * a.passes + pass) * a.nv;
-      const int slice = pass * Cn + c;
-      if (slice >= a.slices) {
+      // with the vocabulary split (F = ksplit > 1, one pass), consumer c takes d-slice c % slices
+      // and, as part c / slices, the vocabulary tiles part, part + F, ...
+      const int F = kSplit ? a.ksplit : 1;
+      const int slice = kSplit ? c % a.slices : pass * Cn + c;
+      const int part = kSplit ? c / a.slices : 0;
+      if (!kSplit && slice >= a.slices) {
         // idle in this pass, but every consumer paces and releases every slot
         if (wave >= 4)
           for (int v = 0; v < a.nv; ++v) {
@@ -462,8 +474,46 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
       }
       const int m0 = slice * 256;  // first column of dL/dh
       Acc16 acc;
-      consumer_mainloop<C>(a.WT + (int64_t)m0 * a.Vp, a.Vp, a.d - m0, ring, R, a.nv, gbase, S, published,
-                           consumed, abort, a.limit, lds, acc, tix);
+      consumer_mainloop<C>(a.WT + (int64_t)m0 * a.Vp, a.Vp, a.d - m0, ring, R, (a.nv - part + F - 1) / F,
+                           gbase + part, F, part, S, published, consumed, abort, a.limit, lds, acc, tix);
+      if constexpr (kSplit) {
+        // Parts 1 .. F-1 hand their float32 sums to part 0 through a per-(team, slice, part)
+        // buffer, in the thread order of the accumulators; part 0 adds them in part order (a
+        // fixed order) and writes the slice. Flags (per team): ready[c] = row tiles whose sums
+        // consumer c has written, freed[slice] = row tiles whose sums part 0 has read.
+        int* ready = sync + kSyncSlots + 8 * S + 8 * a.items_max + x * 2 * kCeTeam;
+        int* freed = ready + kCeTeam;
+        const size_t per = (size_t)256 * 256;
+        float* mine = a.partial + (((size_t)x * a.slices + slice) * (F - 1)) * per;
+        if (part > 0) {
+          float* dst = mine + (size_t)(part - 1) * per;
+          wait_geq(freed + slice, j, abort, a.limit, kSitePartial);  // row tile j-1's sums were read
+#pragma unroll
+          for (int i = 0; i < Mma16::TM; ++i)
+#pragma unroll
+            for (int jj = 0; jj < Mma16::TN; ++jj)
+              *reinterpret_cast<f32x4*>(dst + ((size_t)(i * Mma16::TN + jj) * C::NT + tix) * 4) = acc[i][jj];
+          __builtin_amdgcn_s_waitcnt(0);  // this wave's sums are in the L2
+          __syncthreads();
+          if (tix == 0) st_agent(ready + c, j + 1);
+          continue;  // part 0 writes the slice
+        }
+        for (int f = 1; f < F; ++f) {
+          wait_geq(ready + f * a.slices + slice, j + 1, abort, a.limit, kSitePartial);
+          l1_invalidate();
+          const float* src = mine + (size_t)(f - 1) * per;
+#pragma unroll
+          for (int i = 0; i < Mma16::TM; ++i)
+#pragma unroll
+            for (int jj = 0; jj < Mma16::TN; ++jj) {
+              const f32x4 v = *reinterpret_cast<const f32x4*>(src + ((size_t)(i * Mma16::TN + jj) * C::NT + tix) * 4);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[i][jj][e] += v[e];
+            }
+        }
+        __syncthreads();  // every wave has its sums of all parts
+        if (tix == 0) st_agent(freed + slice, j + 1);
+      }
       // row scales: sigma_t from the producers' per-tile sums in a fixed order (two threads per
       // token: even and odd vocab tiles), sa = coef / (1 + sigma), sb = coef sigma / (1 + sigma)
       float* sig = reinterpret_cast<float*>(smem);  // [256][2], after the mainloop's last barrier
@@ -545,6 +595,15 @@ __global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
   }
 }
 
+template <bool kLabel>
+__global__ __launch_bounds__(512) void ce_fused_bwd_kernel(CeFusedArgs a) {
+  ce_fused_body<kLabel, false>(a);
+}
+template <bool kLabel>
+__global__ __launch_bounds__(512) void ce_fused_bwd_split_kernel(CeFusedArgs a) {
+  ce_fused_body<kLabel, true>(a);
+}
+
 // Zeroes `n` ints (the sync areas) with vector stores.
 __global__ __launch_bounds__(256) void ce_sync_clear_kernel(int* p, int n) {
   for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
@@ -568,7 +627,9 @@ __global__ __launch_bounds__(256) void ce_fused_nan_kernel(const int* sync, floa
 
 // ------------------------------------------------------------------------------------------
 size_t ce_fused_ring_bytes(int slots) { return (size_t)8 * slots * kSlotBytes; }
-int ce_fused_sync_ints(int slots, int items_max) { return kSyncSlots + 8 * slots + 8 * items_max; }
+int ce_fused_sync_ints(int slots, int items_max) {
+  return kSyncSlots + 8 * slots + 8 * items_max + 8 * 2 * kCeTeam;
+}
 
 hipError_t launch_ce_sync_clear(int* sync, int n, hipStream_t s) {
   const int blocks = (n + 255) / 256 < 64 ? (n + 255) / 256 : 64;
@@ -577,21 +638,22 @@ hipError_t launch_ce_sync_clear(int* sync, int n, hipStream_t s) {
 }
 
 hipError_t launch_ce_fused(bool label, const CeFusedArgs& a, hipStream_t s) {
+  const void* fns[2][2] = {{reinterpret_cast<const void*>(ce_fused_bwd_kernel<false>),
+                            reinterpret_cast<const void*>(ce_fused_bwd_split_kernel<false>)},
+                           {reinterpret_cast<const void*>(ce_fused_bwd_kernel<true>),
+                            reinterpret_cast<const void*>(ce_fused_bwd_split_kernel<true>)}};
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(ce_fused_bwd_kernel<true>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLds);
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(ce_fused_bwd_kernel<false>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLds);
-    if (e != hipSuccess) return e;
+    for (int i = 0; i < 4; ++i) {
+      hipError_t e = hipFuncSetAttribute(fns[i >> 1][i & 1], hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFusedLds);
+      if (e != hipSuccess) return e;
+    }
     attr = true;
   }
   CeFusedArgs arg = a;
   void* args[] = {&arg};
   KernelTimer t(label ? K_CE_FUSED : K_CE_GUARD, s);
-  const void* fn = label ? reinterpret_cast<const void*>(ce_fused_bwd_kernel<true>)
-                         : reinterpret_cast<const void*>(ce_fused_bwd_kernel<false>);
+  const void* fn = fns[label ? 1 : 0][a.ksplit > 1 ? 1 : 0];
   return hipLaunchCooperativeKernel(fn, dim3(8 * kCeTeam), dim3(CfgBig::NT), args, (unsigned)kFusedLds, s);
 }
 

@@ -264,8 +264,11 @@ struct CeFusedArgs {
   int nv;                     // vocabulary tiles of 256
   int row_tiles;              // row tiles of 256
   int slices;                 // d-slices of 256
-  int consumers;              // consumers per team (<= slices); producers = kCeTeam - consumers
+  int consumers;              // consumers per team; producers = kCeTeam - consumers
   int passes;                 // ceil(slices / consumers): the row tile's tiles are made once per pass
+  int ksplit;                 // consumers per d-slice (F): part f takes vocabulary tiles f, f + F, ...
+                              // (F > 1 only with one pass and consumers = slices x F)
+  float* partial;             // F > 1: [8 teams][slices][F - 1][256 x 256] float32 partial sums
   int slots;                  // ring slots per XCD
   int items_max;              // items of the busiest team, rounded up to a multiple of 4
 };

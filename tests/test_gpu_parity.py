@@ -154,6 +154,27 @@ def test_ce_ragged(attt, bf16, shape):
     _ce_case(attt, h, W, labels, weights, off, bf16)
 
 
+# d below 16 slices of 256: the consumers of a d-slice split its vocabulary tiles (F = 16 / slices,
+# at most the tile count) and their sums meet in a fixed order. Several row tiles per team, so
+# a part hands over its sums more than once: (4700, 256, 3000) F = 12 with 19 row tiles,
+# (4100, 1024, 9000) F = 4 with 17, (4500, 2048, 4000) F = 2 with 18.
+@pytest.mark.parametrize("shape", [(4700, 256, 3000), (4100, 1024, 9000), (4500, 2048, 4000)])
+def test_ce_vocab_split_many_row_tiles(attt, shape):
+    N, d, V = shape
+    note(f"ce vocabulary split {shape}")
+    h = random_dense((N, d), 1.0, True, 91)
+    W = random_dense((V, d), 0.05, True, 92)
+    rng = np.random.default_rng(93)
+    labels = rng.integers(0, V, N).astype(np.int32)
+    weights = rng.uniform(0.05, 1, N).astype(np.float32)
+    off = np.array([0, 1234, N], np.int64)
+    loss, lse, dH = _ce_case(attt, h, W, labels, weights, off, True)
+    again = [host(t) for t in attt.weighted_ce_fwd_bwd(dev_dense(h), dev_dense(W), dev_i32(labels), dev_f32(weights),
+                                                       row_offsets=off)]
+    for a, b in zip((loss, lse, dH), again):
+        assert a.tobytes() == b.tobytes()
+
+
 def test_ce_unit_weights_is_mean_ce(attt):
     N, d, V = 128, 64, 500
     h = random_dense((N, d), 1.0, False, 21)
