@@ -233,7 +233,9 @@ attt_status attt_ngram_set_weights(void* const* sets, const int32_t* tokens, con
  * vocabulary) at all: one persistent kernel computes 256 x 256 tiles of the softmax numerators
  * e_tv = exp(z_tv - z_{t,labels[t]}) and, on other CUs of the same XCD, contracts them with W as
  * they arrive through a ring of a few MB in the workspace (dL/dh is a per-row scale of
- * sum_v e_tv W_v minus the label term). It needs the MI355X layout of 256 CUs in 8 XCDs and
+ * sum_v e_tv W_v minus the label term). Below 16 slices of 256 in d, the consumers of a slice
+ * split the vocabulary tiles, and the workspace also holds their float32 partial sums (at
+ * most 30 MiB); they are added in a fixed order, so results stay bitwise repeatable. It needs the MI355X layout of 256 CUs in 8 XCDs and
  * cooperative launch (ATTT_EUNSUPPORTED otherwise). The float32 backward stages dL/dz for blocks
  * of at most 8192 rows x 131072 columns in the workspace.
  *
