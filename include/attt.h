@@ -133,7 +133,7 @@ attt_status attt_ngram_weights_noalloc(const int32_t* history, const int64_t* hi
  * lse, dsum       device float32 [heads][N]: the forward's log-sum-exp and D (written)
  * All device pointers 16-byte aligned. Errors (before any HIP call): ATTT_EINVAL for bad
  * offsets, null or misaligned pointers, heads not a multiple of kv_heads, a bad scale;
- * ATTT_EUNSUPPORTED for head_dim != 128 or N >= 2^31 / heads. */
+ * ATTT_EUNSUPPORTED for head_dim != 128, heads >= 2^16 or N >= 2^31 / heads. */
 attt_status attt_attention_bwd(const void* q, const void* k, const void* v, const void* dout,
                                const int64_t* row_offsets, int32_t num_episodes, int64_t N,
                                int32_t heads, int32_t kv_heads, int32_t head_dim, float scale,

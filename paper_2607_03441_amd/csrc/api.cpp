@@ -386,6 +386,7 @@ extern "C" attt_status attt_attention_bwd(const void* q, const void* k, const vo
   if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(ATTT_EINVAL, "attention: scale must be finite and > 0");
   if (N < 0) return fail(ATTT_EINVAL, "attention: N must be >= 0");
   if (N * heads >= INT32_MAX) return fail(ATTT_EUNSUPPORTED, "attention: N x heads must be < 2^31");
+  if (heads >= (1 << 16)) return fail(ATTT_EUNSUPPORTED, "attention: heads must be < 2^16 (got %d)", heads);
   if (num_episodes < 1) return fail(ATTT_EINVAL, "attention: num_episodes must be >= 1 (got %d)", num_episodes);
   int64_t single[2] = {0, N};
   const int64_t* off = row_offsets;

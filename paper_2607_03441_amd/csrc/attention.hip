@@ -71,13 +71,16 @@ __device__ __forceinline__ void load_key_frags(bf16x8 (&f)[4], const bf16_t* src
 // 8 (tid % 16) .. +7: fetch_block issues its four 16-byte loads (rows >= nvalid read as zero),
 // store_block writes them with four 16-byte stores and, for each of its eight columns, one
 // 8-byte store of the four rows.
+// The loads go through one buffer descriptor over the block's valid rows (base and range in
+// scalar registers, 32-bit offsets per lane): rows at or past nvalid fall outside its range and
+// read as zero. A 64-row block spans less than 2^30 bytes (heads < 2^16, checked on the host).
 __device__ __forceinline__ void fetch_block(u32x4 (&v)[4], const bf16_t* src, int64_t stride, int nvalid, int tid) {
   const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 8;
+  const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(src, nvalid > 0 ? (int)(((int64_t)(nvalid - 1) * stride + DH) * 2) : 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[i] = u32x4{0u, 0u, 0u, 0u};
-    if (r0 + i < nvalid) v[i] = *reinterpret_cast<const u32x4*>(src + (int64_t)(r0 + i) * stride + c0);
-  }
+  for (int i = 0; i < 4; ++i)
+    v[i] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(((int64_t)(r0 + i) * stride + c0) * 2), 0, 0));
 }
 
 __device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, bf16_t* dstT, int tid) {

@@ -330,6 +330,7 @@ def test_attention_validation(L):
     assert _attn(L, scale=0.0) == attt.EINVAL
     assert _attn(L, scale=float("nan")) == attt.EINVAL
     assert _attn(L, N=-1) == attt.EINVAL
+    assert _attn(L, N=1, H=1 << 16, Hkv=1) == attt.EUNSUPPORTED   # a block's byte range must stay < 2^30
     assert _attn(L, E=2) == attt.EINVAL                       # NULL offsets need one episode
     assert _attn(L, off=[0, 10, 60]) == attt.EINVAL           # offsets end != N
     assert _attn(L, off=[0, 40, 30, 64]) == attt.EINVAL       # decreasing
