@@ -17,9 +17,9 @@
 // the B operand of the score products, so each lane ends up with 16 scores of its own row. The
 // probabilities (or dS) of that row then enter the second product (P V, P^T dO, dS^T Q, dS K)
 // directly as the A operand: the contraction index is the one the lane's registers run over,
-// in the order they hold it, and the B operand is read from a transposed LDS tile in the same
-// order. Every block goes to LDS once row-major and, where a product needs it, once transposed,
-// with 16- and 8-byte stores.
+// in the order they hold it, and the B operand is read in the same order from the row-major LDS
+// tile with transposing reads (ds_read_tr16_b64). Every block goes to LDS once, row-major, with
+// 16-byte stores.
 // P and dS enter their second products as bf16 pairs hi + lo (two MFMA passes, about 16
 // significant bits): those sums mix signs (dS even sums to zero over each row), and a single
 // bf16 rounding of P or dS would show in their small elements. The final bf16 rounding of the
@@ -33,7 +33,6 @@ namespace {
 constexpr int DH = 128;     // head dimension
 constexpr int BLK = 64;     // query / key rows per block
 constexpr int PR = DH + 8;  // LDS pitch of a [64][128] tile (bf16): 272 B, conflict-free b128 reads
-constexpr int PT = BLK + 8; // LDS pitch of a transposed [128][64] tile and of P / dS staging
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
@@ -66,11 +65,9 @@ __device__ __forceinline__ void load_key_frags(bf16x8 (&f)[4], const bf16_t* src
   }
 }
 
-// Rows [0, BLK) of a [rows][DH] block, staged in LDS twice: row-major into dst (pitch PR) and
-// transposed into dstT[c][...] (pitch PT; row r of the block at 4 ((r / 4) ^ (c / 8)) + r % 4). Thread tid takes rows 4 (tid / 16) .. +3 and columns
-// 8 (tid % 16) .. +7: fetch_block issues its four 16-byte loads (rows >= nvalid read as zero),
-// store_block writes them with four 16-byte stores and, for each of its eight columns, one
-// 8-byte store of the four rows.
+// Rows [0, BLK) of a [rows][DH] block, staged in LDS row-major (pitch PR). Thread tid takes rows
+// 4 (tid / 16) .. +3 and columns 8 (tid % 16) .. +7: fetch_block issues its four 16-byte loads
+// (rows >= nvalid read as zero), store_block writes them with four 16-byte stores.
 // The loads go through one buffer descriptor over the block's valid rows (base and range in
 // scalar registers, 32-bit offsets per lane): rows at or past nvalid fall outside its range and
 // read as zero. A 64-row block spans less than 2^30 bytes (heads < 2^16, checked on the host).
@@ -83,22 +80,10 @@ __device__ __forceinline__ void fetch_block(u32x4 (&v)[4], const bf16_t* src, in
         u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(((int64_t)(r0 + i) * stride + c0) * 2), 0, 0));
 }
 
-__device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, bf16_t* dstT, int tid) {
+__device__ __forceinline__ void store_block(const u32x4 (&v)[4], bf16_t* dst, int tid) {
   const int r0 = (tid >> 4) * 4, c0 = (tid & 15) * 8;
-  if (dst)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
-  if (!dstT) return;
-  // groups of four rows are placed at group ^ (c / 8) within a transposed row c (see tfrag),
-  // which spreads the sixteen columns a 16-lane group writes over distinct banks
-  const int unit = (r0 >> 2) ^ (c0 >> 3);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int wi = e >> 1, sh = (e & 1) * 16;
-    const uint32_t x0 = (v[0][wi] >> sh) & 0xFFFFu, x1 = (v[1][wi] >> sh) & 0xFFFFu;
-    const uint32_t x2 = (v[2][wi] >> sh) & 0xFFFFu, x3 = (v[3][wi] >> sh) & 0xFFFFu;
-    *reinterpret_cast<uint2*>(dstT + (c0 + e) * PT + 4 * unit) = make_uint2(x0 | (x1 << 16), x2 | (x3 << 16));
-  }
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(dst + (r0 + i) * PR + c0) = v[i];
 }
 
 // hi = RN(x), lo = RN(x - hi) of the eight values of an MFMA operand, as bf16x8 pairs.
@@ -113,13 +98,20 @@ __device__ __forceinline__ void split_frag(const float (&x)[8], bf16x8& hi, bf16
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
-// B operand over 32 queries of chunk u from a transposed tile (pitch PT, store_block's layout):
-// lane (l16, q4) takes column c = c0 + l16 at queries 32 u + 4 q4 .. +3 and 32 u + 16 + 4 q4 ..
-// +3, the order in which the P / dS fragments hold them.
-__device__ __forceinline__ bf16x8 tfrag(const bf16_t* T, int c, int u, int q4) {
-  const int f = (c >> 3) & 15;  // the row-group swizzle of store_block
-  const uint2 a = *reinterpret_cast<const uint2*>(T + c * PT + 4 * ((8 * u + q4) ^ f));
-  const uint2 b = *reinterpret_cast<const uint2*>(T + c * PT + 4 * ((8 * u + 4 + q4) ^ f));
+// B operand of the second products over the 32 rows (queries, or keys) of chunk u, from a
+// row-major [64][DH] tile (pitch PR) through transposing LDS reads: lane (l16, q4) receives
+// column c0 + l16 at rows 32 u + 4 q4 .. +3 and 32 u + 16 + 4 q4 .. +3, the order in which the
+// P / dS fragments hold them. ds_read_tr16_b64 hands, within each group of 16 lanes, lane i the
+// element i mod 4 of lanes 4e + i/4 (e = 0..3), so lane 4e + c of group q4 addresses row
+// 32 u + 4 q4 + e (then 16 rows further) at columns c0 + 4c .. +3.
+__device__ __forceinline__ bf16x8 trfrag(const bf16_t* R, int c0, int u, int lane) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4s* lds_v4s;
+  const int q4 = lane >> 4, e = (lane >> 2) & 3, c = lane & 3;
+  const bf16_t* p = R + (32 * u + 4 * q4 + e) * PR + c0 + 4 * c;
+  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p));
+  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(p + 16 * PR));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
   return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
 }
 
@@ -138,7 +130,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
   const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
   extern __shared__ __align__(16) uint8_t smem[];
   bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* Vt = Ks + BLK * PR;                     // [128][PT]
+  bf16_t* Vs = Ks + BLK * PR;                     // [64][PR]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
   const int qry = 16 * w + l16;
@@ -160,8 +152,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
     __syncthreads();  // the previous block's reads of the tiles are done
-    store_block(fk, Ks, nullptr, tid);
-    store_block(fv, nullptr, Vt, tid);
+    store_block(fk, Ks, tid);
+    store_block(fv, Vs, tid);
     __syncthreads();
     if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
     f32x4 st[4];
@@ -217,7 +209,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
     for (int j = 0; j < 8; ++j)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const bf16x8 bv = tfrag(Vt, 16 * j + l16, u, q4);
+        const bf16x8 bv = trfrag(Vs, 16 * j, u, lane);
         o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bv, o[j], 0, 0, 0);
         o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bv, o[j], 0, 0, 0);
       }
@@ -257,9 +249,7 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
   extern __shared__ __align__(16) uint8_t smem[];
   bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
   bf16_t* dOs = Qs + BLK * PR;                    // [64][PR]
-  bf16_t* Qt = dOs + BLK * PR;                    // [128][PT]
-  bf16_t* dOt = Qt + DH * PT;                     // [128][PT]
-  float* lse_s = reinterpret_cast<float*>(dOt + DH * PT);  // [64]
+  float* lse_s = reinterpret_cast<float*>(dOs + BLK * PR);  // [64]
   float* d_s = lse_s + BLK;                                // [64]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
@@ -294,8 +284,8 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
   for (int i = 0; i < steps; ++i) {
     const int q0 = (nqb - 1 - i / g) * BLK;
     __syncthreads();  // the previous step's reads of the tiles are done
-    store_block(fq, Qs, Qt, tid);
-    store_block(fo, dOs, dOt, tid);
+    store_block(fq, Qs, tid);
+    store_block(fo, dOs, tid);
     if (tid < BLK) lse_s[tid] = fl, d_s[tid] = fd;
     __syncthreads();
     if (i + 1 < steps) fetch(i + 1);  // the next step's blocks load while this one computes
@@ -341,10 +331,10 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
       for (int j = 0; j < 8; ++j)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const bf16x8 bo = tfrag(dOt, 16 * j + l16, u, q4);
+          const bf16x8 bo = trfrag(dOs, 16 * j, u, lane);
           dv[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bo, dv[j], 0, 0, 0);
           dv[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bo, dv[j], 0, 0, 0);
-          const bf16x8 bq = tfrag(Qt, 16 * j + l16, u, q4);
+          const bf16x8 bq = trfrag(Qs, 16 * j, u, lane);
           dk[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh[u], bq, dk[j], 0, 0, 0);
           dk[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bq, dk[j], 0, 0, 0);
         }
@@ -379,7 +369,6 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
   extern __shared__ __align__(16) uint8_t smem[];
   bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
   bf16_t* Vs = Ks + BLK * PR;                     // [64][PR]
-  bf16_t* Kt = Vs + BLK * PR;                     // [128][PT]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
   const int qry = 16 * w + l16;  // this lane's query in the block
@@ -404,8 +393,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
     __syncthreads();  // the previous block's reads of the tiles are done
-    store_block(fk, Ks, Kt, tid);
-    store_block(fv, Vs, nullptr, tid);
+    store_block(fk, Ks, tid);
+    store_block(fv, Vs, tid);
     __syncthreads();
     if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
     // S^T[16 t + 4 q4 + r][query] and dP^T likewise
@@ -442,7 +431,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
     for (int j = 0; j < 8; ++j)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const bf16x8 bk = tfrag(Kt, 16 * j + l16, u, q4);
+        const bf16x8 bk = trfrag(Ks, 16 * j, u, lane);
         dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh[u], bk, dq[j], 0, 0, 0);
         dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bk, dq[j], 0, 0, 0);
       }
@@ -459,9 +448,9 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
 }
 
 size_t attn_lds_bytes(int kernel) {
-  if (kernel == 0) return (size_t)(BLK * PR + DH * PT) * 2;
-  if (kernel == 1) return (size_t)(2 * BLK * PR + 2 * DH * PT) * 2 + 2 * BLK * 4;
-  return (size_t)(2 * BLK * PR + DH * PT) * 2;
+  if (kernel == 0) return (size_t)(2 * BLK * PR) * 2;
+  if (kernel == 1) return (size_t)(2 * BLK * PR) * 2 + 2 * BLK * 4;
+  return (size_t)(2 * BLK * PR) * 2;
 }
 
 hipError_t launch_attn(int kernel, const AttnArgs& a, const AttnBatch& b, int wgs, hipStream_t s) {
