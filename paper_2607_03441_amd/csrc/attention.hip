@@ -19,11 +19,14 @@
 // directly as the A operand: the contraction index is the one the lane's registers run over,
 // in the order they hold it, and the B operand is read in the same order from the row-major LDS
 // tile with transposing reads (ds_read_tr16_b64). Every block goes to LDS once, row-major, with
-// 16-byte stores.
+// 16-byte stores, into one of two buffers (one barrier per block). Blocks strictly below the
+// diagonal skip the causal and ragged-row masks.
 // P and dS enter their second products as bf16 pairs hi + lo (two MFMA passes, about 16
 // significant bits): those sums mix signs (dS even sums to zero over each row), and a single
 // bf16 rounding of P or dS would show in their small elements. The final bf16 rounding of the
 // outputs is then the main error.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -34,6 +37,23 @@ constexpr int DH = 128;     // head dimension
 constexpr int BLK = 64;     // query / key rows per block
 constexpr int PR = DH + 8;  // LDS pitch of a [64][128] tile (bf16): 272 B, conflict-free b128 reads
 constexpr float kLog2e = 1.4426950408889634f;
+
+// LDS: two buffers, so that the next block is stored while the current one is read and a step
+// needs one barrier. A buffer of the per-query kernels holds the K and V tiles; one of the
+// per-key kernel holds the Q and dO tiles, then lse and D of the block's 64 queries.
+constexpr int kTileBytes = BLK * PR * 2;
+constexpr int kKvBuf = 2 * kTileBytes;
+constexpr int kQoBuf = 2 * kTileBytes + 2 * BLK * 4;
+
+__device__ __forceinline__ bf16_t* kv_tile(uint8_t* smem, int buf, int t) {
+  return reinterpret_cast<bf16_t*>(smem + buf * kKvBuf + t * kTileBytes);
+}
+__device__ __forceinline__ bf16_t* qo_tile(uint8_t* smem, int buf, int t) {
+  return reinterpret_cast<bf16_t*>(smem + buf * kQoBuf + t * kTileBytes);
+}
+__device__ __forceinline__ float* qo_stats(uint8_t* smem, int buf) {  // lse [64], then D [64]
+  return reinterpret_cast<float*>(smem + buf * kQoBuf + 2 * kTileBytes);
+}
 
 __device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 __device__ __forceinline__ bf16_t f2bf(float x) { return (bf16_t)(pack_bf16x2(x, 0.0f) & 0xFFFFu); }
@@ -128,9 +148,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
   const AttnEp E = b.e[ei];
   const int kh = h / (a.heads / a.kv_heads);
   const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
-  extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* Vs = Ks + BLK * PR;                     // [64][PR]
+  extern __shared__ __align__(16) uint8_t smem[];  // two buffers of [K tile][V tile], [64][PR] each
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
   const int qry = 16 * w + l16;
@@ -149,13 +167,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
     fetch_block(fv, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
   };
   fetch(0);
+  store_block(fk, kv_tile(smem, 0, 0), tid);
+  store_block(fv, kv_tile(smem, 0, 1), tid);
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
-    __syncthreads();  // the previous block's reads of the tiles are done
-    store_block(fk, Ks, tid);
-    store_block(fv, Vs, tid);
+    // This block's tiles are stored, and every wave is done with the other buffer.
     __syncthreads();
     if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
+    const bf16_t* Ks = kv_tile(smem, kb & 1, 0);
+    const bf16_t* Vs = kv_tile(smem, kb & 1, 1);
     f32x4 st[4];
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0};
@@ -167,30 +187,38 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
             bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
         st[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[s4], st[tt], 0, 0, 0);
       }
-    // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r
-    float mx = -INFINITY;
+    // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r.
+    // A key block before the query block is whole and entirely allowed: no mask there.
+    float mx = -INFINITY, mn = 0.0f, pv[2][8], sum = 0.0f;
+    auto softmax = [&](auto masked) {
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
+      for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kl = 16 * tt + 4 * q4 + r;
-        const float v = (k0 + kl <= q0 + qry && kl < nk) ? st[tt][r] * sl : -INFINITY;
-        st[tt][r] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx);
+        for (int r = 0; r < 4; ++r) {
+          const int kl = 16 * tt + 4 * q4 + r;
+          float v = st[tt][r] * sl;
+          if constexpr (decltype(masked)::value) v = (k0 + kl <= q0 + qry && kl < nk) ? v : -INFINITY;
+          st[tt][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mn = fmaxf(m, mx);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float p = __builtin_amdgcn_exp2f(st[tt][r] - mn);
+          if constexpr (decltype(masked)::value) p = (st[tt][r] == -INFINITY) ? 0.0f : p;
+          pv[tt >> 1][4 * (tt & 1) + r] = p;
+          sum += p;
+        }
+    };
+    if (kb < qb)
+      softmax(std::false_type{});
+    else
+      softmax(std::true_type{});
     const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
-    float pv[2][8], sum = 0.0f;
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = (st[tt][r] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(st[tt][r] - mn);
-        pv[tt >> 1][4 * (tt & 1) + r] = p;
-        sum += p;
-      }
     sum += __shfl_xor(sum, 16, 64);
     sum += __shfl_xor(sum, 32, 64);
     l = l * alpha + sum;
@@ -213,6 +241,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
         o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bv, o[j], 0, 0, 0);
         o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bv, o[j], 0, 0, 0);
       }
+    if (kb < qb) {
+      store_block(fk, kv_tile(smem, (kb + 1) & 1, 0), tid);
+      store_block(fv, kv_tile(smem, (kb + 1) & 1, 1), tid);
+    }
   }
   // lse of this lane's query; D of the queries of O's rows 4 q4 + r (normalised by their l)
   if (q4 == 0 && qry < nq) a.lse[(int64_t)h * a.N + E.row0 + q0 + qry] = m / kLog2e + logf(l);
@@ -246,11 +278,7 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
   const AttnEp E = b.e[ei];
   const int g = a.heads / a.kv_heads;
   const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
-  extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Qs = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* dOs = Qs + BLK * PR;                    // [64][PR]
-  float* lse_s = reinterpret_cast<float*>(dOs + BLK * PR);  // [64]
-  float* d_s = lse_s + BLK;                                // [64]
+  extern __shared__ __align__(16) uint8_t smem[];  // two buffers of [Q tile][dO tile][lse][D]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
   const int key = 16 * w + l16;  // this lane's key in the block
@@ -280,15 +308,22 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
       fd = tid < nq ? a.dsum[t] : 0.0f;
     }
   };
+  auto stage = [&](int buf) {
+    store_block(fq, qo_tile(smem, buf, 0), tid);
+    store_block(fo, qo_tile(smem, buf, 1), tid);
+    if (tid < BLK) qo_stats(smem, buf)[tid] = fl, qo_stats(smem, buf)[BLK + tid] = fd;
+  };
   fetch(0);
+  stage(0);
   for (int i = 0; i < steps; ++i) {
     const int q0 = (nqb - 1 - i / g) * BLK;
-    __syncthreads();  // the previous step's reads of the tiles are done
-    store_block(fq, Qs, tid);
-    store_block(fo, dOs, tid);
-    if (tid < BLK) lse_s[tid] = fl, d_s[tid] = fd;
+    // This step's tiles are stored, and every wave is done with the other buffer.
     __syncthreads();
     if (i + 1 < steps) fetch(i + 1);  // the next step's blocks load while this one computes
+    const bf16_t* Qs = qo_tile(smem, i & 1, 0);
+    const bf16_t* dOs = qo_tile(smem, i & 1, 1);
+    const float* lse_s = qo_stats(smem, i & 1);
+    const float* d_s = lse_s + BLK;
     {
       // S[16 t + 4 q4 + r][key] and dP likewise
       f32x4 st[4], dp[4];
@@ -306,21 +341,28 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
           dp[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ao, vf[s4], dp[t], 0, 0, 0);
         }
       // P and dS of this lane's 16 (query, key) pairs, in fragment order: chunk u, slot i is
-      // query 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4
+      // query 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4. A query block after the key
+      // block sees every key, and the key block is then not the last, so it is whole: no mask.
       float pv[2][8], dsv[2][8];
+      auto probs = [&](auto masked) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const f32x4 ls = *reinterpret_cast<const f32x4*>(lse_s + 16 * t + 4 * q4);
-        const f32x4 dd = *reinterpret_cast<const f32x4*>(d_s + 16 * t + 4 * q4);
+        for (int t = 0; t < 4; ++t) {
+          const f32x4 ls = *reinterpret_cast<const f32x4*>(lse_s + 16 * t + 4 * q4);
+          const f32x4 dd = *reinterpret_cast<const f32x4*>(d_s + 16 * t + 4 * q4);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int ql = 16 * t + 4 * q4 + r;
-          const bool ok = (k0 + key <= q0 + ql) && (key < nk);
-          const float p = ok ? __builtin_amdgcn_exp2f(st[t][r] * sl - ls[r]) : 0.0f;
-          pv[t >> 1][4 * (t & 1) + r] = p;
-          dsv[t >> 1][4 * (t & 1) + r] = p * (dp[t][r] - dd[r]);
+          for (int r = 0; r < 4; ++r) {
+            const int ql = 16 * t + 4 * q4 + r;
+            float p = __builtin_amdgcn_exp2f(st[t][r] * sl - ls[r]);
+            if constexpr (decltype(masked)::value) p = (k0 + key <= q0 + ql && key < nk) ? p : 0.0f;
+            pv[t >> 1][4 * (t & 1) + r] = p;
+            dsv[t >> 1][4 * (t & 1) + r] = p * (dp[t][r] - dd[r]);
+          }
         }
-      }
+      };
+      if (q0 > k0)
+        probs(std::false_type{});
+      else
+        probs(std::true_type{});
       bf16x8 ph[2], pl[2], sh[2], slo[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -339,6 +381,7 @@ __global__ __launch_bounds__(256, 2) void attn_dkdv_kernel(AttnArgs a, AttnBatch
           dk[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bq, dk[j], 0, 0, 0);
         }
     }
+    if (i + 1 < steps) stage((i + 1) & 1);
   }
   // D of dV / dK tile j: lane (l16, q4), register r -> key 16 w + 4 q4 + r, column 16 j + l16
 #pragma unroll
@@ -366,9 +409,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
   const AttnEp E = b.e[ei];
   const int kh = h / (a.heads / a.kv_heads);
   const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
-  extern __shared__ __align__(16) uint8_t smem[];
-  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);  // [64][PR]
-  bf16_t* Vs = Ks + BLK * PR;                     // [64][PR]
+  extern __shared__ __align__(16) uint8_t smem[];  // two buffers of [K tile][V tile], [64][PR] each
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
   const int qry = 16 * w + l16;  // this lane's query in the block
@@ -390,13 +431,15 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
     fetch_block(fv, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
   };
   fetch(0);
+  store_block(fk, kv_tile(smem, 0, 0), tid);
+  store_block(fv, kv_tile(smem, 0, 1), tid);
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
-    __syncthreads();  // the previous block's reads of the tiles are done
-    store_block(fk, Ks, tid);
-    store_block(fv, Vs, tid);
+    // This block's tiles are stored, and every wave is done with the other buffer.
     __syncthreads();
     if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
+    const bf16_t* Ks = kv_tile(smem, kb & 1, 0);
+    const bf16_t* Vs = kv_tile(smem, kb & 1, 1);
     // S^T[16 t + 4 q4 + r][query] and dP^T likewise
     f32x4 st[4], dp[4];
 #pragma unroll
@@ -413,17 +456,24 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
         dp[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, of[s4], dp[tt], 0, 0, 0);
       }
     // dS of this lane's query against 16 keys, in fragment order: chunk u, slot i is key
-    // 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4
+    // 32 u + 4 q4 + i (i < 4) or 32 u + 16 + 4 q4 + i - 4. A key block before the query block
+    // is whole and entirely allowed: no mask there.
     float dsv[2][8];
+    auto grad = [&](auto masked) {
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
+      for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int kl = 16 * tt + 4 * q4 + r;
-        const bool ok = (k0 + kl <= q0 + qry) && (kl < nk);
-        const float p = ok ? __builtin_amdgcn_exp2f(st[tt][r] * sl - ls) : 0.0f;
-        dsv[tt >> 1][4 * (tt & 1) + r] = p * (dp[tt][r] - dd);
-      }
+        for (int r = 0; r < 4; ++r) {
+          const int kl = 16 * tt + 4 * q4 + r;
+          float p = __builtin_amdgcn_exp2f(st[tt][r] * sl - ls);
+          if constexpr (decltype(masked)::value) p = (k0 + kl <= q0 + qry && kl < nk) ? p : 0.0f;
+          dsv[tt >> 1][4 * (tt & 1) + r] = p * (dp[tt][r] - dd);
+        }
+    };
+    if (kb < qb)
+      grad(std::false_type{});
+    else
+      grad(std::true_type{});
     bf16x8 sh[2], slo[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) split_frag(dsv[u], sh[u], slo[u]);
@@ -435,6 +485,10 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
         dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sh[u], bk, dq[j], 0, 0, 0);
         dq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(slo[u], bk, dq[j], 0, 0, 0);
       }
+    if (kb < qb) {
+      store_block(fk, kv_tile(smem, (kb + 1) & 1, 0), tid);
+      store_block(fv, kv_tile(smem, (kb + 1) & 1, 1), tid);
+    }
   }
   // D of dQ tile j: lane (l16, q4), register r -> query 16 w + 4 q4 + r, column 16 j + l16
 #pragma unroll
@@ -447,11 +501,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(AttnArgs a, AttnBatch b
   }
 }
 
-size_t attn_lds_bytes(int kernel) {
-  if (kernel == 0) return (size_t)(2 * BLK * PR) * 2;
-  if (kernel == 1) return (size_t)(2 * BLK * PR) * 2 + 2 * BLK * 4;
-  return (size_t)(2 * BLK * PR) * 2;
-}
+size_t attn_lds_bytes(int kernel) { return 2 * (size_t)(kernel == 1 ? kQoBuf : kKvBuf); }
 
 hipError_t launch_attn(int kernel, const AttnArgs& a, const AttnBatch& b, int wgs, hipStream_t s) {
   if (wgs <= 0) return hipSuccess;
