@@ -7,8 +7,8 @@
 // Three kernels, each recomputing S from Q and K on v_mfma_f32_16x16x32_bf16 over 64 x 64
 // blocks, 256 threads (four waves of 16 rows), blocks in the causal order with the longest rows
 // first, the next block's global loads in flight while the current one computes:
-//   attn_fwd_stats_kernel  per (query head, 64-query block): lse and D (online softmax; O kept
-//                          in float32 registers and contracted with dO, never written)
+//   attn_fwd_stats_kernel  per (query head, 64-query block): lse and D (online softmax; D as
+//                          the softmax-weighted sum of dP = dO V^T, so O is never formed)
 //   attn_dkdv_kernel       per (key/value head, 64-key block): dK and dV accumulated in
 //                          registers over every query head of the group and every later query
 //                          block, in a fixed order (no atomics)
@@ -55,7 +55,6 @@ __device__ __forceinline__ float* qo_stats(uint8_t* smem, int buf) {  // lse [64
   return reinterpret_cast<float*>(smem + buf * kQoBuf + 2 * kTileBytes);
 }
 
-__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
 __device__ __forceinline__ bf16_t f2bf(float x) { return (bf16_t)(pack_bf16x2(x, 0.0f) & 0xFFFFu); }
 
 // The block a workgroup works on: episode, head, block index. Workgroups start in launch
@@ -136,12 +135,13 @@ __device__ __forceinline__ bf16x8 trfrag(const bf16_t* R, int c0, int u, int lan
 }
 
 // lse and D = rowsum(dO * O) of one (query head, 64-query block). Wave w owns queries 16 w ..
-// 16 w + 15; their Q fragments stay in registers. Per key block: S^T = K Q^T with the keys on the
-// MFMA rows, so each lane holds 16 scores of its own query and the online softmax of a query
-// is a reduction over the lane's registers and its three partner lanes (lanes l, l + 16, l + 32,
-// l + 48 hold the same query). P then feeds O += P V as the A operand (contraction over the keys
-// in the order the lane holds them) with the B operand from the transposed V tile. O stays in
-// float32 registers, its row 4 q4 + r belonging to query 16 w + 4 q4 + r, and is never written.
+// 16 w + 15; their Q and dO fragments stay in registers. Per key block: S^T = K Q^T and
+// dP^T = V dO^T with the keys on the MFMA rows, so each lane holds 16 scores of its own query and
+// the online softmax of a query is a reduction over the lane's registers and its three partner
+// lanes (lanes l, l + 16, l + 32, l + 48 hold the same query). O = P V is never formed: since
+// O = sum_k P_k V_k, D = sum_k P_k (dO . V_k) = sum_k P_k dP_k, so each lane keeps, beside the
+// running softmax sum, the running sum of p dP over its keys, both rescaled by the same factor
+// when the running max grows; the four partial sums of a query are added at the end.
 __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, AttnBatch b) {
   int ei, h, qb;
   attn_locate(b, a.heads, true, ei, h, qb);
@@ -153,13 +153,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
   const int l16 = lane & 15, q4 = lane >> 4;
   const int qry = 16 * w + l16;
   const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
-  bf16x8 qf[4];
+  bf16x8 qf[4], of[4];
   load_key_frags(qf, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  load_key_frags(of, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
   const float sl = a.scale * kLog2e;
-  float m = -INFINITY, l = 0.0f;  // running max (base 2) and sum of this lane's query
-  f32x4 o[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) o[j] = f32x4{0, 0, 0, 0};
+  // running max (base 2, the same in the query's four lanes), and this lane's running sums of
+  // p and of p dP over its keys
+  float m = -INFINITY, l = 0.0f, dacc = 0.0f;
   u32x4 fk[4], fv[4];
   auto fetch = [&](int kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
@@ -176,20 +176,24 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
     if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
     const bf16_t* Ks = kv_tile(smem, kb & 1, 0);
     const bf16_t* Vs = kv_tile(smem, kb & 1, 1);
-    f32x4 st[4];
+    // S^T[16 tt + 4 q4 + r][query] and dP^T likewise
+    f32x4 st[4], dp[4];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0};
+    for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0}, dp[tt] = f32x4{0, 0, 0, 0};
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4)
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
         const bf16x8 ak = __builtin_bit_cast(
             bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+        const bf16x8 av = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(Vs + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
         st[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[s4], st[tt], 0, 0, 0);
+        dp[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, of[s4], dp[tt], 0, 0, 0);
       }
     // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r.
     // A key block before the query block is whole and entirely allowed: no mask there.
-    float mx = -INFINITY, mn = 0.0f, pv[2][8], sum = 0.0f;
+    float mx = -INFINITY, mn = 0.0f, sum = 0.0f, dsum = 0.0f;
     auto softmax = [&](auto masked) {
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt)
@@ -210,8 +214,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
         for (int r = 0; r < 4; ++r) {
           float p = __builtin_amdgcn_exp2f(st[tt][r] - mn);
           if constexpr (decltype(masked)::value) p = (st[tt][r] == -INFINITY) ? 0.0f : p;
-          pv[tt >> 1][4 * (tt & 1) + r] = p;
           sum += p;
+          dsum += p * dp[tt][r];
         }
     };
     if (kb < qb)
@@ -219,49 +223,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
     else
       softmax(std::true_type{});
     const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
-    sum += __shfl_xor(sum, 16, 64);
-    sum += __shfl_xor(sum, 32, 64);
     l = l * alpha + sum;
+    dacc = dacc * alpha + dsum;
     m = mn;
-    // O row 4 q4 + r is query 16 w + 4 q4 + r: its scale factor lives in lane 16 q4 + 4 q4 + r
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float ar = __shfl(alpha, 16 * q4 + 4 * q4 + r, 64);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) o[j][r] *= ar;
-    }
-    bf16x8 ph[2], pl[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) split_frag(pv[u], ph[u], pl[u]);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const bf16x8 bv = trfrag(Vs, 16 * j, u, lane);
-        o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph[u], bv, o[j], 0, 0, 0);
-        o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[u], bv, o[j], 0, 0, 0);
-      }
     if (kb < qb) {
       store_block(fk, kv_tile(smem, (kb + 1) & 1, 0), tid);
       store_block(fv, kv_tile(smem, (kb + 1) & 1, 1), tid);
     }
   }
-  // lse of this lane's query; D of the queries of O's rows 4 q4 + r (normalised by their l)
-  if (q4 == 0 && qry < nq) a.lse[(int64_t)h * a.N + E.row0 + q0 + qry] = m / kLog2e + logf(l);
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int qi = 16 * w + 4 * q4 + r;
-    const float lr = __shfl(l, 16 * q4 + 4 * q4 + r, 64);
-    const float inv = lr > 0.0f ? 1.0f / lr : 0.0f;
-    float d = 0.0f;
-    if (qi < nq) {
-      const bf16_t* dor = a.dout + ((int64_t)(E.row0 + q0 + qi) * a.heads + h) * DH;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) d += bf2f(dor[16 * j + l16]) * (o[j][r] * inv);
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) d += __shfl_xor(d, off, 64);
-    if (l16 == 0 && qi < nq) a.dsum[(int64_t)h * a.N + E.row0 + q0 + qi] = d;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  dacc += __shfl_xor(dacc, 16, 64);
+  dacc += __shfl_xor(dacc, 32, 64);
+  if (q4 == 0 && qry < nq) {
+    const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qry;
+    a.lse[t] = m / kLog2e + logf(l);
+    a.dsum[t] = dacc / l;
   }
 }
 
