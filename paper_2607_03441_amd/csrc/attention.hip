@@ -15,7 +15,7 @@
 //   attn_dq_kernel         per (query head, 64-query block): dQ over the allowed key blocks
 // The operand that stays in a wave (its 16 queries, or its 16 keys) is held in registers as
 // the B operand of the score products, so each lane ends up with 16 scores of its own row. The
-// probabilities (or dS) of that row then enter the second product (P V, P^T dO, dS^T Q, dS K)
+// probabilities (or dS) of that row then enter the second product (P^T dO, dS^T Q, dS K)
 // directly as the A operand: the contraction index is the one the lane's registers run over,
 // in the order they hold it, and the B operand is read in the same order from the row-major LDS
 // tile with transposing reads (ds_read_tr16_b64). Every block goes to LDS once, row-major, with
