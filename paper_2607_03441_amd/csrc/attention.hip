@@ -4,10 +4,11 @@
 // accumulation. With S = scale Q K^T, P = softmax(S) over the allowed keys, O = P V:
 //   D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
 //   dQ = scale dS K,  dK = scale dS^T Q,  dV = P^T dO.
-// Three kernels, each recomputing S from Q and K on v_mfma_f32_16x16x32_bf16 over 64 x 64
-// blocks, 256 threads (four waves of 16 rows), blocks in the causal order with the longest rows
-// first, the next block's global loads in flight while the current one computes:
-//   attn_fwd_stats_kernel  per (query head, 64-query block): lse and D (online softmax; D as
+// Three kernels, each recomputing S from Q and K on v_mfma_f32_16x16x32_bf16 over blocks of 64
+// keys, 256 threads (four waves of 16 rows; 32 query rows in the statistics kernel), blocks in
+// the causal order with the longest rows first, the next block's global loads in flight while
+// the current one computes:
+//   attn_fwd_stats_kernel  per (query head, 128-query block): lse and D (online softmax; D as
 //                          the softmax-weighted sum of dP = dO V^T, so O is never formed)
 //   attn_dkdv_kernel       per (key/value head, 64-key block): dK and dV accumulated in
 //                          registers over every query head of the group and every later query
@@ -35,6 +36,7 @@ namespace attt {
 namespace {
 constexpr int DH = 128;     // head dimension
 constexpr int BLK = 64;     // query / key rows per block
+constexpr int SBLK = 128;   // query rows per block of the statistics kernel
 constexpr int PR = DH + 8;  // LDS pitch of a [64][128] tile (bf16): 272 B, conflict-free b128 reads
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -134,11 +136,12 @@ __device__ __forceinline__ bf16x8 trfrag(const bf16_t* R, int c0, int u, int lan
   return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
 }
 
-// lse and D = rowsum(dO * O) of one (query head, 64-query block). Wave w owns queries 16 w ..
-// 16 w + 15; their Q and dO fragments stay in registers. Per key block: S^T = K Q^T and
-// dP^T = V dO^T with the keys on the MFMA rows, so each lane holds 16 scores of its own query and
-// the online softmax of a query is a reduction over the lane's registers and its three partner
-// lanes (lanes l, l + 16, l + 32, l + 48 hold the same query). O = P V is never formed: since
+// lse and D = rowsum(dO * O) of one (query head, 128-query block). Wave w owns queries 32 w ..
+// 32 w + 31 as two tiles of 16; their Q and dO fragments stay in registers. Per key block: S^T =
+// K Q^T and dP^T = V dO^T with the keys on the MFMA rows, each K and V fragment read from LDS once
+// for both tiles, so each lane holds 16 scores of each of its two queries and the online softmax
+// of a query is a reduction over the lane's registers and its three partner lanes (lanes l,
+// l + 16, l + 32, l + 48 hold the same queries). O = P V is never formed: since
 // O = sum_k P_k V_k, D = sum_k P_k (dO . V_k) = sum_k P_k dP_k, so each lane keeps, beside the
 // running softmax sum, the running sum of p dP over its keys, both rescaled by the same factor
 // when the running max grows; the four partial sums of a query are added at the end.
@@ -147,98 +150,129 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_stats_kernel(AttnArgs a, Attn
   attn_locate(b, a.heads, true, ei, h, qb);
   const AttnEp E = b.e[ei];
   const int kh = h / (a.heads / a.kv_heads);
-  const int q0 = qb * BLK, nq = min(BLK, E.L - q0);
+  const int q0 = qb * SBLK, nq = min(SBLK, E.L - q0);
   extern __shared__ __align__(16) uint8_t smem[];  // two buffers of [K tile][V tile], [64][PR] each
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4;
-  const int qry = 16 * w + l16;
   const int64_t qs = (int64_t)a.heads * DH, ks = (int64_t)a.kv_heads * DH;
-  bf16x8 qf[4], of[4];
-  load_key_frags(qf, a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
-  load_key_frags(of, a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  bf16x8 qf[2][4], of[2][4];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int qry = 32 * w + 16 * c + l16;
+    load_key_frags(qf[c], a.q + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+    load_key_frags(of[c], a.dout + ((int64_t)(E.row0 + q0) * a.heads + h) * DH, qs, qry, nq, q4);
+  }
   const float sl = a.scale * kLog2e;
-  // running max (base 2, the same in the query's four lanes), and this lane's running sums of
-  // p and of p dP over its keys
-  float m = -INFINITY, l = 0.0f, dacc = 0.0f;
+  // per query tile: running max (base 2, the same in the query's four lanes), and this lane's
+  // running sums of p and of p dP over its keys
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.0f, 0.0f}, dacc[2] = {0.0f, 0.0f};
   u32x4 fk[4], fv[4];
   auto fetch = [&](int kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
     fetch_block(fk, a.k + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
     fetch_block(fv, a.v + ((int64_t)(E.row0 + k0) * a.kv_heads + kh) * DH, ks, nk, tid);
   };
+  const int kb_last = (q0 + nq - 1) / BLK;  // the key block of the block's last query
+  const int wq0 = q0 + 32 * w;              // this wave's first query
   fetch(0);
   store_block(fk, kv_tile(smem, 0, 0), tid);
   store_block(fv, kv_tile(smem, 0, 1), tid);
-  for (int kb = 0; kb <= qb; ++kb) {
+  for (int kb = 0; kb <= kb_last; ++kb) {
     const int k0 = kb * BLK, nk = min(BLK, E.L - k0);
     // This block's tiles are stored, and every wave is done with the other buffer.
     __syncthreads();
-    if (kb < qb) fetch(kb + 1);  // the next key block loads while this one computes
-    const bf16_t* Ks = kv_tile(smem, kb & 1, 0);
-    const bf16_t* Vs = kv_tile(smem, kb & 1, 1);
-    // S^T[16 tt + 4 q4 + r][query] and dP^T likewise
-    f32x4 st[4], dp[4];
+    if (kb < kb_last) fetch(kb + 1);  // the next key block loads while this one computes
+    // A wave whose queries all precede the block has nothing to add (it still takes part in
+    // the barriers and the stores).
+    if (k0 <= wq0 + 31) {
+      const bf16_t* Ks = kv_tile(smem, kb & 1, 0);
+      const bf16_t* Vs = kv_tile(smem, kb & 1, 1);
+      // S^T[16 tt + 4 q4 + r][query] and dP^T likewise, for both query tiles
+      f32x4 st[2][4], dp[2][4];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) st[tt] = f32x4{0, 0, 0, 0}, dp[tt] = f32x4{0, 0, 0, 0};
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4)
+        for (int tt = 0; tt < 4; ++tt) st[c][tt] = f32x4{0, 0, 0, 0}, dp[c][tt] = f32x4{0, 0, 0, 0};
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        const bf16x8 ak = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
-        const bf16x8 av = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(Vs + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
-        st[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[s4], st[tt], 0, 0, 0);
-        dp[tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, of[s4], dp[tt], 0, 0, 0);
+      for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+          const bf16x8 ak = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(Ks + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+          const bf16x8 av = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(Vs + (16 * tt + l16) * PR + 32 * s4 + 8 * q4));
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            st[c][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, qf[c][s4], st[c][tt], 0, 0, 0);
+            dp[c][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, of[c][s4], dp[c][tt], 0, 0, 0);
+          }
+        }
+      // each K and V fragment pair is read just ahead of its four products, which bounds the
+      // registers held by reads in flight
+#pragma unroll
+      for (int n = 0; n < 16; ++n) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
       }
-    // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r.
-    // A key block before the query block is whole and entirely allowed: no mask there.
-    float mx = -INFINITY, mn = 0.0f, sum = 0.0f, dsum = 0.0f;
-    auto softmax = [&](auto masked) {
+      // online softmax (base-2 exponent of scale * S) over this block's keys 16 tt + 4 q4 + r.
+      // A whole key block that ends at or before the wave's first query is entirely allowed:
+      // no mask there.
+      auto softmax = [&](auto masked) {
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
+        for (int c = 0; c < 2; ++c) {
+          const int qry = 32 * w + 16 * c + l16;
+          float mx = -INFINITY, sum = 0.0f, dsum = 0.0f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kl = 16 * tt + 4 * q4 + r;
-          float v = st[tt][r] * sl;
-          if constexpr (decltype(masked)::value) v = (k0 + kl <= q0 + qry && kl < nk) ? v : -INFINITY;
-          st[tt][r] = v;
-          mx = fmaxf(mx, v);
+          for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int kl = 16 * tt + 4 * q4 + r;
+              float v = st[c][tt][r] * sl;
+              if constexpr (decltype(masked)::value) v = (k0 + kl <= q0 + qry && kl < nk) ? v : -INFINITY;
+              st[c][tt][r] = v;
+              mx = fmaxf(mx, v);
+            }
+          mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+          const float mn = fmaxf(m[c], mx);
+#pragma unroll
+          for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              float p = __builtin_amdgcn_exp2f(st[c][tt][r] - mn);
+              if constexpr (decltype(masked)::value) p = (st[c][tt][r] == -INFINITY) ? 0.0f : p;
+              sum += p;
+              dsum += p * dp[c][tt][r];
+            }
+          const float alpha = (m[c] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m[c] - mn);
+          l[c] = l[c] * alpha + sum;
+          dacc[c] = dacc[c] * alpha + dsum;
+          m[c] = mn;
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      mn = fmaxf(m, mx);
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float p = __builtin_amdgcn_exp2f(st[tt][r] - mn);
-          if constexpr (decltype(masked)::value) p = (st[tt][r] == -INFINITY) ? 0.0f : p;
-          sum += p;
-          dsum += p * dp[tt][r];
-        }
-    };
-    if (kb < qb)
-      softmax(std::false_type{});
-    else
-      softmax(std::true_type{});
-    const float alpha = (m == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(m - mn);
-    l = l * alpha + sum;
-    dacc = dacc * alpha + dsum;
-    m = mn;
-    if (kb < qb) {
+      };
+      if (k0 + BLK - 1 <= wq0 && nk == BLK)
+        softmax(std::false_type{});
+      else
+        softmax(std::true_type{});
+    }
+    if (kb < kb_last) {
       store_block(fk, kv_tile(smem, (kb + 1) & 1, 0), tid);
       store_block(fv, kv_tile(smem, (kb + 1) & 1, 1), tid);
     }
   }
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  dacc += __shfl_xor(dacc, 16, 64);
-  dacc += __shfl_xor(dacc, 32, 64);
-  if (q4 == 0 && qry < nq) {
-    const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qry;
-    a.lse[t] = m / kLog2e + logf(l);
-    a.dsum[t] = dacc / l;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int qry = 32 * w + 16 * c + l16;
+    float lc = l[c], dc = dacc[c];
+    lc += __shfl_xor(lc, 16, 64);
+    lc += __shfl_xor(lc, 32, 64);
+    dc += __shfl_xor(dc, 16, 64);
+    dc += __shfl_xor(dc, 32, 64);
+    if (q4 == 0 && qry < nq) {
+      const int64_t t = (int64_t)h * a.N + E.row0 + q0 + qry;
+      a.lse[t] = m[c] / kLog2e + logf(lc);
+      a.dsum[t] = dc / lc;
+    }
   }
 }
 
@@ -491,7 +525,17 @@ hipError_t launch_attn(int kernel, const AttnArgs& a, const AttnBatch& b, int wg
     attr[kernel] = true;
   }
   KernelTimer t(kernel == 0 ? K_ATTN_FWD : kernel == 1 ? K_ATTN_DKDV : K_ATTN_DQ, s);
-  if (kernel == 0) hipLaunchKernelGGL(attn_fwd_stats_kernel, dim3(wgs), dim3(256), lds, s, a, b);
+  if (kernel == 0) {
+    // the statistics kernel works on 128-query blocks: its own block counts and grid
+    AttnBatch b2 = b;
+    int n = 0;
+    for (int i = 0; i < b2.count; ++i) {
+      b2.e[i].blocks = (b2.e[i].L + SBLK - 1) / SBLK;
+      b2.e[i].wg_begin = n;
+      n += b2.e[i].blocks * a.heads;
+    }
+    if (n > 0) hipLaunchKernelGGL(attn_fwd_stats_kernel, dim3(n), dim3(256), lds, s, a, b2);
+  }
   if (kernel == 1) hipLaunchKernelGGL(attn_dkdv_kernel, dim3(wgs), dim3(256), lds, s, a, b);
   if (kernel == 2) hipLaunchKernelGGL(attn_dq_kernel, dim3(wgs), dim3(256), lds, s, a, b);
   return hipGetLastError();
